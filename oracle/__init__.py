@@ -1,0 +1,179 @@
+"""Plain fp64 CPU oracle for the Hidden Decoding hot path -- TEST INFRASTRUCTURE.
+
+Only the tests, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
+``bench.py`` may import this package.  The product path (the HIP library and its
+Python binding) never imports, links or calls it.
+
+The arithmetic lives in ``sfa_oracle.c`` (fp64, explicit mask from the paper's
+definitions: eq. (expansion), eq. (indices), eq. (mask_intra) and the causal mask of
+Fig. "masks"(a)).  This module only marshals numpy arrays through ctypes and
+builds the shared object with gcc.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "sfa_oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+INTRA, MIX = 0, 1
+_F64, _F32, _BF16 = 0, 1, 2
+
+_lib = None
+
+
+def build() -> str:
+    """Compile sfa_oracle.c into liboracle.so (plain gcc, no fast-math)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-Wall", "-fPIC", "-shared", "-pthread",
+           "-o", _LIB + ".tmp", _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        build()
+    lib = ctypes.CDLL(_LIB)
+    i64, vp, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    dbl = ctypes.c_double
+    dims = [i64] * 6 + [i32, dbl, i32]  # B L n Hq Hkv D mode scale nthreads
+    lib.oracle_sfa_fwd.argtypes = [vp, vp, vp, i32, vp, vp] + dims
+    lib.oracle_sfa_fwd_rows.argtypes = [vp, vp, vp, i32, vp, i64, vp, vp] + dims
+    lib.oracle_sfa_bwd.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp] + dims
+    lib.oracle_sfa_bwd_dq_rows.argtypes = [vp, vp, vp, vp, i32, vp, i64, vp] + dims
+    lib.oracle_sfa_bwd_dkdv_rows.argtypes = [vp, vp, vp, vp, i32, vp, i64, vp, vp] + dims
+    for f in (lib.oracle_sfa_fwd, lib.oracle_sfa_fwd_rows, lib.oracle_sfa_bwd,
+              lib.oracle_sfa_bwd_dq_rows, lib.oracle_sfa_bwd_dkdv_rows):
+        f.restype = None
+    lib.oracle_expand_embed.argtypes = [vp, vp, vp, i64, i64, i64, i64, i64, i64]
+    lib.oracle_expand_embed.restype = i64
+    lib.oracle_sfa_mask.argtypes = [vp, i64, i64, i32]
+    lib.oracle_sfa_mask.restype = None
+    _lib = lib
+    return lib
+
+
+def default_threads() -> int:
+    return max(1, min(16, os.cpu_count() or 1))
+
+
+def _dtype_code(a: np.ndarray) -> int:
+    if a.dtype == np.float64:
+        return _F64
+    if a.dtype == np.float32:
+        return _F32
+    if a.dtype == np.uint16:  # bf16 bit patterns
+        return _BF16
+    raise TypeError(f"oracle inputs must be float64, float32 or uint16 (bf16 bits), got {a.dtype}")
+
+
+def _prep(*arrays):
+    out = [np.ascontiguousarray(a) for a in arrays]
+    code = _dtype_code(out[0])
+    for a in out[1:]:
+        if _dtype_code(a) != code:
+            raise TypeError("oracle inputs must share one dtype")
+    return out, code
+
+
+def _ptr(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _dims(q, k, B, L, n, mode, scale, nthreads):
+    N = n * L
+    if q.shape[:2] != (B, N) or k.shape[:2] != (B, N) or q.shape[3] != k.shape[3]:
+        raise ValueError("q must be [B][n*L][Hq][D] and k/v [B][n*L][Hkv][D]")
+    Hq, D, Hkv = q.shape[2], q.shape[3], k.shape[2]
+    if Hq % Hkv:
+        raise ValueError("Hq must be a multiple of Hkv")
+    return (B, L, n, Hq, Hkv, D, int(mode), float(scale),
+            int(nthreads or default_threads())), Hq, Hkv, D
+
+
+def sfa_fwd(q, k, v, *, L, n, mode, scale, nthreads=None):
+    """Full forward. Returns (o [B][N][Hq][D], lse [B][Hq][N]) in float64."""
+    (q, k, v), code = _prep(q, k, v)
+    B = q.shape[0]
+    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads)
+    o = np.zeros((B, n * L, Hq, D))
+    lse = np.zeros((B, Hq, n * L))
+    _load().oracle_sfa_fwd(_ptr(q), _ptr(k), _ptr(v), code, _ptr(o), _ptr(lse), *dims)
+    return o, lse
+
+
+def sfa_fwd_rows(q, k, v, rows, *, L, n, mode, scale, nthreads=None):
+    """Forward of listed rows; rows is int64 [R][3] of (b, hq, p)."""
+    (q, k, v), code = _prep(q, k, v)
+    rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
+    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads)
+    o = np.zeros((len(rows), D))
+    lse = np.zeros(len(rows))
+    _load().oracle_sfa_fwd_rows(_ptr(q), _ptr(k), _ptr(v), code, _ptr(rows), len(rows),
+                                _ptr(o), _ptr(lse), *dims)
+    return o, lse
+
+
+def sfa_bwd(q, k, v, dout, *, L, n, mode, scale, nthreads=None):
+    """Full backward from (q, k, v, dO). Returns (dq, dk, dv) in float64."""
+    (q, k, v, dout), code = _prep(q, k, v, dout)
+    B = q.shape[0]
+    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads)
+    dq = np.zeros((B, n * L, Hq, D))
+    dk = np.zeros((B, n * L, Hkv, D))
+    dv = np.zeros((B, n * L, Hkv, D))
+    _load().oracle_sfa_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), code, _ptr(dq), _ptr(dk),
+                           _ptr(dv), *dims)
+    return dq, dk, dv
+
+
+def sfa_bwd_dq_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None):
+    """dQ of listed query rows (b, hq, p)."""
+    (q, k, v, dout), code = _prep(q, k, v, dout)
+    rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
+    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads)
+    dq = np.zeros((len(rows), D))
+    _load().oracle_sfa_bwd_dq_rows(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), code, _ptr(rows),
+                                   len(rows), _ptr(dq), *dims)
+    return dq
+
+
+def sfa_bwd_dkdv_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None):
+    """dK, dV of listed key rows (b, hk, j), summed over the group's query heads."""
+    (q, k, v, dout), code = _prep(q, k, v, dout)
+    rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
+    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads)
+    dk = np.zeros((len(rows), D))
+    dv = np.zeros((len(rows), D))
+    _load().oracle_sfa_bwd_dkdv_rows(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), code, _ptr(rows),
+                                     len(rows), _ptr(dk), _ptr(dv), *dims)
+    return dk, dv
+
+
+def expand_embed(ids, tables):
+    """eq. (expansion): ids [B][L] int32, tables [n][V][Dm] (any dtype) -> (out, bad)."""
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    tables = np.ascontiguousarray(tables)
+    B, L = ids.shape
+    n, V, Dm = tables.shape
+    out = np.empty((B, n * L, Dm), dtype=tables.dtype)
+    bad = _load().oracle_expand_embed(_ptr(ids), _ptr(tables), _ptr(out), B, L, n, V, Dm,
+                                      tables.dtype.itemsize)
+    return out, int(bad)
+
+
+def sfa_mask(L, n, mode):
+    """Explicit [N][N] 0/1 mask straight from the definitions."""
+    N = n * L
+    m = np.zeros((N, N), dtype=np.uint8)
+    _load().oracle_sfa_mask(_ptr(m), L, n, int(mode))
+    return m

@@ -1,0 +1,421 @@
+/*
+ * sfa_oracle.c -- plain fp64 CPU oracle for the Hidden Decoding hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing on the product path may call, link or load
+ * this file; it exists so that tests, the smoke check and the CPU-baseline leg of
+ * the benchmark can compare the HIP kernels against an obviously correct,
+ * independently written reference.  It shares no code, header or constant with
+ * the HIP library.
+ *
+ * What it computes (paper: "Hidden Decoding at Scale", Sec. 2 "Method"):
+ *   - multi-stream token expansion, eq. (expansion): expanded position of stream k
+ *     of token i holds E_k(x_i); 0-based here: row p = t*n + s holds tables[s][ids[t]];
+ *   - token/stream index maps, eq. (indices), 0-based: t(p) = p / n, s(p) = p % n;
+ *   - intra-stream attention mask, eq. (mask_intra): key p' visible from query p
+ *     iff s(p') == s(p) and p' <= p (equivalently t(p') <= t(p));
+ *   - full cross-stream ("mixing") mask, Fig. "masks" (a): the standard causal mask
+ *     over the expanded sequence, written here in token/stream form:
+ *     t(p') < t(p), or t(p') == t(p) and s(p') <= s(p);
+ *   - softmax attention under that mask, its log-sum-exp, and the analytic
+ *     gradients with respect to q, k and v (standard softmax-attention calculus:
+ *     dP = dO v^T, Delta = dO . O, dS = P (dP - Delta), dQ = scale dS K,
+ *     dK = scale dS^T Q, dV = P^T dO; grouped-query heads sum dK/dV over the
+ *     query heads that share a key/value head).
+ *
+ * Everything is fp64.  Inputs may be given as fp64, fp32 or bf16 bit patterns and
+ * are upcast exactly.  The mask is evaluated from its definition for every
+ * (query, key) pair; only visible pairs contribute.  No blocking, no online
+ * softmax, no reordering beyond the plain definitions above.
+ *
+ * Layouts (row-major, 0-based):
+ *   q, o, dO, dq : [B][N][Hq][D]     k, v, dk, dv : [B][N][Hkv][D]
+ *   lse          : [B][Hq][N] (natural log)        N = n * L
+ *   query head hq uses key/value head hq / (Hq / Hkv).
+ *
+ * Every function here is pinned by tests (closed forms, library reductions,
+ * invariants and finite differences); none is "parity unpinned".
+ */
+#include <math.h>
+#include <pthread.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+enum { ORC_INTRA = 0, ORC_MIX = 1 };
+enum { ORC_F64 = 0, ORC_F32 = 1, ORC_BF16 = 2 };
+
+/* ---------------------------------------------------------------- inputs */
+
+typedef struct {
+    const void *q, *k, *v, *dout;
+    int dtype;
+    int64_t B, L, n, Hq, Hkv, D;
+    int mode;
+    double scale;
+} problem_t;
+
+static double load_elem(const void *base, int dtype, int64_t idx)
+{
+    if (dtype == ORC_F64) return ((const double *)base)[idx];
+    if (dtype == ORC_F32) return (double)((const float *)base)[idx];
+    /* bf16: the 16 stored bits are the top half of an fp32 */
+    uint32_t bits = ((uint32_t)((const uint16_t *)base)[idx]) << 16;
+    float f;
+    memcpy(&f, &bits, sizeof f);
+    return (double)f;
+}
+
+/* ------------------------------------------------- index maps and masks */
+
+/* eq. (indices), 0-based: token and stream of expanded position p */
+static int64_t token_of(int64_t p, int64_t n) { return p / n; }
+static int64_t stream_of(int64_t p, int64_t n) { return p % n; }
+
+/* 1 if key position pk is visible from query position pq */
+static int visible(int mode, int64_t n, int64_t pq, int64_t pk)
+{
+    int64_t t = token_of(pq, n), s = stream_of(pq, n);
+    int64_t tk = token_of(pk, n), sk = stream_of(pk, n);
+    if (mode == ORC_INTRA) /* eq. (mask_intra): same stream, not later */
+        return sk == s && pk <= pq;
+    /* full cross-stream layer: causal over the expanded sequence */
+    return tk < t || (tk == t && sk <= s);
+}
+
+static int64_t q_index(const problem_t *P, int64_t b, int64_t p, int64_t h, int64_t d)
+{
+    return ((b * (P->n * P->L) + p) * P->Hq + h) * P->D + d;
+}
+
+static int64_t kv_index(const problem_t *P, int64_t b, int64_t p, int64_t h, int64_t d)
+{
+    return ((b * (P->n * P->L) + p) * P->Hkv + h) * P->D + d;
+}
+
+/* ------------------------------------------------------- one query row */
+
+/*
+ * Forward of one query row (b, hq, p).  x (length N) is caller scratch; on return
+ * x[j] holds the probability P_pj for visible j and 0 otherwise.  o gets D values.
+ */
+static void row_forward(const problem_t *P, int64_t b, int64_t hq, int64_t p,
+                        double *x, double *o, double *lse)
+{
+    const int64_t N = P->n * P->L, D = P->D;
+    const int64_t hk = hq / (P->Hq / P->Hkv);
+    double m = -INFINITY;
+    for (int64_t j = 0; j < N; ++j) {
+        if (!visible(P->mode, P->n, p, j)) { x[j] = -INFINITY; continue; }
+        double dot = 0.0;
+        for (int64_t d = 0; d < D; ++d)
+            dot += load_elem(P->q, P->dtype, q_index(P, b, p, hq, d)) *
+                   load_elem(P->k, P->dtype, kv_index(P, b, j, hk, d));
+        x[j] = P->scale * dot;
+        if (x[j] > m) m = x[j];
+    }
+    double l = 0.0;
+    for (int64_t j = 0; j < N; ++j)
+        if (x[j] != -INFINITY) l += exp(x[j] - m);
+    for (int64_t j = 0; j < N; ++j)
+        x[j] = (x[j] == -INFINITY) ? 0.0 : exp(x[j] - m) / l;
+    for (int64_t d = 0; d < D; ++d) o[d] = 0.0;
+    for (int64_t j = 0; j < N; ++j) {
+        if (!visible(P->mode, P->n, p, j)) continue;
+        for (int64_t d = 0; d < D; ++d)
+            o[d] += x[j] * load_elem(P->v, P->dtype, kv_index(P, b, j, hk, d));
+    }
+    *lse = m + log(l);
+}
+
+/*
+ * Backward of one query row.  Needs the row's probabilities (x from row_forward)
+ * and its exact output o.  Writes dq (D values, may be NULL) and, when dk/dv are
+ * non-NULL, adds this row's contributions into dk/dv rows laid out [N][D] for the
+ * key/value head of hq (caller owns the per-head accumulation).
+ */
+static void row_backward(const problem_t *P, int64_t b, int64_t hq, int64_t p,
+                         const double *x, const double *o, double *dq,
+                         double *dk_head, double *dv_head, const int64_t *only_key,
+                         int64_t n_only)
+{
+    const int64_t N = P->n * P->L, D = P->D;
+    const int64_t hk = hq / (P->Hq / P->Hkv);
+    double delta = 0.0; /* Delta_p = dO_p . O_p */
+    for (int64_t d = 0; d < D; ++d)
+        delta += load_elem(P->dout, P->dtype, q_index(P, b, p, hq, d)) * o[d];
+    if (dq)
+        for (int64_t d = 0; d < D; ++d) dq[d] = 0.0;
+    for (int64_t j = 0; j < N; ++j) {
+        if (!visible(P->mode, P->n, p, j)) continue;
+        int64_t slot = j;
+        if (only_key) { /* restrict dk/dv accumulation to listed keys */
+            slot = -1;
+            for (int64_t r = 0; r < n_only; ++r)
+                if (only_key[r] == j) { slot = r; break; }
+            if (slot < 0 && !dq) continue;
+        }
+        double dp = 0.0; /* dP_pj = dO_p . v_j */
+        for (int64_t d = 0; d < D; ++d)
+            dp += load_elem(P->dout, P->dtype, q_index(P, b, p, hq, d)) *
+                  load_elem(P->v, P->dtype, kv_index(P, b, j, hk, d));
+        double ds = x[j] * (dp - delta); /* dS_pj */
+        if (dq)
+            for (int64_t d = 0; d < D; ++d)
+                dq[d] += P->scale * ds * load_elem(P->k, P->dtype, kv_index(P, b, j, hk, d));
+        if (dk_head && slot >= 0)
+            for (int64_t d = 0; d < D; ++d) {
+                dk_head[slot * D + d] +=
+                    P->scale * ds * load_elem(P->q, P->dtype, q_index(P, b, p, hq, d));
+                dv_head[slot * D + d] +=
+                    x[j] * load_elem(P->dout, P->dtype, q_index(P, b, p, hq, d));
+            }
+    }
+}
+
+/* ---------------------------------------------------------- threading */
+
+typedef struct {
+    const problem_t *P;
+    int64_t first, count; /* work units */
+    void *out[6];
+    const int64_t *rows;
+    int64_t nrows;
+} job_t;
+
+typedef void *(*job_fn)(void *);
+
+static void run_jobs(job_fn fn, job_t *tmpl, int64_t units, int nthreads)
+{
+    if (nthreads < 1) nthreads = 1;
+    if (nthreads > units) nthreads = (int)(units > 0 ? units : 1);
+    pthread_t *th = calloc((size_t)nthreads, sizeof *th);
+    job_t *jobs = calloc((size_t)nthreads, sizeof *jobs);
+    int64_t per = units / nthreads, extra = units % nthreads, at = 0;
+    for (int i = 0; i < nthreads; ++i) {
+        jobs[i] = *tmpl;
+        jobs[i].first = at;
+        jobs[i].count = per + (i < extra ? 1 : 0);
+        at += jobs[i].count;
+    }
+    for (int i = 1; i < nthreads; ++i) pthread_create(&th[i], NULL, fn, &jobs[i]);
+    fn(&jobs[0]);
+    for (int i = 1; i < nthreads; ++i) pthread_join(th[i], NULL);
+    free(th);
+    free(jobs);
+}
+
+/* ------------------------------------------------------------ forward */
+
+/* unit = one (b, hq) head; all N rows */
+static void *fwd_job(void *arg)
+{
+    job_t *J = arg;
+    const problem_t *P = J->P;
+    const int64_t N = P->n * P->L;
+    double *o = J->out[0], *lse = J->out[1];
+    double *x = malloc((size_t)N * sizeof *x);
+    for (int64_t u = J->first; u < J->first + J->count; ++u) {
+        int64_t b = u / P->Hq, hq = u % P->Hq;
+        for (int64_t p = 0; p < N; ++p)
+            row_forward(P, b, hq, p, x, &o[q_index(P, b, p, hq, 0)],
+                        &lse[(b * P->Hq + hq) * N + p]);
+    }
+    free(x);
+    return NULL;
+}
+
+static problem_t make_problem(const void *q, const void *k, const void *v, const void *dout,
+                              int dtype, int64_t B, int64_t L, int64_t n, int64_t Hq,
+                              int64_t Hkv, int64_t D, int mode, double scale)
+{
+    problem_t P = {q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, scale};
+    return P;
+}
+
+/* Full forward: o [B][N][Hq][D], lse [B][Hq][N]. */
+void oracle_sfa_fwd(const void *q, const void *k, const void *v, int dtype, double *o,
+                    double *lse, int64_t B, int64_t L, int64_t n, int64_t Hq, int64_t Hkv,
+                    int64_t D, int mode, double scale, int nthreads)
+{
+    problem_t P = make_problem(q, k, v, NULL, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    job_t J = {&P, 0, 0, {o, lse}, NULL, 0};
+    run_jobs(fwd_job, &J, B * Hq, nthreads);
+}
+
+/* unit = one listed row (b, hq, p) */
+static void *fwd_rows_job(void *arg)
+{
+    job_t *J = arg;
+    const problem_t *P = J->P;
+    const int64_t N = P->n * P->L, D = P->D;
+    double *o = J->out[0], *lse = J->out[1];
+    double *x = malloc((size_t)N * sizeof *x);
+    for (int64_t r = J->first; r < J->first + J->count; ++r) {
+        const int64_t *row = &J->rows[3 * r];
+        row_forward(P, row[0], row[1], row[2], x, &o[r * D], &lse[r]);
+    }
+    free(x);
+    return NULL;
+}
+
+/* Forward of selected rows: rows = nrows triplets (b, hq, p); o_rows [nrows][D]. */
+void oracle_sfa_fwd_rows(const void *q, const void *k, const void *v, int dtype,
+                         const int64_t *rows, int64_t nrows, double *o_rows,
+                         double *lse_rows, int64_t B, int64_t L, int64_t n, int64_t Hq,
+                         int64_t Hkv, int64_t D, int mode, double scale, int nthreads)
+{
+    problem_t P = make_problem(q, k, v, NULL, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    job_t J = {&P, 0, 0, {o_rows, lse_rows}, rows, nrows};
+    run_jobs(fwd_rows_job, &J, nrows, nthreads);
+}
+
+/* ----------------------------------------------------------- backward */
+
+/* unit = one (b, hk) key/value head: all query heads of its group, all rows */
+static void *bwd_job(void *arg)
+{
+    job_t *J = arg;
+    const problem_t *P = J->P;
+    const int64_t N = P->n * P->L, D = P->D, G = P->Hq / P->Hkv;
+    double *dq = J->out[0], *dk = J->out[1], *dv = J->out[2];
+    double *x = malloc((size_t)N * sizeof *x);
+    double *o = malloc((size_t)D * sizeof *o);
+    double *dk_head = malloc((size_t)(N * D) * sizeof *dk_head);
+    double *dv_head = malloc((size_t)(N * D) * sizeof *dv_head);
+    for (int64_t u = J->first; u < J->first + J->count; ++u) {
+        int64_t b = u / P->Hkv, hk = u % P->Hkv;
+        memset(dk_head, 0, (size_t)(N * D) * sizeof *dk_head);
+        memset(dv_head, 0, (size_t)(N * D) * sizeof *dv_head);
+        for (int64_t hq = hk * G; hq < (hk + 1) * G; ++hq)
+            for (int64_t p = 0; p < N; ++p) {
+                double lse;
+                row_forward(P, b, hq, p, x, o, &lse);
+                row_backward(P, b, hq, p, x, o, &dq[q_index(P, b, p, hq, 0)], dk_head,
+                             dv_head, NULL, 0);
+            }
+        for (int64_t j = 0; j < N; ++j)
+            for (int64_t d = 0; d < D; ++d) {
+                dk[kv_index(P, b, j, hk, d)] = dk_head[j * D + d];
+                dv[kv_index(P, b, j, hk, d)] = dv_head[j * D + d];
+            }
+    }
+    free(x);
+    free(o);
+    free(dk_head);
+    free(dv_head);
+    return NULL;
+}
+
+/* Full backward from (q, k, v, dO): dq [B][N][Hq][D], dk/dv [B][N][Hkv][D]. */
+void oracle_sfa_bwd(const void *q, const void *k, const void *v, const void *dout, int dtype,
+                    double *dq, double *dk, double *dv, int64_t B, int64_t L, int64_t n,
+                    int64_t Hq, int64_t Hkv, int64_t D, int mode, double scale, int nthreads)
+{
+    problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    job_t J = {&P, 0, 0, {dq, dk, dv}, NULL, 0};
+    run_jobs(bwd_job, &J, B * Hkv, nthreads);
+}
+
+/* unit = one listed query row (b, hq, p) */
+static void *dq_rows_job(void *arg)
+{
+    job_t *J = arg;
+    const problem_t *P = J->P;
+    const int64_t N = P->n * P->L, D = P->D;
+    double *dq = J->out[0];
+    double *x = malloc((size_t)N * sizeof *x);
+    double *o = malloc((size_t)D * sizeof *o);
+    for (int64_t r = J->first; r < J->first + J->count; ++r) {
+        const int64_t *row = &J->rows[3 * r];
+        double lse;
+        row_forward(P, row[0], row[1], row[2], x, o, &lse);
+        row_backward(P, row[0], row[1], row[2], x, o, &dq[r * D], NULL, NULL, NULL, 0);
+    }
+    free(x);
+    free(o);
+    return NULL;
+}
+
+/* dQ of selected query rows (b, hq, p); dq_rows [nrows][D]. */
+void oracle_sfa_bwd_dq_rows(const void *q, const void *k, const void *v, const void *dout,
+                            int dtype, const int64_t *rows, int64_t nrows, double *dq_rows,
+                            int64_t B, int64_t L, int64_t n, int64_t Hq, int64_t Hkv,
+                            int64_t D, int mode, double scale, int nthreads)
+{
+    problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    job_t J = {&P, 0, 0, {dq_rows}, rows, nrows};
+    run_jobs(dq_rows_job, &J, nrows, nthreads);
+}
+
+/* unit = one listed key row (b, hk, j): sum over the group's query heads and rows */
+static void *dkdv_rows_job(void *arg)
+{
+    job_t *J = arg;
+    const problem_t *P = J->P;
+    const int64_t N = P->n * P->L, D = P->D, G = P->Hq / P->Hkv;
+    double *dk = J->out[0], *dv = J->out[1];
+    double *x = malloc((size_t)N * sizeof *x);
+    double *o = malloc((size_t)D * sizeof *o);
+    for (int64_t r = J->first; r < J->first + J->count; ++r) {
+        const int64_t b = J->rows[3 * r], hk = J->rows[3 * r + 1], j = J->rows[3 * r + 2];
+        for (int64_t d = 0; d < D; ++d) dk[r * D + d] = dv[r * D + d] = 0.0;
+        for (int64_t hq = hk * G; hq < (hk + 1) * G; ++hq)
+            for (int64_t p = 0; p < N; ++p) {
+                if (!visible(P->mode, P->n, p, j)) continue;
+                double lse;
+                row_forward(P, b, hq, p, x, o, &lse);
+                row_backward(P, b, hq, p, x, o, NULL, &dk[r * D], &dv[r * D], &j, 1);
+            }
+    }
+    free(x);
+    free(o);
+    return NULL;
+}
+
+/* dK/dV of selected key rows (b, hk, j); dk_rows, dv_rows [nrows][D]. */
+void oracle_sfa_bwd_dkdv_rows(const void *q, const void *k, const void *v, const void *dout,
+                              int dtype, const int64_t *rows, int64_t nrows, double *dk_rows,
+                              double *dv_rows, int64_t B, int64_t L, int64_t n, int64_t Hq,
+                              int64_t Hkv, int64_t D, int mode, double scale, int nthreads)
+{
+    problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    job_t J = {&P, 0, 0, {dk_rows, dv_rows}, rows, nrows};
+    run_jobs(dkdv_rows_job, &J, nrows, nthreads);
+}
+
+/* ---------------------------------------------------- stream expansion */
+
+/*
+ * eq. (expansion), 0-based: out[b][t*n + s][:] = tables[s][ids[b][t]][:].
+ * Element-size agnostic byte copy.  An id outside [0, V) gives n zero rows and
+ * counts once (per token, not per stream); the count is returned.
+ */
+int64_t oracle_expand_embed(const int32_t *ids, const void *tables, void *out, int64_t B,
+                            int64_t L, int64_t n, int64_t V, int64_t Dm, int64_t elem_bytes)
+{
+    int64_t bad = 0;
+    const int64_t row_bytes = Dm * elem_bytes;
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t t = 0; t < L; ++t)
+            for (int64_t s = 0; s < n; ++s) {
+                int64_t p = t * n + s;
+                int64_t id = ids[b * L + t];
+                char *dst = (char *)out + (b * n * L + p) * row_bytes;
+                if (id < 0 || id >= V) {
+                    memset(dst, 0, (size_t)row_bytes);
+                    if (s == 0) ++bad;
+                    continue;
+                }
+                const char *src = (const char *)tables + (s * V + id) * row_bytes;
+                memcpy(dst, src, (size_t)row_bytes);
+            }
+    return bad;
+}
+
+/* Mask as bytes [N][N] straight from the definition (for probes and pins). */
+void oracle_sfa_mask(unsigned char *mask, int64_t L, int64_t n, int mode)
+{
+    const int64_t N = n * L;
+    for (int64_t p = 0; p < N; ++p)
+        for (int64_t j = 0; j < N; ++j) mask[p * N + j] = (unsigned char)visible(mode, n, p, j);
+}

@@ -1,0 +1,93 @@
+"""Named workload shapes and useful-work accounting for the SFA hot path.
+
+Shapes follow the paper's dense Qwen3-8B study (Sec. "Progressive expansion",
+32 query / 8 key-value heads of width 128) and its 617B-like head layout
+(Table "model_config": 96/8 heads, width 128, here one GPU's 64/8 share).
+"""
+from __future__ import annotations
+
+import math
+from dataclasses import dataclass, field
+
+INTRA, MIX = 0, 1
+MODE_NAMES = {INTRA: "intra", MIX: "mix"}
+
+# bf16 dense MFMA peak of one MI355X (256 CU x 2.4 GHz x 4096 flop/clk/CU)
+MI355X_BF16_PEAK_TFLOPS = 2516.6
+MI355X_HBM_PEAK_GBS = 8000.0
+
+
+@dataclass(frozen=True)
+class Shape:
+    B: int
+    L: int
+    n: int
+    Hq: int
+    Hkv: int
+    D: int
+
+    @property
+    def N(self) -> int:
+        return self.n * self.L
+
+    @property
+    def scale(self) -> float:
+        return 1.0 / math.sqrt(self.D)
+
+
+@dataclass(frozen=True)
+class Workload:
+    name: str
+    shape: Shape
+    dtype: str = "bf16"
+    qkv_std: float = 1.0 / math.sqrt(2.0)
+    dout_std: float = 1.0
+    k_spike: tuple | None = None
+    modes: tuple = (INTRA, MIX)
+    extra: dict = field(default_factory=dict)
+
+
+TINY = Workload("tiny-f32-L64-n2", Shape(1, 64, 2, 2, 1, 32), dtype="f32", qkv_std=1.0)
+QWEN8B = Workload("qwen3-8b-like-L4096-n4", Shape(1, 4096, 4, 32, 8, 128))
+SWEEP = tuple(Workload(f"sweep-B2-L2048-n{n}", Shape(2, 2048, n, 32, 8, 128)) for n in (1, 2, 4, 8))
+FRONTIER = Workload("frontier-share-L8192-n4", Shape(1, 8192, 4, 64, 8, 128),
+                    k_spike=(0.01, 8.0))
+
+# 36-layer stack: mixing layers at these indices, intra-stream elsewhere, each layer at
+# the Qwen3-8B-like shape; plus the stream expansion from n tables of V x Dm.
+STACK_LAYERS = 36
+STACK_MIX_LAYERS = (8, 17, 26, 35)
+STACK_VOCAB = 151936
+STACK_DMODEL = 4096
+STACK_EMBED_STD = 0.02
+
+
+def stack_modes():
+    return [MIX if i in STACK_MIX_LAYERS else INTRA for i in range(STACK_LAYERS)]
+
+
+def visible_pairs(s: Shape, mode: int) -> int:
+    """Visible (query, key) pairs summed over batch and query heads."""
+    if mode == INTRA:
+        return s.B * s.Hq * s.n * s.L * (s.L + 1) // 2
+    return s.B * s.Hq * s.N * (s.N + 1) // 2
+
+
+# useful flop per visible pair per head dim: fwd QK^T + PV; bwd recompute QK^T, dV, dP, dQ, dK
+FWD_FLOP_PER_PAIR_D = 4
+BWD_FLOP_PER_PAIR_D = 10
+
+
+def useful_flop(s: Shape, mode: int, phase: str = "fwdbwd") -> int:
+    c = {"fwd": FWD_FLOP_PER_PAIR_D, "bwd": BWD_FLOP_PER_PAIR_D,
+         "fwdbwd": FWD_FLOP_PER_PAIR_D + BWD_FLOP_PER_PAIR_D}[phase]
+    return c * s.D * visible_pairs(s, mode)
+
+
+def stack_useful_flop(s: Shape = QWEN8B.shape) -> int:
+    return sum(useful_flop(s, m) for m in stack_modes())
+
+
+def embed_bytes(B: int, L: int, n: int, Dm: int, esize: int = 2) -> int:
+    """Compulsory traffic of the expansion: read n*L rows, write n*L rows, read ids."""
+    return 2 * B * n * L * Dm * esize + B * L * 4

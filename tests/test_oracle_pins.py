@@ -1,0 +1,357 @@
+"""Pins of the fp64 oracle against facts fixed by the paper and by mathematics.
+
+None of these re-types the oracle's formulas.  Each check uses an independent
+statement of the result: torch's fp64 scaled_dot_product_attention (a library routine)
+on de-interleaved or expanded sequences, closed forms, invariants, hand-written
+golden fixtures and central finite differences.
+"""
+import json
+import math
+import os
+
+import numpy as np
+import pytest
+import torch
+import torch.nn.functional as F
+
+from paper_2607_08186_amd import synth
+
+INTRA, MIX = 0, 1
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _rand(seed, B, L, n, Hq, Hkv, D, std=1.0):
+    N = n * L
+    r = np.random.default_rng(seed)
+    q = r.standard_normal((B, N, Hq, D)) * std
+    k = r.standard_normal((B, N, Hkv, D)) * std
+    v = r.standard_normal((B, N, Hkv, D))
+    do = r.standard_normal((B, N, Hq, D))
+    return q, k, v, do
+
+
+def _torch_causal(q, k, v, do, scale):
+    """Library causal attention on [B][S][H][D] fp64 arrays with GQA by head repeat.
+
+    Returns o [B][S][Hq][D], lse [B][Hq][S], dq, dk, dv (dk/dv summed over groups).
+    """
+    Hq, Hkv = q.shape[2], k.shape[2]
+    G = Hq // Hkv
+    tq = torch.tensor(q).permute(0, 2, 1, 3).contiguous().requires_grad_(True)
+    tk = torch.tensor(k).permute(0, 2, 1, 3).contiguous().requires_grad_(True)
+    tv = torch.tensor(v).permute(0, 2, 1, 3).contiguous().requires_grad_(True)
+    kk = tk.repeat_interleave(G, dim=1)
+    vv = tv.repeat_interleave(G, dim=1)
+    o = F.scaled_dot_product_attention(tq, kk, vv, is_causal=True, scale=scale)
+    o.backward(torch.tensor(do).permute(0, 2, 1, 3))
+    S = q.shape[1]
+    logits = scale * torch.matmul(tq.detach(), kk.detach().transpose(-1, -2))
+    keep = torch.ones(S, S, dtype=torch.bool).tril()
+    lse = torch.logsumexp(logits.masked_fill(~keep, float("-inf")), dim=-1)
+    back = lambda t: t.permute(0, 2, 1, 3).detach().numpy()
+    return back(o), lse.numpy(), back(tq.grad), back(tk.grad), back(tv.grad)
+
+
+def _deinterleave(x, n, s):
+    B, N, H, D = x.shape
+    return x.reshape(B, N // n, n, H, D)[:, :, s]
+
+
+SHAPES = [  # B, L, n, Hq, Hkv, D
+    (1, 7, 3, 2, 1, 4),
+    (2, 5, 2, 4, 2, 8),
+    (1, 6, 4, 3, 3, 5),
+    (1, 9, 1, 2, 2, 6),
+]
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_intra_equals_causal_per_stream(oracle_mod, shape):
+    """INTRA(n) == ordinary causal attention on each de-interleaved stream (fwd + bwd)."""
+    B, L, n, Hq, Hkv, D = shape
+    q, k, v, do = _rand(1, *shape)
+    scale = 1.0 / math.sqrt(D)
+    o, lse = oracle_mod.sfa_fwd(q, k, v, L=L, n=n, mode=INTRA, scale=scale)
+    dq, dk, dv = oracle_mod.sfa_bwd(q, k, v, do, L=L, n=n, mode=INTRA, scale=scale)
+    for s in range(n):
+        ro, rlse, rdq, rdk, rdv = _torch_causal(*(_deinterleave(x, n, s) for x in (q, k, v, do)),
+                                                scale)
+        np.testing.assert_allclose(_deinterleave(o, n, s), ro, atol=1e-12, rtol=0)
+        np.testing.assert_allclose(lse[:, :, s::n], rlse, atol=1e-12, rtol=0)
+        np.testing.assert_allclose(_deinterleave(dq, n, s), rdq, atol=1e-11, rtol=0)
+        np.testing.assert_allclose(_deinterleave(dk, n, s), rdk, atol=1e-11, rtol=0)
+        np.testing.assert_allclose(_deinterleave(dv, n, s), rdv, atol=1e-11, rtol=0)
+
+
+@pytest.mark.parametrize("shape", SHAPES)
+def test_mix_equals_causal_over_expanded(oracle_mod, shape):
+    """MIX(n) == ordinary causal attention over all n*L expanded rows, for every n."""
+    B, L, n, Hq, Hkv, D = shape
+    q, k, v, do = _rand(2, *shape)
+    scale = 1.0 / math.sqrt(D)
+    o, lse = oracle_mod.sfa_fwd(q, k, v, L=L, n=n, mode=MIX, scale=scale)
+    dq, dk, dv = oracle_mod.sfa_bwd(q, k, v, do, L=L, n=n, mode=MIX, scale=scale)
+    ro, rlse, rdq, rdk, rdv = _torch_causal(q, k, v, do, scale)
+    np.testing.assert_allclose(o, ro, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lse, rlse, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(dq, rdq, atol=1e-11, rtol=0)
+    np.testing.assert_allclose(dk, rdk, atol=1e-11, rtol=0)
+    np.testing.assert_allclose(dv, rdv, atol=1e-11, rtol=0)
+
+
+def test_n1_modes_coincide(oracle_mod):
+    """With one stream the two masks are the same causal mask."""
+    q, k, v, do = _rand(3, 1, 11, 1, 2, 1, 8)
+    a = oracle_mod.sfa_fwd(q, k, v, L=11, n=1, mode=INTRA, scale=0.3)
+    b = oracle_mod.sfa_fwd(q, k, v, L=11, n=1, mode=MIX, scale=0.3)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+
+
+def test_masks_match_hand_written_golden(oracle_mod):
+    lines = [ln.strip() for ln in open(os.path.join(GOLDEN, "masks_n2_L3.txt"))
+             if ln.strip() and not ln.startswith("#")]
+    want = {}
+    cur = None
+    for ln in lines:
+        if ln in ("intra", "mix"):
+            cur = ln
+            want[cur] = []
+        else:
+            want[cur].append([int(c) for c in ln])
+    np.testing.assert_array_equal(oracle_mod.sfa_mask(3, 2, INTRA), np.array(want["intra"]))
+    np.testing.assert_array_equal(oracle_mod.sfa_mask(3, 2, MIX), np.array(want["mix"]))
+
+
+@pytest.mark.parametrize("L,n", [(5, 3), (16, 4), (7, 1), (4, 8)])
+def test_mask_is_progression_or_prefix(oracle_mod, L, n):
+    """INTRA row p sees exactly range(p % n, p + 1, n); MIX row p sees range(0, p + 1)."""
+    N = n * L
+    mi = oracle_mod.sfa_mask(L, n, INTRA)
+    mm = oracle_mod.sfa_mask(L, n, MIX)
+    for p in range(N):
+        want_i = np.zeros(N, np.uint8)
+        want_i[list(range(p % n, p + 1, n))] = 1
+        want_m = np.zeros(N, np.uint8)
+        want_m[: p + 1] = 1
+        np.testing.assert_array_equal(mi[p], want_i)
+        np.testing.assert_array_equal(mm[p], want_m)
+
+
+def test_rows_sum_to_one_via_constant_values(oracle_mod):
+    """With every V entry equal to 1, O is exactly the row sum of P, which must be 1."""
+    q, k, v, _ = _rand(4, 2, 6, 3, 4, 2, 5)
+    v = np.ones_like(v)
+    for mode in (INTRA, MIX):
+        o, _ = oracle_mod.sfa_fwd(q, k, v, L=6, n=3, mode=mode, scale=0.7)
+        np.testing.assert_allclose(o, 1.0, atol=1e-12, rtol=0)
+
+
+@pytest.mark.parametrize("mode", [INTRA, MIX])
+def test_first_token_rows_closed_form(oracle_mod, mode):
+    """A row that sees only itself copies its own v, lse = scale q.k, and dQ = 0."""
+    B, L, n, Hq, Hkv, D = 1, 6, 4, 4, 2, 8
+    q, k, v, do = _rand(5, B, L, n, Hq, Hkv, D)
+    scale = 0.37
+    o, lse = oracle_mod.sfa_fwd(q, k, v, L=L, n=n, mode=mode, scale=scale)
+    dq, _, _ = oracle_mod.sfa_bwd(q, k, v, do, L=L, n=n, mode=mode, scale=scale)
+    rows = range(n) if mode == INTRA else range(1)
+    for p in rows:
+        for h in range(Hq):
+            hk = h // (Hq // Hkv)
+            np.testing.assert_allclose(o[0, p, h], v[0, p, hk], atol=1e-14, rtol=0)
+            assert abs(lse[0, h, p] - scale * float(q[0, p, h] @ k[0, p, hk])) < 1e-13
+            np.testing.assert_allclose(dq[0, p, h], 0.0, atol=1e-15)
+
+
+@pytest.mark.parametrize("mode", [INTRA, MIX])
+def test_uniform_logit_probe(oracle_mod, mode):
+    """Q = 0 makes every visible logit 0: lse = ln |vis(p)| and, with one-hot
+    V_j = e_(j mod D), O_p[d] = #{j in vis(p): j = d mod D} / |vis(p)|."""
+    L, n, D = 8, 4, 16
+    N = n * L
+    q = np.zeros((1, N, 1, D))
+    k = np.random.default_rng(6).standard_normal((1, N, 1, D))
+    v = np.zeros((1, N, 1, D))
+    for j in range(N):
+        v[0, j, 0, j % D] = 1.0
+    o, lse = oracle_mod.sfa_fwd(q, k, v, L=L, n=n, mode=mode, scale=1.0)
+    for p in range(N):
+        vis = list(range(p % n, p + 1, n)) if mode == INTRA else list(range(p + 1))
+        assert abs(lse[0, 0, p] - math.log(len(vis))) < 1e-13
+        want = np.bincount(np.array(vis) % D, minlength=D) / len(vis)
+        np.testing.assert_allclose(o[0, p, 0], want, atol=1e-14, rtol=0)
+        if mode == INTRA:  # n | D: columns of other residues are exactly zero
+            assert np.all(o[0, p, 0][np.arange(D) % n != p % n] == 0.0)
+
+
+def test_stream_replicated_inputs(oracle_mod):
+    """Identical q/k/v across the n streams of a token (what eq. (cyclic_init) yields at
+    the input).  INTRA: each stream is causal attention over the L tokens.  MIX: row
+    (t, s) weights earlier tokens by n and its own token by s + 1; at s = n - 1 the
+    output is the causal-L output and lse gains ln n."""
+    B, L, n, H, D = 1, 7, 3, 2, 6
+    r = np.random.default_rng(7)
+    base = [r.standard_normal((B, L, H, D)) for _ in range(3)]
+    rep = [np.repeat(x, n, axis=1) for x in base]  # row t*n+s = token t
+    scale = 0.45
+    do = np.zeros((B, L, H, D))
+    ro, rlse, *_ = _torch_causal(*base, do, scale)
+    oi, lsei = oracle_mod.sfa_fwd(*rep, L=L, n=n, mode=INTRA, scale=scale)
+    om, lsem = oracle_mod.sfa_fwd(*rep, L=L, n=n, mode=MIX, scale=scale)
+    for s in range(n):
+        np.testing.assert_allclose(oi[:, s::n], ro, atol=1e-12, rtol=0)
+        np.testing.assert_allclose(lsei[:, :, s::n], rlse, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(om[:, n - 1::n], ro, atol=1e-12, rtol=0)
+    np.testing.assert_allclose(lsem[:, :, n - 1::n], rlse + math.log(n), atol=1e-12, rtol=0)
+    # intermediate streams: explicit weighted softmax over tokens
+    q, k, v = base
+    for t in range(L):
+        for s in range(n):
+            for h in range(H):
+                x = scale * (k[0, : t + 1, h] @ q[0, t, h])
+                w = np.full(t + 1, float(n))
+                w[t] = s + 1
+                a = w * np.exp(x - x.max())
+                np.testing.assert_allclose(om[0, t * n + s, h], a @ v[0, : t + 1, h] / a.sum(),
+                                           atol=1e-12, rtol=0)
+                assert abs(lsem[0, h, t * n + s] - (x.max() + math.log(a.sum()))) < 1e-12
+
+
+@pytest.mark.parametrize("mode", [INTRA, MIX])
+def test_gradient_sums(oracle_mod, mode):
+    """Sum over keys of dV equals the group's summed dO; sum over keys of dK is 0 --
+    per (b, kv-head), and per stream for INTRA."""
+    B, L, n, Hq, Hkv, D = 2, 6, 3, 4, 2, 5
+    q, k, v, do = _rand(8, B, L, n, Hq, Hkv, D)
+    dq, dk, dv = oracle_mod.sfa_bwd(q, k, v, do, L=L, n=n, mode=mode, scale=0.6)
+    G = Hq // Hkv
+    for b in range(B):
+        for hk in range(Hkv):
+            group_do = do[b, :, hk * G:(hk + 1) * G]
+            np.testing.assert_allclose(dv[b, :, hk].sum(0), group_do.sum((0, 1)), atol=1e-12)
+            np.testing.assert_allclose(dk[b, :, hk].sum(0), 0.0, atol=1e-12)
+            if mode == INTRA:
+                for s in range(n):
+                    np.testing.assert_allclose(dv[b, s::n, hk].sum(0),
+                                               group_do[s::n].sum((0, 1)), atol=1e-12)
+                    np.testing.assert_allclose(dk[b, s::n, hk].sum(0), 0.0, atol=1e-12)
+
+
+def test_gqa_equals_repeated_heads(oracle_mod):
+    """Grouped heads == one key/value head per query head with K/V repeated;
+    dK/dV are the group sums of the repeated-head gradients."""
+    B, L, n, Hq, Hkv, D = 1, 5, 2, 6, 2, 4
+    G = Hq // Hkv
+    q, k, v, do = _rand(9, B, L, n, Hq, Hkv, D)
+    kr, vr = np.repeat(k, G, axis=2), np.repeat(v, G, axis=2)
+    for mode in (INTRA, MIX):
+        o, lse = oracle_mod.sfa_fwd(q, k, v, L=L, n=n, mode=mode, scale=0.5)
+        o2, lse2 = oracle_mod.sfa_fwd(q, kr, vr, L=L, n=n, mode=mode, scale=0.5)
+        np.testing.assert_allclose(o, o2, atol=1e-14)
+        np.testing.assert_allclose(lse, lse2, atol=1e-14)
+        dq, dk, dv = oracle_mod.sfa_bwd(q, k, v, do, L=L, n=n, mode=mode, scale=0.5)
+        dq2, dk2, dv2 = oracle_mod.sfa_bwd(q, kr, vr, do, L=L, n=n, mode=mode, scale=0.5)
+        np.testing.assert_allclose(dq, dq2, atol=1e-13)
+        np.testing.assert_allclose(dk, dk2.reshape(B, n * L, Hkv, G, D).sum(3), atol=1e-13)
+        np.testing.assert_allclose(dv, dv2.reshape(B, n * L, Hkv, G, D).sum(3), atol=1e-13)
+
+
+def _fd_check(oracle_mod, shape, mode, seed, max_entries=None):
+    B, L, n, Hq, Hkv, D = shape
+    q, k, v, do = _rand(seed, *shape)
+    scale = 1.0 / math.sqrt(D)
+    grads = oracle_mod.sfa_bwd(q, k, v, do, L=L, n=n, mode=mode, scale=scale)
+    h = 1e-6
+
+    def f(qq, kk, vv):
+        o, _ = oracle_mod.sfa_fwd(qq, kk, vv, L=L, n=n, mode=mode, scale=scale, nthreads=1)
+        return float((do * o).sum())
+
+    r = np.random.default_rng(seed + 100)
+    for idx, (name, g) in enumerate(zip("qkv", grads)):
+        x = [q, k, v][idx]
+        entries = np.arange(x.size)
+        if max_entries is not None and x.size > max_entries:
+            entries = r.choice(x.size, size=max_entries, replace=False)
+        gmax = np.abs(g).max()
+        for e in entries:
+            args = [q.copy(), k.copy(), v.copy()]
+            args[idx].flat[e] += h
+            fp = f(*args)
+            args[idx].flat[e] -= 2 * h
+            fm = f(*args)
+            fd = (fp - fm) / (2 * h)
+            assert abs(fd - g.flat[e]) <= 1e-6 * max(gmax, 1.0), (name, e, fd, g.flat[e])
+
+
+@pytest.mark.parametrize("mode", [INTRA, MIX])
+def test_finite_differences_every_entry_small(oracle_mod, mode):
+    _fd_check(oracle_mod, (1, 4, 3, 2, 1, 4), mode, seed=10)
+
+
+@pytest.mark.parametrize("mode", [INTRA, MIX])
+def test_finite_differences_tiny_config_sampled(oracle_mod, mode):
+    """Seeded subset of entries at the tiny fp32 workload shape (B=1 L=64 n=2 Hq=2 Hkv=1 D=32)."""
+    _fd_check(oracle_mod, (1, 64, 2, 2, 1, 32), mode, seed=11, max_entries=24)
+
+
+def test_bf16_inputs_upcast_exactly(oracle_mod):
+    """bf16 bit patterns are read as their exact values (same result as fp64 input)."""
+    B, L, n, Hq, Hkv, D = 1, 5, 2, 2, 1, 8
+    ins = synth.sfa_inputs(B, L, n, Hq, Hkv, D, seed=12, dtype="bf16")
+    as64 = {kk: synth.bf16_bits_to_f32(vv).astype(np.float64) for kk, vv in ins.items()}
+    for mode in (INTRA, MIX):
+        a = oracle_mod.sfa_fwd(ins["q"], ins["k"], ins["v"], L=L, n=n, mode=mode, scale=0.3)
+        b = oracle_mod.sfa_fwd(as64["q"], as64["k"], as64["v"], L=L, n=n, mode=mode, scale=0.3)
+        np.testing.assert_array_equal(a[0], b[0])
+        ga = oracle_mod.sfa_bwd(ins["q"], ins["k"], ins["v"], ins["dout"], L=L, n=n, mode=mode,
+                                scale=0.3)
+        gb = oracle_mod.sfa_bwd(as64["q"], as64["k"], as64["v"], as64["dout"], L=L, n=n,
+                                mode=mode, scale=0.3)
+        for x, y in zip(ga, gb):
+            np.testing.assert_array_equal(x, y)
+
+
+@pytest.mark.parametrize("mode", [INTRA, MIX])
+def test_row_sampled_entry_points_match_full(oracle_mod, mode):
+    B, L, n, Hq, Hkv, D = 2, 6, 3, 4, 2, 8
+    q, k, v, do = _rand(13, B, L, n, Hq, Hkv, D)
+    kw = dict(L=L, n=n, mode=mode, scale=0.4)
+    o, lse = oracle_mod.sfa_fwd(q, k, v, **kw)
+    dq, dk, dv = oracle_mod.sfa_bwd(q, k, v, do, **kw)
+    rows = np.array([[0, 0, 0], [1, 3, 17], [0, 2, 9], [1, 1, 5]])
+    ro, rl = oracle_mod.sfa_fwd_rows(q, k, v, rows, **kw)
+    rdq = oracle_mod.sfa_bwd_dq_rows(q, k, v, do, rows, **kw)
+    for i, (b, h, p) in enumerate(rows):
+        np.testing.assert_array_equal(ro[i], o[b, p, h])
+        assert rl[i] == lse[b, h, p]
+        np.testing.assert_array_equal(rdq[i], dq[b, p, h])
+    krows = np.array([[0, 0, 0], [1, 1, 17], [0, 1, 10]])
+    rdk, rdv = oracle_mod.sfa_bwd_dkdv_rows(q, k, v, do, krows, **kw)
+    for i, (b, h, j) in enumerate(krows):
+        np.testing.assert_allclose(rdk[i], dk[b, j, h], atol=1e-13)
+        np.testing.assert_allclose(rdv[i], dv[b, j, h], atol=1e-13)
+
+
+def test_expand_matches_paper_two_stream_example(oracle_mod):
+    g = json.load(open(os.path.join(GOLDEN, "expand_n2.json")))
+    tables = np.array([g["tables_E1"], g["tables_E2"]], dtype=np.uint16)
+    ids = np.array([g["ids"]], dtype=np.int32)
+    out, bad = oracle_mod.expand_embed(ids, tables)
+    assert bad == 0
+    np.testing.assert_array_equal(out[0], np.array(g["expected_rows"], dtype=np.uint16))
+    cyc = np.concatenate([tables, tables])  # eq. (cyclic_init): (E1, E2, E1, E2)
+    out4, _ = oracle_mod.expand_embed(ids, cyc)
+    np.testing.assert_array_equal(out4[0], np.array(g["cyclic_expected_rows_n4"], np.uint16))
+
+
+def test_expand_bad_ids_zero_and_counted(oracle_mod):
+    tables = np.arange(2 * 4 * 3, dtype=np.uint16).reshape(2, 4, 3) + 1
+    ids = np.array([[0, -1, 4, 3], [7, 2, 2, 0]], dtype=np.int32)
+    out, bad = oracle_mod.expand_embed(ids, tables)
+    assert bad == 3
+    assert np.all(out[0, 2:4] == 0) and np.all(out[0, 4:6] == 0) and np.all(out[1, 0:2] == 0)
+    np.testing.assert_array_equal(out[0, 6], tables[0, 3])
+    np.testing.assert_array_equal(out[0, 7], tables[1, 3])
+    np.testing.assert_array_equal(out[1, 3], tables[1, 2])
