@@ -1,0 +1,262 @@
+"""Benchmark of the Hidden Decoding hot path on one MI355X.
+
+One step = one pass of the whole hot path over one batch of synthetic input, the
+36-layer stack at the Qwen3-8B-like shape (B=1, L=4096 tokens, n=4 streams, N=16384
+expanded rows, Hq=32, Hkv=8, D=128, bf16):
+  * the stream expansion of 4096 token ids through n=4 tables of 151936 x 4096,
+  * the forward of 36 attention layers (mixing layers at 8, 17, 26, 35, intra-stream
+    layers elsewhere), then their backward in reverse order,
+each layer on its own seeded q/k/v/dO, all resident in HBM before timing starts.
+
+Prints one JSON line.  value = useful TFLOP/s of the whole step (useful flop counts
+only visible query/key pairs: 4*D per pair forward, 10*D backward).  The roofline
+entry is for the kernel with the largest share of the step, timed with HIP events
+recorded by the library around every launch, on the launch stream.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "SFA fwd+bwd useful TFLOP/s and % of bf16 MFMA peak, n=4 L=4096 (1 GPU)"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="stack36",
+                    choices=["stack36", "qwen8b-intra", "qwen8b-mix", "frontier-intra",
+                             "frontier-mix"] + [f"sweep-n{n}-{m}" for n in (1, 2, 4, 8)
+                                                for m in ("intra", "mix")])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-tokens", type=int, default=384)
+    return ap.parse_args()
+
+
+def per_kernel_flops(shape, mode):
+    """Algorithmic flop per kernel family for one layer (useful pairs only)."""
+    from paper_2607_08186_amd import workloads as W
+
+    pairs = W.visible_pairs(shape, mode)
+    D = shape.D
+    # forward: S = QK^T and O = PV; dK/dV pass: S, dP, dV, dK; dQ pass: dQ only
+    # (it recomputes S and dP, which the useful count does not credit twice)
+    return {"fwd": 4 * D * pairs, "dkdv": 8 * D * pairs, "dq": 2 * D * pairs}
+
+
+def kernel_family(name):
+    for fam in ("fwd", "dkdv", "dq", "preprocess", "expand"):
+        if fam in name:
+            return fam
+    return name
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(every run here uses a single MI355X); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    import paper_2607_08186_amd as hd
+    from paper_2607_08186_amd import synth
+    from paper_2607_08186_amd import workloads as W
+
+    if not os.path.exists(hd.binding.LIB_PATH):
+        from paper_2607_08186_amd import build as hip_build
+
+        hip_build.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+
+    # ---------------------------------------------------------------- workload
+    if args.workload == "stack36":
+        shape = W.QWEN8B.shape
+        modes = W.stack_modes()
+        with_embed = True
+        wl_desc = (f"stack36: expand_embed (n=4 tables of {W.STACK_VOCAB}x{W.STACK_DMODEL}) + "
+                   f"fwd of 36 layers (mix at {list(W.STACK_MIX_LAYERS)}, intra elsewhere) + "
+                   "bwd in reverse, each layer B=1 L=4096 n=4 Hq=32 Hkv=8 D=128")
+        std = W.QWEN8B.qkv_std
+        spike = None
+    else:
+        parts = args.workload.split("-")
+        m = W.INTRA if parts[-1] == "intra" else W.MIX
+        if parts[0] == "qwen8b":
+            wl = W.QWEN8B
+        elif parts[0] == "frontier":
+            wl = W.FRONTIER
+        else:
+            wl = {w.shape.n: w for w in W.SWEEP}[int(parts[1][1:])]
+        shape, modes, with_embed = wl.shape, [m], False
+        wl_desc = f"{wl.name} {W.MODE_NAMES[m]} fwd+bwd"
+        std, spike = wl.qkv_std, wl.k_spike
+    s = shape
+    nl = len(modes)
+    scale = s.scale
+
+    # ------------------------------------------------- resident synthetic inputs
+    t_gen = time.time()
+    layers = []
+    for li in range(nl):
+        seed = synth.seed_for("bench", args.workload, li)
+        q = synth.device_normal((s.B, s.N, s.Hq, s.D), std, seed + 1, dev, torch.bfloat16)
+        k = synth.device_normal((s.B, s.N, s.Hkv, s.D), std, seed + 2, dev, torch.bfloat16)
+        v = synth.device_normal((s.B, s.N, s.Hkv, s.D), std, seed + 3, dev, torch.bfloat16)
+        do = synth.device_normal((s.B, s.N, s.Hq, s.D), W.QWEN8B.dout_std, seed + 4, dev,
+                                 torch.bfloat16)
+        if spike is not None:  # scale a seeded 1% of K rows by 8 (exact in bf16)
+            flat = k.view(-1, s.D)
+            g = torch.Generator(device=dev)
+            g.manual_seed(seed + 5)
+            pick = torch.randperm(flat.shape[0], generator=g, device=dev)[
+                :int(spike[0] * flat.shape[0])]
+            flat[pick] *= spike[1]
+        o = torch.empty_like(q)
+        lse = torch.empty((s.B, s.Hq, s.N), dtype=torch.float32, device=dev)
+        layers.append(dict(q=q, k=k, v=v, do=do, o=o, lse=lse, mode=modes[li]))
+    dq = torch.empty_like(layers[0]["q"])
+    dk = torch.empty_like(layers[0]["k"])
+    dv = torch.empty_like(layers[0]["v"])
+    ws_bytes = max(hd.hd_sfa_bwd_workspace_bytes(s.B, s.L, s.n, s.Hq, s.Hkv, s.D, m,
+                                                 hd.HD_DTYPE_BF16) for m in set(modes))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    if with_embed:
+        ids = torch.randint(0, W.STACK_VOCAB, (1, s.L), dtype=torch.int32, device=dev,
+                            generator=torch.Generator(device=dev).manual_seed(11))
+        tables = synth.device_normal((s.n, W.STACK_VOCAB, W.STACK_DMODEL), W.STACK_EMBED_STD,
+                                     12, dev, torch.bfloat16)
+        emb = torch.empty((1, s.N, W.STACK_DMODEL), dtype=torch.bfloat16, device=dev)
+    torch.cuda.synchronize()
+    t_gen = time.time() - t_gen
+
+    def step():
+        if with_embed:
+            hd.hd_expand_embed(ids, tables, emb, 1, s.L, s.n, W.STACK_VOCAB, W.STACK_DMODEL,
+                               stream=stream)
+        for ly in layers:
+            hd.hd_sfa_fwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L, s.n, s.Hq,
+                          s.Hkv, s.D, ly["mode"], scale, stream=stream)
+        for ly in reversed(layers):
+            hd.hd_sfa_bwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq, dk, dv,
+                          s.B, s.L, s.n, s.Hq, s.Hkv, s.D, ly["mode"], scale, ws, ws_bytes,
+                          stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    hd.hd_timing_enable(True)
+    hd.hd_timing_collect()  # drop anything recorded before
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step()
+        print(f"[bench] step {i + 1}/{args.steps} enqueued", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    hd.hd_timing_enable(False)
+    ktimes = hd.hd_timing_collect()
+
+    flop_step = sum(W.useful_flop(s, m) for m in modes)
+    ms_per_step = elapsed * 1e3 / args.steps
+    value = flop_step * args.steps / elapsed / 1e12
+
+    # ------------------------------------------------------ per-kernel roofline
+    fam_flops = {}
+    for m in modes:
+        for fam, f in per_kernel_flops(s, m).items():
+            fam_flops[fam] = fam_flops.get(fam, 0) + f
+    per_kernel = []
+    fam_ms = {}
+    for name, launches, total_ms in ktimes:
+        fam = kernel_family(name)
+        fam_ms[fam] = fam_ms.get(fam, 0.0) + total_ms
+        per_kernel.append({"kernel": name, "launches": launches,
+                           "avg_ms": round(total_ms / launches, 5),
+                           "share": round(total_ms / (elapsed * 1e3), 4)})
+    dom = max(ktimes, key=lambda r: r[2])
+    dom_fam = kernel_family(dom[0])
+    dom_launches = dom[1]
+    avg_ms = dom[2] / dom_launches
+    if dom_fam in fam_flops:
+        per_launch = fam_flops[dom_fam] * args.steps / dom_launches
+        achieved = per_launch / (avg_ms * 1e-3) / 1e12
+        roofline = {"kernel": dom[0], "bound": "mfma", "achieved": round(achieved, 2),
+                    "peak": W.MI355X_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(achieved / W.MI355X_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                    "flop_per_launch": per_launch, "avg_launch_ms": round(avg_ms, 5)}
+    else:
+        roofline = {"kernel": dom[0], "bound": "hbm", "achieved": None, "peak": 8000.0,
+                    "unit": "GB/s", "frac": None, "traffic": None}
+    breakdown = {}
+    for fam, ms in fam_ms.items():
+        ent = {"ms_per_step": round(ms / args.steps, 4)}
+        if fam in fam_flops:
+            ent["tflops"] = round(fam_flops[fam] / (ms / args.steps * 1e-3) / 1e12, 2)
+        if fam == "expand":
+            nbytes = W.embed_bytes(1, s.L, s.n, W.STACK_DMODEL)
+            ent["gbs"] = round(nbytes / (ms / args.steps * 1e-3) / 1e9, 1)
+            ent["bytes_per_launch"] = nbytes
+        breakdown[fam] = ent
+
+    out = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+        "data": "synthetic (seeded device normal draws; no dataset or weights)",
+        "config": {"workload": wl_desc, "B": s.B, "L": s.L, "n": s.n, "Hq": s.Hq,
+                   "Hkv": s.Hkv, "D": s.D, "layers": nl,
+                   "useful_tflop_per_step": round(flop_step / 1e12, 4)},
+        "frac_of_peak": round(value / W.MI355X_BF16_PEAK_TFLOPS, 4),
+        "roofline": roofline, "breakdown": breakdown, "per_kernel": per_kernel,
+        "input_gen_s": round(t_gen, 2),
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(args.cpu_sample_tokens)
+    print(json.dumps(out), flush=True)
+
+
+def cpu_baseline(Ls):
+    """The fp64 oracle on a bounded sample of the same workload: one intra-stream and
+    one mixing layer of the stack, fwd + bwd, all 32 query heads, first Ls tokens."""
+    import numpy as np  # noqa: F401
+
+    import oracle
+    from paper_2607_08186_amd import synth
+    from paper_2607_08186_amd import workloads as W
+
+    base = W.QWEN8B.shape
+    sh = W.Shape(1, Ls, base.n, base.Hq, base.Hkv, base.D)
+    nthreads = oracle.default_threads()
+    ins = synth.sfa_inputs(sh.B, sh.L, sh.n, sh.Hq, sh.Hkv, sh.D, seed=synth.seed_for("cpu"),
+                           dtype="bf16", qkv_std=W.QWEN8B.qkv_std)
+    flop = 0
+    t0 = time.perf_counter()
+    for mode in (W.INTRA, W.MIX):
+        kw = dict(L=sh.L, n=sh.n, mode=mode, scale=sh.scale, nthreads=nthreads)
+        oracle.sfa_fwd(ins["q"], ins["k"], ins["v"], **kw)
+        oracle.sfa_bwd(ins["q"], ins["k"], ins["v"], ins["dout"], **kw)
+        flop += W.useful_flop(sh, mode)
+        print(f"[bench] cpu oracle mode {mode} done", file=sys.stderr, flush=True)
+    dt = time.perf_counter() - t0
+    return {"value": round(flop / dt / 1e12, 6), "unit": "TFLOP/s", "cores": nthreads,
+            "kind": "oracle", "seconds": round(dt, 2),
+            "sample": (f"one intra + one mix layer, fwd+bwd, B=1 L={Ls} n={sh.n} "
+                       f"Hq={sh.Hq} Hkv={sh.Hkv} D={sh.D} (prefix of the step's layer shape), "
+                       f"fp64, {nthreads} threads (bwd parallel over {sh.Hkv} kv-heads)")}
+
+
+if __name__ == "__main__":
+    main()

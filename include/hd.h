@@ -1,0 +1,146 @@
+/*
+ * hd.h -- C ABI of libhd.so: the Hidden Decoding hot path on AMD MI355X (gfx950).
+ *
+ * Paper: "Hidden Decoding at Scale: Latent Computation Scaling for Large Language
+ * Models".  Notation used below (0-based, token-major interleave):
+ *   L tokens, n streams, N = n*L expanded positions, expanded row p = t*n + s
+ *   (eq. (expansion) places stream k of token i at physical position (i-1)n + k;
+ *   eq. (indices) recovers token and stream from the position).
+ *
+ * Conventions shared by every entry point:
+ *   - All tensor pointers are DEVICE pointers owned by the caller, 16-byte aligned,
+ *     dense and row-major in the layouts stated per function.
+ *   - The library never allocates, frees or synchronises device memory.  Work is
+ *     enqueued on `stream` (0 = the null stream) and the call returns after enqueue.
+ *     Outputs are overwritten, never accumulated into.
+ *   - Arguments are validated on the host before anything is enqueued.  On a
+ *     non-HD_OK return nothing has been enqueued, except for HD_ERR_HIP, which
+ *     reports a launch failure; hd_last_error() then holds a readable detail.
+ *   - Per-batch slices of every tensor must stay below 2^31 bytes (32-bit offsets
+ *     inside the kernels); larger inputs are rejected with HD_ERR_INVALID_ARG.
+ *   - Calls are thread-safe with respect to each other; calls that write the same
+ *     output buffers on overlapping streams race, as with any kernel.
+ */
+#ifndef HD_H
+#define HD_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct ihipStream_t *hd_stream_t; /* a hipStream_t */
+
+typedef enum {
+    HD_OK = 0,
+    HD_ERR_INVALID_ARG = 1, /* null pointer, bad size, misalignment, short workspace */
+    HD_ERR_UNSUPPORTED = 2, /* valid request this build does not implement (e.g. D) */
+    HD_ERR_HIP = 3          /* the HIP runtime reported an error at launch */
+} hd_status_t;
+
+/*
+ * Attention mask of one Stream-Factorized Attention layer (Sec. "Stream-Factorized
+ * Attention").  With t = p / n and s = p % n:
+ *   HD_SFA_INTRA -- eq. (mask_intra): query p sees key p' iff s' == s and t' <= t
+ *                   (intra-stream layer, Fig. "masks" panel (c)).
+ *   HD_SFA_MIX   -- full cross-stream layer, Fig. "masks" panel (a): the standard
+ *                   causal mask over the expanded sequence, i.e. t' < t, or t' == t
+ *                   and s' <= s (p' <= p).
+ */
+typedef enum { HD_SFA_INTRA = 0, HD_SFA_MIX = 1 } hd_sfa_mode_t;
+
+typedef enum { HD_DTYPE_BF16 = 0, HD_DTYPE_F32 = 1 } hd_dtype_t;
+
+/*
+ * hd_expand_embed -- multi-stream token expansion, eq. (expansion):
+ *   out[b][t*n + s][:] = tables[s][ids[b][t]][:]     (tables[0] is the paper's E_1)
+ *
+ * ids          device int32 [B][L], token ids.
+ * tables       device [n][V][Dm] of `dtype` (bf16 or f32), the n per-stream tables.
+ * out          device [B][n*L][Dm] of `dtype`, overwritten.
+ * bad_id_count device int32 (nullable).  For each id outside [0, V) the n rows of that
+ *              token are written as zeros and *bad_id_count is incremented once (so
+ *              the caller zeroes it first to obtain a count).
+ * Errors: INVALID_ARG for null ids/tables/out, B, L, n, Dm <= 0, V <= 0 or
+ *         V > INT32_MAX, or unaligned pointers.
+ */
+hd_status_t hd_expand_embed(const int32_t *ids, const void *tables, void *out, int B, int L,
+                            int n, int64_t V, int Dm, hd_dtype_t dtype,
+                            int32_t *bad_id_count, hd_stream_t stream);
+
+/*
+ * hd_sfa_fwd -- Stream-Factorized Attention forward over the expanded sequence.
+ *   O_p = sum_{p' visible from p} softmax_p'(scale * q_p . k_p') v_p'
+ *   lse_p = log sum_{p' visible} exp(scale * q_p . k_p')       (natural log)
+ * with the visibility of `mode` (eq. (mask_intra) or the full causal mask).
+ *
+ * q, o   device [B][N][Hq][D]  of `dtype`.
+ * k, v   device [B][N][Hkv][D] of `dtype`; query head h uses key/value head
+ *        h / (Hq / Hkv) (grouped-query attention, contiguous groups).
+ * lse    device float [B][Hq][N].
+ * scale  softmax scale, finite and > 0 (typically 1/sqrt(D)), used exactly as given.
+ * Every row sees at least its own key, so no row is empty and no output is NaN for
+ * finite inputs.  INTRA reads only the keys of the query's own stream.
+ * Errors: INVALID_ARG for null pointers, any size <= 0, Hq % Hkv != 0, bad scale,
+ *         misalignment or oversize tensors; UNSUPPORTED for D not in {32, 64, 128}.
+ */
+hd_status_t hd_sfa_fwd(const void *q, const void *k, const void *v, void *o, float *lse,
+                       int B, int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode,
+                       float scale, hd_dtype_t dtype, hd_stream_t stream);
+
+/*
+ * hd_sfa_bwd_workspace_bytes -- device workspace hd_sfa_bwd needs for these sizes
+ * (per-row softmax statistics).  Returns 0 for arguments hd_sfa_bwd would reject.
+ */
+size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
+                                  hd_sfa_mode_t mode, hd_dtype_t dtype);
+
+/*
+ * hd_sfa_bwd -- gradients of the forward above, recomputing the attention
+ * probabilities from q, k and the forward's lse:
+ *   P = exp(scale q k^T - lse), dP = dO v^T, Delta = rowsum(dO * O),
+ *   dS = P * (dP - Delta), dq = scale dS k, dk = scale dS^T q, dv = P^T dO,
+ * dk/dv summed over the query heads of each key/value group.
+ *
+ * q, o, dO, dq  device [B][N][Hq][D] of `dtype`;  k, v, dk, dv  device [B][N][Hkv][D].
+ * lse           device float [B][Hq][N] exactly as written by hd_sfa_fwd.
+ * workspace     device, 256-byte aligned, at least hd_sfa_bwd_workspace_bytes(...)
+ *               bytes; contents on entry are ignored and on exit unspecified.
+ * Errors: as hd_sfa_fwd, plus INVALID_ARG for a missing or short workspace.
+ */
+hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *o,
+                       const float *lse, const void *dO, void *dq, void *dk, void *dv, int B,
+                       int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode, float scale,
+                       hd_dtype_t dtype, void *workspace, size_t workspace_bytes,
+                       hd_stream_t stream);
+
+/* Static name of a status code ("HD_OK", ...). */
+const char *hd_status_str(hd_status_t s);
+
+/* Detail of the last non-OK return on the calling thread ("" if none). */
+const char *hd_last_error(void);
+
+/*
+ * Per-kernel timing (diagnostics, not needed for normal use).  While enabled, every
+ * kernel the library launches is bracketed by a pair of HIP events recorded on the
+ * launch stream (event objects are created on first use and reused).
+ * hd_timing_collect waits for the recorded events, writes up to `max` entries of
+ * accumulated (kernel name, launch count, total milliseconds) and clears the record.
+ * Returns the number of entries written, or -1 on a HIP error.
+ */
+typedef struct {
+    char name[64];
+    int launches;
+    double total_ms;
+} hd_kernel_time_t;
+
+hd_status_t hd_timing_enable(int enable);
+int hd_timing_collect(hd_kernel_time_t *out, int max);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HD_H */

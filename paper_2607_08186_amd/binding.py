@@ -1,0 +1,192 @@
+"""ctypes binding of libhd.so: the C ABI of include/hd.h, argument marshalling only.
+
+Each ``hd_*`` function here has the name and argument order of its C counterpart;
+tensors stand in for device pointers (``torch.Tensor`` on the GPU; plain ints are
+accepted as raw addresses).  All computation happens in the HIP kernels of libhd.so.
+If the library is missing, every call raises: there is no fallback path.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libhd.so")
+
+HD_OK, HD_ERR_INVALID_ARG, HD_ERR_UNSUPPORTED, HD_ERR_HIP = 0, 1, 2, 3
+HD_SFA_INTRA, HD_SFA_MIX = 0, 1
+HD_DTYPE_BF16, HD_DTYPE_F32 = 0, 1
+
+# every symbol include/hd.h declares
+EXPORTS = ("hd_expand_embed", "hd_sfa_fwd", "hd_sfa_bwd_workspace_bytes", "hd_sfa_bwd",
+           "hd_status_str", "hd_last_error", "hd_timing_enable", "hd_timing_collect")
+
+
+class HDError(RuntimeError):
+    def __init__(self, status: int, detail: str):
+        self.status = status
+        super().__init__(f"{_STATUS.get(status, status)}: {detail}")
+
+
+_STATUS = {0: "HD_OK", 1: "HD_ERR_INVALID_ARG", 2: "HD_ERR_UNSUPPORTED", 3: "HD_ERR_HIP"}
+
+
+class KernelTime(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 64), ("launches", ctypes.c_int),
+                ("total_ms", ctypes.c_double)]
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libhd.so (built in-tree by paper_2607_08186_amd.build); raise if absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built: run __graft_entry__.build() "
+                          "(there is no fallback implementation)")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, i64, f32 = ctypes.c_void_p, ctypes.c_int, ctypes.c_int64, ctypes.c_float
+    sz = ctypes.c_size_t
+    L.hd_expand_embed.argtypes = [vp, vp, vp, i32, i32, i32, i64, i32, i32, vp, vp]
+    L.hd_sfa_fwd.argtypes = [vp, vp, vp, vp, vp] + [i32] * 7 + [f32, i32, vp]
+    L.hd_sfa_bwd_workspace_bytes.argtypes = [i32] * 8
+    L.hd_sfa_bwd_workspace_bytes.restype = sz
+    L.hd_sfa_bwd.argtypes = [vp] * 9 + [i32] * 7 + [f32, i32, vp, sz, vp]
+    for f in (L.hd_expand_embed, L.hd_sfa_fwd, L.hd_sfa_bwd, L.hd_timing_enable):
+        f.restype = i32
+    L.hd_status_str.argtypes = [i32]
+    L.hd_status_str.restype = ctypes.c_char_p
+    L.hd_last_error.argtypes = []
+    L.hd_last_error.restype = ctypes.c_char_p
+    L.hd_timing_enable.argtypes = [i32]
+    L.hd_timing_collect.argtypes = [ctypes.POINTER(KernelTime), i32]
+    L.hd_timing_collect.restype = i32
+    _lib = L
+    return L
+
+
+def _ptr(x):
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    if not x.is_contiguous():
+        raise ValueError("tensors passed to libhd must be contiguous")
+    return x.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _dtype_code(t, dtype):
+    if dtype is not None:
+        return int(dtype)
+    import torch
+
+    if t.dtype == torch.bfloat16:
+        return HD_DTYPE_BF16
+    if t.dtype == torch.float32:
+        return HD_DTYPE_F32
+    raise TypeError(f"unsupported tensor dtype {t.dtype}")
+
+
+def _check(status: int):
+    if status != HD_OK:
+        raise HDError(status, lib().hd_last_error().decode())
+
+
+def hd_expand_embed(ids, tables, out, B, L, n, V, Dm, dtype=None, bad_id_count=None,
+                    stream=None):
+    _check(lib().hd_expand_embed(_ptr(ids), _ptr(tables), _ptr(out), B, L, n, V, Dm,
+                                 _dtype_code(tables, dtype), _ptr(bad_id_count),
+                                 _stream(stream)))
+
+
+def hd_sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, mode, scale, dtype=None, stream=None):
+    _check(lib().hd_sfa_fwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, L, n, Hq, Hkv, D,
+                            int(mode), float(scale), _dtype_code(q, dtype), _stream(stream)))
+
+
+def hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, dtype) -> int:
+    return int(lib().hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, int(mode), int(dtype)))
+
+
+def hd_sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, mode, scale, workspace,
+               workspace_bytes, dtype=None, stream=None):
+    _check(lib().hd_sfa_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dO), _ptr(dq),
+                            _ptr(dk), _ptr(dv), B, L, n, Hq, Hkv, D, int(mode), float(scale),
+                            _dtype_code(q, dtype), _ptr(workspace), int(workspace_bytes),
+                            _stream(stream)))
+
+
+def hd_timing_enable(enable: bool):
+    _check(lib().hd_timing_enable(1 if enable else 0))
+
+
+def hd_timing_collect(max_entries: int = 64):
+    """-> list of (kernel name, launches, total ms) accumulated since the last collect."""
+    buf = (KernelTime * max_entries)()
+    n = lib().hd_timing_collect(buf, max_entries)
+    if n < 0:
+        raise HDError(HD_ERR_HIP, lib().hd_last_error().decode())
+    return [(buf[i].name.decode(), buf[i].launches, buf[i].total_ms) for i in range(n)]
+
+
+# ---------------------------------------------------------------- conveniences
+# Shape inference and output allocation through torch (device memory plumbing only).
+
+def _shape(q, k, n):
+    B, N, Hq, D = q.shape
+    Hkv = k.shape[2]
+    if N % n:
+        raise ValueError(f"expanded length {N} is not a multiple of n={n}")
+    return B, N // n, Hq, Hkv, D
+
+
+def sfa_forward(q, k, v, *, n, mode, scale=None, stream=None):
+    """q [B][n*L][Hq][D], k/v [B][n*L][Hkv][D] -> (o, lse [B][Hq][n*L] fp32)."""
+    import torch
+
+    B, L, Hq, Hkv, D = _shape(q, k, n)
+    scale = scale if scale is not None else D ** -0.5
+    o = torch.empty_like(q)
+    lse = torch.empty((B, Hq, n * L), dtype=torch.float32, device=q.device)
+    hd_sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, mode, scale, stream=stream)
+    return o, lse
+
+
+def sfa_backward(q, k, v, o, lse, dO, *, n, mode, scale=None, workspace=None, stream=None):
+    """-> (dq, dk, dv).  A workspace tensor (uint8, 256-byte aligned) may be passed in."""
+    import torch
+
+    B, L, Hq, Hkv, D = _shape(q, k, n)
+    scale = scale if scale is not None else D ** -0.5
+    dtype = _dtype_code(q, None)
+    need = hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, dtype)
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    hd_sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, mode, scale, workspace,
+               workspace.numel(), stream=stream)
+    return dq, dk, dv
+
+
+def expand_embed(ids, tables, *, bad_id_count=None, stream=None):
+    """ids [B][L] int32, tables [n][V][Dm] -> out [B][n*L][Dm]."""
+    import torch
+
+    B, L = ids.shape
+    n, V, Dm = tables.shape
+    out = torch.empty((B, n * L, Dm), dtype=tables.dtype, device=tables.device)
+    hd_expand_embed(ids, tables, out, B, L, n, V, Dm, bad_id_count=bad_id_count, stream=stream)
+    return out

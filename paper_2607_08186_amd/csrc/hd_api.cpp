@@ -1,0 +1,287 @@
+// hd_api.cpp -- the C ABI of libhd.so: argument validation, dispatch, diagnostics.
+//
+// Every entry point validates all arguments on the host before enqueuing anything;
+// the kernels then run on the caller's stream.  No allocation, no synchronisation.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/hd.h"
+#include "hd_internal.h"
+
+namespace {
+
+thread_local char g_err[512] = "";
+
+hd_status_t fail(hd_status_t st, const char *fmt, ...)
+{
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(g_err, sizeof g_err, fmt, ap);
+    va_end(ap);
+    return st;
+}
+
+hd_status_t hip_status(hipError_t e, const char *what)
+{
+    if (e == hipSuccess) return HD_OK;
+    return fail(HD_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+constexpr int64_t kSliceLimit = (int64_t)1 << 31;  // bytes per batch slice
+
+// Shared shape checks of the SFA entry points.
+hd_status_t check_sfa(int B, int L, int n, int Hq, int Hkv, int D, int mode, float scale,
+                      int dtype)
+{
+    if (B <= 0 || L <= 0 || n <= 0 || Hq <= 0 || Hkv <= 0 || D <= 0)
+        return fail(HD_ERR_INVALID_ARG, "sizes must be positive (B=%d L=%d n=%d Hq=%d Hkv=%d D=%d)",
+                    B, L, n, Hq, Hkv, D);
+    if (Hq % Hkv != 0)
+        return fail(HD_ERR_INVALID_ARG, "Hq=%d is not a multiple of Hkv=%d", Hq, Hkv);
+    if (mode != HD_SFA_INTRA && mode != HD_SFA_MIX)
+        return fail(HD_ERR_INVALID_ARG, "mode %d is neither HD_SFA_INTRA nor HD_SFA_MIX", mode);
+    if (!std::isfinite(scale) || !(scale > 0.f))
+        return fail(HD_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", (double)scale);
+    if (dtype != HD_DTYPE_BF16 && dtype != HD_DTYPE_F32)
+        return fail(HD_ERR_INVALID_ARG, "unknown dtype %d", dtype);
+    if (D != 32 && D != 64 && D != 128)
+        return fail(HD_ERR_UNSUPPORTED, "head dim D=%d not supported (32, 64 or 128)", D);
+    const int64_t N = (int64_t)n * L;
+    const int64_t esize = dtype == HD_DTYPE_BF16 ? 2 : 4;
+    if (N > (1 << 30))
+        return fail(HD_ERR_INVALID_ARG, "expanded length n*L=%lld too large", (long long)N);
+    if (N * Hq * D * esize >= kSliceLimit || (int64_t)Hq * N * 4 >= kSliceLimit)
+        return fail(HD_ERR_INVALID_ARG,
+                    "per-batch tensor slice of %lld bytes exceeds the 2^31-byte limit",
+                    (long long)(N * Hq * D * esize));
+    const int64_t len = mode == HD_SFA_INTRA ? L : N;
+    const int64_t problems = (int64_t)B * Hq * (mode == HD_SFA_INTRA ? n : 1);
+    if (problems * ((len + 63) / 64) >= ((int64_t)1 << 31))
+        return fail(HD_ERR_INVALID_ARG, "grid too large");
+    return HD_OK;
+}
+
+// ------------------------------------------------------------------ timing
+
+struct TimingRecord {
+    std::string name;
+    hipEvent_t start, stop;
+};
+
+std::mutex g_tmu;
+bool g_timing = false;
+std::vector<hipEvent_t> g_pool;
+std::vector<TimingRecord> g_records;
+thread_local int g_open = -1;
+
+hipEvent_t take_event()
+{
+    if (!g_pool.empty()) {
+        hipEvent_t e = g_pool.back();
+        g_pool.pop_back();
+        return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+}
+
+}  // namespace
+
+namespace hd {
+
+void timing_before(const char *name, hipStream_t s)
+{
+    std::lock_guard<std::mutex> lk(g_tmu);
+    g_open = -1;
+    if (!g_timing) return;
+    TimingRecord r{name, take_event(), take_event()};
+    if (!r.start || !r.stop) return;
+    (void)hipEventRecord(r.start, s);
+    g_records.push_back(r);
+    g_open = (int)g_records.size() - 1;
+}
+
+void timing_after(hipStream_t s)
+{
+    std::lock_guard<std::mutex> lk(g_tmu);
+    if (g_open < 0) return;
+    (void)hipEventRecord(g_records[g_open].stop, s);
+    g_open = -1;
+}
+
+}  // namespace hd
+
+extern "C" {
+
+const char *hd_status_str(hd_status_t s)
+{
+    switch (s) {
+    case HD_OK: return "HD_OK";
+    case HD_ERR_INVALID_ARG: return "HD_ERR_INVALID_ARG";
+    case HD_ERR_UNSUPPORTED: return "HD_ERR_UNSUPPORTED";
+    case HD_ERR_HIP: return "HD_ERR_HIP";
+    }
+    return "HD_ERR_UNKNOWN";
+}
+
+const char *hd_last_error(void) { return g_err; }
+
+hd_status_t hd_expand_embed(const int32_t *ids, const void *tables, void *out, int B, int L,
+                            int n, int64_t V, int Dm, hd_dtype_t dtype, int32_t *bad_id_count,
+                            hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (!ids || !tables || !out) return fail(HD_ERR_INVALID_ARG, "null ids, tables or out");
+    if (B <= 0 || L <= 0 || n <= 0 || Dm <= 0 || V <= 0)
+        return fail(HD_ERR_INVALID_ARG, "sizes must be positive (B=%d L=%d n=%d V=%lld Dm=%d)", B,
+                    L, n, (long long)V, Dm);
+    if (V > INT32_MAX) return fail(HD_ERR_INVALID_ARG, "V=%lld exceeds int32 ids", (long long)V);
+    if (dtype != HD_DTYPE_BF16 && dtype != HD_DTYPE_F32)
+        return fail(HD_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    if (!aligned16(tables) || !aligned16(out) || (reinterpret_cast<uintptr_t>(ids) & 3))
+        return fail(HD_ERR_INVALID_ARG, "tables/out must be 16-byte aligned, ids 4-byte aligned");
+    if (bad_id_count && (reinterpret_cast<uintptr_t>(bad_id_count) & 3))
+        return fail(HD_ERR_INVALID_ARG, "bad_id_count must be 4-byte aligned");
+    if ((int64_t)B * L >= ((int64_t)1 << 31))
+        return fail(HD_ERR_INVALID_ARG, "B*L too large");
+    const int esize = dtype == HD_DTYPE_BF16 ? 2 : 4;
+    return hip_status(hd::launch_expand_embed(ids, tables, out, B, L, n, V, Dm, esize,
+                                              bad_id_count, (hipStream_t)stream),
+                      "hd_expand_embed launch");
+}
+
+hd_status_t hd_sfa_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                       int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode, float scale,
+                       hd_dtype_t dtype, hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (!q || !k || !v || !o || !lse) return fail(HD_ERR_INVALID_ARG, "null tensor pointer");
+    hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, scale, dtype);
+    if (st != HD_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
+        return fail(HD_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+    const hd::SfaGeom g = hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale);
+    hipError_t e;
+    if (dtype == HD_DTYPE_BF16)
+        e = hd::launch_fwd_bf16(q, k, v, o, lse, g, (hipStream_t)stream);
+    else
+        e = hd::launch_fwd_f32(static_cast<const float *>(q), static_cast<const float *>(k),
+                               static_cast<const float *>(v), static_cast<float *>(o), lse, g,
+                               (hipStream_t)stream);
+    return hip_status(e, "hd_sfa_fwd launch");
+}
+
+size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
+                                  hd_sfa_mode_t mode, hd_dtype_t dtype)
+{
+    char saved[sizeof g_err];
+    memcpy(saved, g_err, sizeof g_err);
+    hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, 1.0f, dtype);
+    memcpy(g_err, saved, sizeof g_err);
+    if (st != HD_OK) return 0;
+    return hd::bwd_workspace_bytes(hd::make_geom(B, L, n, Hq, Hkv, D, mode, 1.0f));
+}
+
+hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *o,
+                       const float *lse, const void *dO, void *dq, void *dk, void *dv, int B,
+                       int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode, float scale,
+                       hd_dtype_t dtype, void *workspace, size_t workspace_bytes,
+                       hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv)
+        return fail(HD_ERR_INVALID_ARG, "null tensor pointer");
+    hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, scale, dtype);
+    if (st != HD_OK) return st;
+    if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) ||
+        !aligned16(dO) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
+        return fail(HD_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
+    const hd::SfaGeom g = hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale);
+    const size_t need = hd::bwd_workspace_bytes(g);
+    if (!workspace) return fail(HD_ERR_INVALID_ARG, "null workspace (%zu bytes needed)", need);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+        return fail(HD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need)
+        return fail(HD_ERR_INVALID_ARG, "workspace of %zu bytes is short of %zu", workspace_bytes,
+                    need);
+    hipError_t e;
+    if (dtype == HD_DTYPE_BF16)
+        e = hd::launch_bwd_bf16(q, k, v, o, lse, dO, dq, dk, dv, g, workspace,
+                                (hipStream_t)stream);
+    else
+        e = hd::launch_bwd_f32(static_cast<const float *>(q), static_cast<const float *>(k),
+                               static_cast<const float *>(v), static_cast<const float *>(o), lse,
+                               static_cast<const float *>(dO), static_cast<float *>(dq),
+                               static_cast<float *>(dk), static_cast<float *>(dv), g, workspace,
+                               (hipStream_t)stream);
+    return hip_status(e, "hd_sfa_bwd launch");
+}
+
+hd_status_t hd_timing_enable(int enable)
+{
+    std::lock_guard<std::mutex> lk(g_tmu);
+    g_timing = enable != 0;
+    return HD_OK;
+}
+
+int hd_timing_collect(hd_kernel_time_t *out, int max)
+{
+    std::vector<TimingRecord> recs;
+    {
+        std::lock_guard<std::mutex> lk(g_tmu);
+        recs.swap(g_records);
+    }
+    std::map<std::string, std::pair<int, double>> acc;
+    std::vector<std::string> order;
+    bool ok = true;
+    for (auto &r : recs) {
+        float ms = 0.f;
+        if (hipEventSynchronize(r.stop) != hipSuccess ||
+            hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) {
+            ok = false;
+            continue;
+        }
+        auto it = acc.find(r.name);
+        if (it == acc.end()) {
+            order.push_back(r.name);
+            acc[r.name] = {1, (double)ms};
+        } else {
+            it->second.first += 1;
+            it->second.second += ms;
+        }
+    }
+    {
+        std::lock_guard<std::mutex> lk(g_tmu);
+        for (auto &r : recs) {
+            g_pool.push_back(r.start);
+            g_pool.push_back(r.stop);
+        }
+    }
+    if (!ok) {
+        fail(HD_ERR_HIP, "hd_timing_collect: event query failed");
+        return -1;
+    }
+    int nout = 0;
+    for (auto &name : order) {
+        if (nout >= max || !out) break;
+        hd_kernel_time_t &t = out[nout++];
+        memset(&t, 0, sizeof t);
+        strncpy(t.name, name.c_str(), sizeof t.name - 1);
+        t.launches = acc[name].first;
+        t.total_ms = acc[name].second;
+    }
+    return nout;
+}
+
+}  // extern "C"

@@ -1,0 +1,72 @@
+// hd_internal.h -- host-side geometry and kernel launchers shared inside libhd.so.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hd {
+
+// One SFA call reduced to independent causal problems over a strided row sequence.
+//   MIX  : one problem per (b, hq); rows p = 0 .. N-1            (len = N, rowmul = 1)
+//   INTRA: one problem per (b, hq, s); rows p = t*n + s, t < L   (len = L, rowmul = n)
+// Row i of a problem is expanded position p = i*rowmul + s, so the intra mask of
+// eq. (mask_intra) becomes the ordinary causal mask i' <= i inside the problem and
+// the kernels never touch rows of other streams.
+struct SfaGeom {
+    int B, L, n, Hq, Hkv, D, G;  // G = Hq / Hkv
+    int N;                       // n * L
+    int mode;                    // 0 intra, 1 mix
+    int len;                     // rows per problem
+    int rowmul;                  // n (intra) or 1 (mix)
+    int streams;                 // n (intra) or 1 (mix): problems per head
+    float scale;                 // softmax scale
+    float scale_log2;            // scale * log2(e)
+};
+
+inline SfaGeom make_geom(int B, int L, int n, int Hq, int Hkv, int D, int mode, float scale)
+{
+    SfaGeom g;
+    g.B = B; g.L = L; g.n = n; g.Hq = Hq; g.Hkv = Hkv; g.D = D; g.G = Hq / Hkv;
+    g.N = n * L;
+    g.mode = mode;
+    g.len = mode == 0 ? L : n * L;
+    g.rowmul = mode == 0 ? n : 1;
+    g.streams = mode == 0 ? n : 1;
+    g.scale = scale;
+    g.scale_log2 = scale * 1.4426950408889634f;
+    return g;
+}
+
+// Launch wrappers record per-kernel timing events when timing is enabled.
+void timing_before(const char *name, hipStream_t s);
+void timing_after(hipStream_t s);
+
+hipError_t launch_expand_embed(const int32_t *ids, const void *tables, void *out, int B, int L,
+                               int n, int64_t V, int Dm, int esize, int32_t *bad,
+                               hipStream_t s);
+
+hipError_t launch_fwd_bf16(const void *q, const void *k, const void *v, void *o, float *lse,
+                           const SfaGeom &g, hipStream_t s);
+hipError_t launch_bwd_bf16(const void *q, const void *k, const void *v, const void *o,
+                           const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                           const SfaGeom &g, void *ws, hipStream_t s);
+
+hipError_t launch_fwd_f32(const float *q, const float *k, const float *v, float *o, float *lse,
+                          const SfaGeom &g, hipStream_t s);
+hipError_t launch_bwd_f32(const float *q, const float *k, const float *v, const float *o,
+                          const float *lse, const float *dO, float *dq, float *dk, float *dv,
+                          const SfaGeom &g, void *ws, hipStream_t s);
+
+// delta = rowsum(dO * O) and lse2 = lse * log2(e), both fp32 [B][Hq][N]; esize = 2 or 4.
+hipError_t launch_bwd_preprocess(const void *o, const void *dO, const float *lse, float *delta,
+                                 float *lse2, const SfaGeom &g, int esize, hipStream_t s);
+
+// Workspace: per-row delta = rowsum(dO * O) and lse in log2 units, both fp32 [B][Hq][N].
+inline size_t bwd_workspace_bytes(const SfaGeom &g)
+{
+    size_t rows = (size_t)g.B * g.Hq * g.N;
+    size_t one = (rows * sizeof(float) + 255) & ~(size_t)255;
+    return 2 * one;
+}
+
+}  // namespace hd

@@ -1,0 +1,269 @@
+// sfa_fwd_bf16.hip -- Stream-Factorized Attention forward, bf16 in/out, fp32 softmax.
+//
+// Computes, per causal problem (see SfaGeom), O = softmax(scale Q K^T + mask) V and the
+// natural-log row log-sum-exp, the forward of the intra-stream layer (eq. (mask_intra))
+// and of the full cross-stream layer (causal mask of Fig. "masks"(a)).
+//
+// Tiling (gfx950, wave64):
+//   workgroup = 4 waves = 128 query rows of one problem; wave w owns rows 32w..32w+31.
+//   Each lane keeps one query row (column l%32 of the MFMA results): the transposed
+//   score tile S^T = K Q^T (keys x queries) puts a row's scores in one lane, so the
+//   row max / row sum need a single cross-half exchange, and P^T feeds the second
+//   MFMA (O^T += V^T P^T) straight from registers.
+//   Key tiles of 64 rows are staged in LDS, double buffered: K row-major (padded) and
+//   V transposed (V^T, keys contiguous per head-dim row, XOR-swizzled 16-byte chunks).
+//   Only tiles at or below the diagonal are visited; the causal mask is applied on the
+//   diagonal tiles alone.  The running max is refreshed only when it grows by more
+//   than 2^8 (log2 units), so the O rescale is rare; results are exact either way
+//   because the normaliser uses the same reference.
+#include "hd_device.h"
+
+namespace hd {
+
+namespace {
+
+constexpr int kBM = 128;  // query rows per workgroup
+constexpr int kBN = 64;   // keys per staged tile
+constexpr float kRescaleThreshold = 8.0f;  // log2 units
+
+__device__ inline int vt_swizzle(int d) { return ((d >> 1) ^ (d >> 3)) & 7; }
+
+template <int D>
+__global__ __launch_bounds__(256, 2) void sfa_fwd_bf16_kernel(const bf16 *__restrict__ q,
+                                                              const bf16 *__restrict__ k,
+                                                              const bf16 *__restrict__ v,
+                                                              bf16 *__restrict__ o,
+                                                              float *__restrict__ lse, SfaGeom g)
+{
+    constexpr int KS = D / 16;         // MFMA k-steps over the head dim
+    constexpr int DB = D / 32;         // 32-wide head-dim blocks of O
+    constexpr int CH = D / 8;          // 16-byte chunks per row
+    constexpr int KSTR = D + 8;        // padded K row in LDS (elements)
+    constexpr int KCH = kBN * CH / 256;  // K chunks staged per thread
+    constexpr int VUNITS = (kBN / 4) * CH;  // V staging units of 4 keys x 8 dims
+
+    __shared__ __attribute__((aligned(16))) bf16 sk[2][kBN * KSTR];
+    __shared__ __attribute__((aligned(16))) bf16 sv[2][D * kBN];
+
+    const int ntiles = (g.len + kBM - 1) / kBM;
+    const int nprob = g.B * g.Hq * g.streams;
+    int prob, tile;
+    decode_tile(blockIdx.x, nprob, ntiles, prob, tile);
+    const int s = prob % g.streams;
+    const int hq = (prob / g.streams) % g.Hq;
+    const int b = prob / (g.streams * g.Hq);
+    const int hk = hq / g.G;
+
+    // per-batch slices; all in-slice byte offsets fit in 31 bits
+    const size_t qslice = (size_t)g.N * g.Hq * D, kslice = (size_t)g.N * g.Hkv * D;
+    const rsrc_t rq = make_rsrc(q + b * qslice, (uint32_t)(qslice * 2));
+    const rsrc_t rk = make_rsrc(k + b * kslice, (uint32_t)(kslice * 2));
+    const rsrc_t rv = make_rsrc(v + b * kslice, (uint32_t)(kslice * 2));
+    const rsrc_t ro = make_rsrc(o + b * qslice, (uint32_t)(qslice * 2));
+    const uint32_t qstride = (uint32_t)g.rowmul * g.Hq * D * 2;
+    const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
+    const uint32_t kstride = (uint32_t)g.rowmul * g.Hkv * D * 2;
+    const uint32_t kbase0 = (uint32_t)(s * g.Hkv + hk) * D * 2;
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int l32 = lane & 31, hi = lane >> 5;
+    const int q0 = tile * kBM;
+    const int row = q0 + wave * 32 + l32;
+
+    // this lane's query row as the B operand of S^T = K Q^T
+    bf16x8 qr[KS];
+    {
+        const uint32_t off = row < g.len ? qbase + (uint32_t)row * qstride : kOob;
+#pragma unroll
+        for (int kk = 0; kk < KS; ++kk)
+            qr[kk] = __builtin_bit_cast(bf16x8, ld16(rq, off + (kk * 16 + hi * 8) * 2));
+    }
+
+    f32x16 oacc[DB];
+#pragma unroll
+    for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
+    float m2 = -INFINITY;  // reference max in log2 units
+    float lsum = 0.f;      // this lane half's share of the row sum
+
+    const int kend = min(g.len, q0 + kBM);
+    const int nkt = (kend + kBN - 1) / kBN;
+
+    u32x4 kreg[KCH];
+    u32x4 vreg[4];
+
+    auto load_tile = [&](int j) {
+#pragma unroll
+        for (int c = 0; c < KCH; ++c) {
+            const int idx = tid + c * 256, r = idx / CH, ch = idx % CH;
+            const int key = j * kBN + r;
+            const uint32_t off = key < g.len ? kbase0 + (uint32_t)key * kstride + ch * 16 : kOob;
+            kreg[c] = ld16(rk, off);
+        }
+        if (tid < VUNITS) {
+            const int ch = tid % CH, kq = tid / CH;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int key = j * kBN + kq * 4 + r;
+                const uint32_t off =
+                    key < g.len ? kbase0 + (uint32_t)key * kstride + ch * 16 : kOob;
+                vreg[r] = ld16(rv, off);
+            }
+        }
+    };
+
+    auto store_tile = [&](int buf) {
+#pragma unroll
+        for (int c = 0; c < KCH; ++c) {
+            const int idx = tid + c * 256, r = idx / CH, ch = idx % CH;
+            *reinterpret_cast<u32x4 *>(&sk[buf][r * KSTR + ch * 8]) = kreg[c];
+        }
+        if (tid < VUNITS) {
+            const int ch = tid % CH, kq = tid / CH;
+            const int pos = swap23(kq * 4);  // keys kq*4 .. +3 land on pos .. pos+3
+            const int c16 = pos >> 3, within = pos & 7;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int d = ch * 8 + e;
+                const int w = e >> 1;
+                uint32_t lo, hi2;
+                if ((e & 1) == 0) {
+                    lo = (vreg[0][w] & 0xffffu) | (vreg[1][w] << 16);
+                    hi2 = (vreg[2][w] & 0xffffu) | (vreg[3][w] << 16);
+                } else {
+                    lo = (vreg[0][w] >> 16) | (vreg[1][w] & 0xffff0000u);
+                    hi2 = (vreg[2][w] >> 16) | (vreg[3][w] & 0xffff0000u);
+                }
+                const int phys = d * kBN + ((c16 ^ vt_swizzle(d)) << 3) + within;
+                *reinterpret_cast<u32x2 *>(&sv[buf][phys]) = u32x2{lo, hi2};
+            }
+        }
+    };
+
+    const float c2 = g.scale_log2;
+    const int wrow_min = q0 + wave * 32, wrow_max = wrow_min + 31;
+
+    load_tile(0);
+    store_tile(0);
+    __syncthreads();
+
+    for (int j = 0; j < nkt; ++j) {
+        const int buf = j & 1;
+        if (j + 1 < nkt) load_tile(j + 1);
+        const int kbase = j * kBN;
+        if (kbase <= wrow_max) {  // wave-uniform: tile holds keys visible to this wave
+            f32x16 sacc[2];
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb) {
+                sacc[mb] = f32x16{};
+#pragma unroll
+                for (int kk = 0; kk < KS; ++kk) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
+                        &sk[buf][(mb * 32 + l32) * KSTR + kk * 16 + hi * 8]);
+                    sacc[mb] = mfma32(a, qr[kk], sacc[mb]);
+                }
+            }
+            if (kbase + kBN - 1 > wrow_min) {  // diagonal tile: causal mask
+#pragma unroll
+                for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                    for (int r = 0; r < 16; ++r) {
+                        const int key = kbase + mb * 32 + 8 * (r >> 2) + 4 * hi + (r & 3);
+                        if (key > row) sacc[mb][r] = -INFINITY;
+                    }
+            }
+            float mx = -INFINITY;
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[mb][r]);
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float mcand = fmaxf(m2, mx * c2);
+            if (__any(mcand > m2 + kRescaleThreshold)) {
+                const float alpha = mcand == -INFINITY ? 1.f : fast_exp2(m2 - mcand);
+                m2 = mcand;
+                lsum *= alpha;
+#pragma unroll
+                for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
+            }
+            bf16x8 pb[4];
+#pragma unroll
+            for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+                for (int h = 0; h < 2; ++h) {
+                    uint32_t w[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float p0 = fast_exp2(__builtin_fmaf(sacc[mb][h * 8 + 2 * e], c2, -m2));
+                        const float p1 = fast_exp2(__builtin_fmaf(sacc[mb][h * 8 + 2 * e + 1], c2, -m2));
+                        lsum += p0 + p1;
+                        w[e] = pack_bf16(p0, p1);
+                    }
+                    pb[mb * 2 + h] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+                }
+#pragma unroll
+            for (int db = 0; db < DB; ++db) {
+                const int d = db * 32 + l32;
+                const int swz = vt_swizzle(d);
+#pragma unroll
+                for (int kk = 0; kk < 4; ++kk) {
+                    const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
+                        &sv[buf][d * kBN + (((kk * 2 + hi) ^ swz) << 3)]);
+                    oacc[db] = mfma32(a, pb[kk], oacc[db]);
+                }
+            }
+        }
+        if (j + 1 < nkt) store_tile(buf ^ 1);
+        __syncthreads();
+    }
+
+    const float l = lsum + __shfl_xor(lsum, 32);
+    if (row < g.len) {
+        const float inv = 1.f / l;
+        const uint32_t obase = qbase + (uint32_t)row * qstride;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int rq = 0; rq < 4; ++rq) {
+                const int d0 = db * 32 + 8 * rq + 4 * hi;
+                const u32x2 w = {pack_bf16(oacc[db][4 * rq] * inv, oacc[db][4 * rq + 1] * inv),
+                                 pack_bf16(oacc[db][4 * rq + 2] * inv, oacc[db][4 * rq + 3] * inv)};
+                st8(ro, obase + d0 * 2, w);
+            }
+        if (hi == 0) {
+            const size_t li = ((size_t)b * g.Hq + hq) * g.N + (size_t)row * g.rowmul + s;
+            lse[li] = (m2 + log2f(l)) * 0.6931471805599453f;
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_fwd_bf16(const void *q, const void *k, const void *v, void *o, float *lse,
+                           const SfaGeom &g, hipStream_t s)
+{
+    const int ntiles = (g.len + kBM - 1) / kBM;
+    const int nprob = g.B * g.Hq * g.streams;
+    const dim3 grid(ntiles * nprob), block(256);
+    const bf16 *qq = static_cast<const bf16 *>(q), *kk = static_cast<const bf16 *>(k),
+               *vv = static_cast<const bf16 *>(v);
+    bf16 *oo = static_cast<bf16 *>(o);
+    switch (g.D) {
+    case 32:
+        timing_before("sfa_fwd_bf16_d32", s);
+        sfa_fwd_bf16_kernel<32><<<grid, block, 0, s>>>(qq, kk, vv, oo, lse, g);
+        break;
+    case 64:
+        timing_before("sfa_fwd_bf16_d64", s);
+        sfa_fwd_bf16_kernel<64><<<grid, block, 0, s>>>(qq, kk, vv, oo, lse, g);
+        break;
+    default:
+        timing_before("sfa_fwd_bf16_d128", s);
+        sfa_fwd_bf16_kernel<128><<<grid, block, 0, s>>>(qq, kk, vv, oo, lse, g);
+        break;
+    }
+    hipError_t e = hipGetLastError();
+    timing_after(s);
+    return e;
+}
+
+}  // namespace hd

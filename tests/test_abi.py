@@ -1,0 +1,119 @@
+"""The C ABI library: it loads, exports every declared symbol, and its host-side
+validation returns the documented status codes before touching the GPU."""
+import ctypes
+import math
+import os
+import re
+
+import pytest
+
+from paper_2607_08186_amd import binding
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hd.h")
+
+FAKE = 0x10000  # aligned fake device addresses: validation fails before any use
+INVALID, UNSUPPORTED = binding.HD_ERR_INVALID_ARG, binding.HD_ERR_UNSUPPORTED
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hd_[a-z_0-9]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return binding.lib()
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(binding.EXPORTS)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings(lib):
+    for code, name in [(0, "HD_OK"), (1, "HD_ERR_INVALID_ARG"), (2, "HD_ERR_UNSUPPORTED"),
+                       (3, "HD_ERR_HIP")]:
+        assert lib.hd_status_str(code).decode() == name
+
+
+def fwd(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, B=1, L=8, n=2, Hq=4, Hkv=2, D=64,
+             mode=0, scale=0.125, dtype=0)
+    a.update(kw)
+    return lib.hd_sfa_fwd(a["q"], a["k"], a["v"], a["o"], a["lse"], a["B"], a["L"], a["n"],
+                          a["Hq"], a["Hkv"], a["D"], a["mode"], a["scale"], a["dtype"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), INVALID), (dict(lse=None), INVALID), (dict(B=0), INVALID),
+    (dict(L=-1), INVALID), (dict(n=0), INVALID), (dict(Hkv=3), INVALID),
+    (dict(Hq=0), INVALID), (dict(scale=float("nan")), INVALID),
+    (dict(scale=float("inf")), INVALID), (dict(scale=-0.1), INVALID), (dict(scale=0.0), INVALID),
+    (dict(mode=2), INVALID), (dict(dtype=7), INVALID), (dict(D=96), UNSUPPORTED),
+    (dict(D=256), UNSUPPORTED), (dict(q=FAKE + 8), INVALID), (dict(lse=FAKE + 4), INVALID),
+    (dict(L=1 << 20, n=64, Hq=64), INVALID),  # per-batch slice beyond 2^31 bytes
+])
+def test_fwd_validation(lib, kw, code):
+    assert fwd(lib, **kw) == code
+    assert lib.hd_last_error().decode() != ""
+
+
+def bwd(lib, ws_bytes=None, ws=FAKE * 16, **kw):
+    a = dict(B=1, L=8, n=2, Hq=4, Hkv=2, D=64, mode=1, scale=0.125, dtype=0)
+    a.update(kw)
+    need = lib.hd_sfa_bwd_workspace_bytes(a["B"], a["L"], a["n"], a["Hq"], a["Hkv"], a["D"],
+                                          a["mode"], a["dtype"])
+    ptrs = [FAKE] * 9
+    for i, name in enumerate(["q", "k", "v", "o", "lse", "dO", "dq", "dk", "dv"]):
+        if name in kw:
+            ptrs[i] = kw[name]
+    return lib.hd_sfa_bwd(*ptrs, a["B"], a["L"], a["n"], a["Hq"], a["Hkv"], a["D"], a["mode"],
+                          a["scale"], a["dtype"], ws, need if ws_bytes is None else ws_bytes,
+                          None), need
+
+
+def test_workspace_size_formula(lib):
+    need = lib.hd_sfa_bwd_workspace_bytes(2, 100, 3, 4, 2, 64, 0, 0)
+    rows = 2 * 4 * 300
+    assert need == 2 * (math.ceil(rows * 4 / 256) * 256)
+    assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 3, 64, 0, 0) == 0  # Hq % Hkv
+    assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 2, 48, 0, 0) == 0  # D
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(dq=None), INVALID), (dict(dO=None), INVALID), (dict(ws=None), INVALID),
+    (dict(ws=FAKE * 16 + 16), INVALID), (dict(ws_bytes=16), INVALID), (dict(D=48), UNSUPPORTED),
+    (dict(dk=FAKE + 2), INVALID), (dict(Hkv=0), INVALID),
+])
+def test_bwd_validation(lib, kw, code):
+    st, _ = bwd(lib, **kw)
+    assert st == code
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(ids=None), INVALID), (dict(B=0), INVALID), (dict(V=0), INVALID),
+    (dict(V=1 << 40), INVALID), (dict(Dm=0), INVALID), (dict(dtype=5), INVALID),
+    (dict(out=FAKE + 8), INVALID), (dict(bad=FAKE + 2), INVALID),
+])
+def test_expand_validation(lib, args, code):
+    a = dict(ids=FAKE, tables=FAKE, out=FAKE, B=1, L=4, n=2, V=10, Dm=8, dtype=0, bad=None)
+    a.update(args)
+    st = lib.hd_expand_embed(a["ids"], a["tables"], a["out"], a["B"], a["L"], a["n"], a["V"],
+                             a["Dm"], a["dtype"], a["bad"], None)
+    assert st == code
+
+
+def test_missing_library_raises(monkeypatch, tmp_path):
+    """No silent fallback: a missing libhd.so is an ImportError on first use."""
+    monkeypatch.setattr(binding, "_lib", None)
+    monkeypatch.setattr(binding, "LIB_PATH", str(tmp_path / "libhd.so"))
+    with pytest.raises(ImportError):
+        binding.lib()
+
+
+def test_timing_collect_empty(lib):
+    assert binding.hd_timing_collect() == []
