@@ -38,7 +38,21 @@ def parse():
                                                 for m in ("intra", "mix")])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=384)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run a plain device-to-device copy of BYTES (3 times) and exit; "
+                         "used to scale HBM traffic counters")
     return ap.parse_args()
+
+
+def copy_calibration(nbytes):
+    import torch
+
+    src = torch.ones(nbytes // 4, dtype=torch.int32, device="cuda:0")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "launches": 3}))
 
 
 def per_kernel_flops(shape, mode):
@@ -65,6 +79,10 @@ def main():
         print("bench.py measures one GPU only: this build has no multi-GPU path "
               "(every run here uses a single MI355X); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
 
     import torch
 
