@@ -5,42 +5,43 @@
 //   P = exp2(scale*log2(e) q.k - lse2),  dP = dO V^T,  dS = P (dP - Delta),
 //   dV = P^T dO,  dK = scale dS^T Q,  dQ = scale dS K,   Delta = rowsum(dO * O).
 // Two deterministic kernels (no atomics):
-//   dK/dV: a workgroup owns 128 keys of one (b, kv-head[, stream]) problem, 32 per wave,
-//          and sweeps the query tiles that see them for every query head of the group,
-//          so the grouped-query sum happens in registers.  Scores are formed as
+//   dK/dV: a workgroup owns 128 keys of one (b, kv-head[, stream]) problem (K and V
+//          resident in LDS), 32 per pair of waves, and sweeps the query tiles that see
+//          them for every query head of the group, so the grouped-query sum happens in
+//          registers; the two waves of a pair split each query tile and add their
+//          partials once at the end.  Scores are formed as
 //          S = Q K^T (one key per lane), which makes P and dS the B operands of
-//          dV^T += dO^T P and dK^T += Q^T dS; Q and dO are staged in LDS both
-//          row-major and transposed.
-//   dQ:    a workgroup owns 128 query rows (32 per wave, one row per lane as in the
+//          dV^T += dO^T P and dK^T += Q^T dS; Q and dO tiles are staged row-major and
+//          read transposed for those two products.
+//   dQ:    a workgroup owns 256 query rows (32 per wave, one row per lane as in the
 //          forward) and sweeps the key tiles at or below the diagonal:
 //          S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T.
-#include "sfa_tiles.h"
+// All tiles move HBM -> LDS through direct-to-LDS buffer loads into double buffers.
+#include "sfa_lds.h"
 
 namespace hd {
 
 namespace {
 
-constexpr int kKeysPerWg = 128;
-constexpr int kRowsPerWg = 128;
+constexpr int kKeysPerWg = 128;  // dK/dV: 4 key groups of 32, each shared by 2 waves
+constexpr int kDkdvWaves = 8;
+constexpr int kDqWaves = 8;
+constexpr int kRowsPerWg = kDqWaves * 32;  // dQ: 8 waves x 32 rows
 
 template <int D>
-struct DkdvLds {
-    static constexpr int RM = kTileRows * (D + 8);  // elements
-    static constexpr int TR = D * kTileRows;
-    static constexpr int Q_RM = 0, DO_RM = RM, Q_TR = 2 * RM, DO_TR = 2 * RM + TR;
-    static constexpr int ELEMS = 2 * RM + 2 * TR;
-    static constexpr int BYTES = ELEMS * 2 + 2 * kTileRows * 4;  // + lse2, delta
-};
-
-template <int D>
-__global__ __launch_bounds__(256, 1) void sfa_dkdv_bf16_kernel(
+__global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
     const bf16 *__restrict__ dO, const float *__restrict__ delta, const float *__restrict__ lse2,
     bf16 *__restrict__ dk, bf16 *__restrict__ dv, SfaGeom g)
 {
-    constexpr int KS = D / 16, DB = D / 32;
-    using LY = DkdvLds<D>;
-    __shared__ __attribute__((aligned(16))) char smem[2][LY::BYTES];
+    constexpr int DB = D / 32, KS = D / 16;
+    using T = Tile<D>;
+    constexpr int STAGE = 2 * T::BYTES + 2 * kRows * 4;       // Q | dO | lse2 | delta
+    constexpr int KV = 2 * (kKeysPerWg / kRows) * T::BYTES;  // K tiles | V tiles
+    constexpr int LDS = 2 * STAGE + KV;
+    static_assert(2 * (kDkdvWaves / 2) * DB * 16 * 64 * 4 <= LDS, "partials must fit in LDS");
+    __shared__ __attribute__((aligned(1024))) char smem[LDS];
+    char *const kvt = smem + 2 * STAGE;
 
     const int nkt = (g.len + kKeysPerWg - 1) / kKeysPerWg;
     const int nprob = g.B * g.Hkv * g.streams;
@@ -51,154 +52,154 @@ __global__ __launch_bounds__(256, 1) void sfa_dkdv_bf16_kernel(
     const int b = prob / (g.streams * g.Hkv);
 
     const size_t qslice = (size_t)g.N * g.Hq * D, kslice = (size_t)g.N * g.Hkv * D;
+    const size_t lslice = (size_t)g.Hq * g.N;
     const rsrc_t rq = make_rsrc(q + b * qslice, (uint32_t)(qslice * 2));
     const rsrc_t rdo = make_rsrc(dO + b * qslice, (uint32_t)(qslice * 2));
     const rsrc_t rk = make_rsrc(k + b * kslice, (uint32_t)(kslice * 2));
     const rsrc_t rv = make_rsrc(v + b * kslice, (uint32_t)(kslice * 2));
     const rsrc_t rdk = make_rsrc(dk + b * kslice, (uint32_t)(kslice * 2));
     const rsrc_t rdv = make_rsrc(dv + b * kslice, (uint32_t)(kslice * 2));
+    const rsrc_t rl2 = make_rsrc(lse2 + b * lslice, (uint32_t)(lslice * 4));
+    const rsrc_t rdl = make_rsrc(delta + b * lslice, (uint32_t)(lslice * 4));
     const uint32_t qstride = (uint32_t)g.rowmul * g.Hq * D * 2;
     const uint32_t kstride = (uint32_t)g.rowmul * g.Hkv * D * 2;
     const uint32_t kbase = (uint32_t)(s * g.Hkv + hk) * D * 2;
 
+    // waves w and w + 4 own the same 32 keys; w takes query rows 0..31 of every
+    // 64-row tile and w + 4 rows 32..63; their dK/dV partials are summed at the end
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l32 = lane & 31, hi = lane >> 5;
+    const int kw = wave & 3, qb = wave >> 2;
     const int k0 = ktile * kKeysPerWg;
-    const int kw0 = k0 + wave * 32;
+    const int kw0 = k0 + kw * 32;
     const int key = kw0 + l32;
 
-    // this lane's key and value rows as B operands
-    bf16x8 kr[KS], vr[KS];
-    {
-        const uint32_t off = key < g.len ? kbase + (uint32_t)key * kstride : kOob;
+    const int qt_first = k0 / kRows;
+    const int qt_end = (g.len + kRows - 1) / kRows;
+    const int nqt = qt_end - qt_first;
+    const int iters = g.G * nqt;
+
+    // this workgroup's 128 keys and values, resident in LDS for the whole sweep
 #pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-            kr[kk] = __builtin_bit_cast(bf16x8, ld16(rk, off + (kk * 16 + hi * 8) * 2));
-            vr[kk] = __builtin_bit_cast(bf16x8, ld16(rv, off + (kk * 16 + hi * 8) * 2));
-        }
+    for (int t = 0; t < kKeysPerWg / kRows; ++t) {
+        T::load(kvt + t * T::BYTES, rk, kbase, kstride, k0 + t * kRows, g.len, wave, kDkdvWaves, lane);
+        T::load(kvt + (kKeysPerWg / kRows + t) * T::BYTES, rv, kbase, kstride, k0 + t * kRows,
+                g.len, wave, kDkdvWaves, lane);
     }
+    const char *ktl = kvt + (kw >> 1) * T::BYTES;                              // tile of my keys
+    const char *vtl = kvt + (kKeysPerWg / kRows + (kw >> 1)) * T::BYTES;
+    const int krow = (kw & 1) * 32 + l32;                                      // my key's row there
+
+    auto issue = [&](int it, int st) {
+        const int gi = it / nqt, qt = qt_first + it % nqt;
+        const int hq = hk * g.G + gi;
+        const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
+        const int row0 = qt * kRows;
+        char *base = smem + st * STAGE;
+        T::load(base, rq, qbase, qstride, row0, g.len, wave, kDkdvWaves, lane);
+        T::load(base + T::BYTES, rdo, qbase, qstride, row0, g.len, wave, kDkdvWaves, lane);
+        if (wave < 2) {  // per-row lse2 (wave 0) and delta (wave 1), 4 bytes per lane
+            const int row = row0 + lane;
+            const uint32_t off =
+                row < g.len ? (uint32_t)(((size_t)hq * g.N + (size_t)row * g.rowmul + s) * 4) : kOob;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                wave == 0 ? rl2 : rdl, (lds_void *)(base + 2 * T::BYTES + wave * kRows * 4), 4,
+                off, 0, 0, 0);
+        }
+    };
+    if (iters > 0) issue(0, 0);
 
     f32x16 adk[DB], adv[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) adk[db] = adv[db] = f32x16{};
 
-    const int qt_first = k0 / kTileRows;
-    const int qt_end = (g.len + kTileRows - 1) / kTileRows;
-    const int nqt = qt_end - qt_first;
-    const int iters = g.G * nqt;
-
-    QuadStager<D> stq, stdo;
-    float lrow = 0.f;
-
-    auto prefetch = [&](int it) {
-        const int gi = it / nqt, qt = qt_first + it % nqt;
-        const int hq = hk * g.G + gi;
-        const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
-        const int row0 = qt * kTileRows;
-        stq.load(rq, qbase, qstride, row0, g.len, tid);
-        stdo.load(rdo, qbase, qstride, row0, g.len, tid);
-        if (tid < 2 * kTileRows) {
-            const int row = row0 + (tid & (kTileRows - 1));
-            const size_t li = ((size_t)b * g.Hq + hq) * g.N + (size_t)row * g.rowmul + s;
-            const float *src = tid < kTileRows ? lse2 : delta;
-            lrow = row < g.len ? src[li] : 0.f;
-        }
-    };
-    auto commit = [&](int buf) {
-        bf16 *base = reinterpret_cast<bf16 *>(smem[buf]);
-        stq.store_rm(base + LY::Q_RM, tid);
-        stq.store_tr(base + LY::Q_TR, tid);
-        stdo.store_rm(base + LY::DO_RM, tid);
-        stdo.store_tr(base + LY::DO_TR, tid);
-        if (tid < 2 * kTileRows) reinterpret_cast<float *>(base + LY::ELEMS)[tid] = lrow;
-    };
-
     const float c2 = g.scale_log2;
-    if (iters > 0) {
-        prefetch(0);
-        commit(0);
-    }
+    wait_lds_loads();
     __syncthreads();
 
     for (int it = 0; it < iters; ++it) {
-        const int buf = it & 1;
-        if (it + 1 < iters) prefetch(it + 1);
-        const int qrow0 = (qt_first + it % nqt) * kTileRows;
-        if (qrow0 + kTileRows - 1 >= kw0) {  // wave-uniform: some query sees some key
-            const bf16 *base = reinterpret_cast<const bf16 *>(smem[buf]);
-            const float *sl = reinterpret_cast<const float *>(base + LY::ELEMS);
-            const float *sdl = sl + kTileRows;
-            f32x16 sacc[2], pacc[2];
+        const int st = it & 1;
+        if (it + 1 < iters) issue(it + 1, st ^ 1);
+        const int qlo = (qt_first + it % nqt) * kRows + qb * 32;
+        if (qlo + 31 >= kw0) {  // wave-uniform: some of my 32 queries see some of my keys
+            const char *qt = smem + st * STAGE;
+            const char *dot = qt + T::BYTES;
+            const float *sl = reinterpret_cast<const float *>(qt + 2 * T::BYTES) + qb * 32;
+            const float *sdl = sl + kRows;
+            f32x16 sacc = f32x16{}, pacc = f32x16{};
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb) {
-                sacc[qb] = f32x16{};
-                pacc[qb] = f32x16{};
-#pragma unroll
-                for (int kk = 0; kk < KS; ++kk) {
-                    sacc[qb] = mfma32(rm_operand<D>(base + LY::Q_RM, qb * 32 + l32, kk, hi), kr[kk],
-                                      sacc[qb]);
-                    pacc[qb] = mfma32(rm_operand<D>(base + LY::DO_RM, qb * 32 + l32, kk, hi),
-                                      vr[kk], pacc[qb]);
-                }
+            for (int kk = 0; kk < KS; ++kk) {
+                sacc = mfma32(T::row_operand(qt, qb * 32 + l32, kk, hi),
+                              T::row_operand(ktl, krow, kk, hi), sacc);
+                pacc = mfma32(T::row_operand(dot, qb * 32 + l32, kk, hi),
+                              T::row_operand(vtl, krow, kk, hi), pacc);
             }
-            const bool need_mask = qrow0 < kw0 + 31;
-            bf16x8 pb[4], dsb[4];
+            const bool need_mask = qlo < kw0 + 31;
+            uint32_t pw[8], dw[8];
 #pragma unroll
-            for (int qb = 0; qb < 2; ++qb) {
-                uint32_t pw[8], dw[8];
+            for (int rq = 0; rq < 4; ++rq) {
+                const f32x4 l4 = *reinterpret_cast<const f32x4 *>(&sl[8 * rq + 4 * hi]);
+                const f32x4 d4 = *reinterpret_cast<const f32x4 *>(&sdl[8 * rq + 4 * hi]);
+                float p[4], ds[4];
 #pragma unroll
-                for (int rq = 0; rq < 4; ++rq) {
-                    const f32x4 l4 = *reinterpret_cast<const f32x4 *>(&sl[qb * 32 + 8 * rq + 4 * hi]);
-                    const f32x4 d4 = *reinterpret_cast<const f32x4 *>(&sdl[qb * 32 + 8 * rq + 4 * hi]);
-                    float p[4], ds[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int r = rq * 4 + e;
-                        p[e] = fast_exp2(__builtin_fmaf(sacc[qb][r], c2, -l4[e]));
-                        if (need_mask) {
-                            const int query = qrow0 + qb * 32 + 8 * rq + 4 * hi + e;
-                            if (query < key) p[e] = 0.f;
-                        }
-                        ds[e] = p[e] * (pacc[qb][r] - d4[e]);
-                    }
-                    pw[rq * 2] = pack_bf16(p[0], p[1]);
-                    pw[rq * 2 + 1] = pack_bf16(p[2], p[3]);
-                    dw[rq * 2] = pack_bf16(ds[0], ds[1]);
-                    dw[rq * 2 + 1] = pack_bf16(ds[2], ds[3]);
+                for (int e = 0; e < 4; ++e) {
+                    const int r = rq * 4 + e;
+                    p[e] = fast_exp2(__builtin_fmaf(sacc[r], c2, -l4[e]));
+                    if (need_mask && qlo + 8 * rq + 4 * hi + e < key) p[e] = 0.f;
+                    ds[e] = p[e] * (pacc[r] - d4[e]);
                 }
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    pb[qb * 2 + h] = __builtin_bit_cast(
-                        bf16x8, u32x4{pw[h * 4], pw[h * 4 + 1], pw[h * 4 + 2], pw[h * 4 + 3]});
-                    dsb[qb * 2 + h] = __builtin_bit_cast(
-                        bf16x8, u32x4{dw[h * 4], dw[h * 4 + 1], dw[h * 4 + 2], dw[h * 4 + 3]});
-                }
+                pw[rq * 2] = pack_bf16(p[0], p[1]);
+                pw[rq * 2 + 1] = pack_bf16(p[2], p[3]);
+                dw[rq * 2] = pack_bf16(ds[0], ds[1]);
+                dw[rq * 2 + 1] = pack_bf16(ds[2], ds[3]);
             }
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const int d = db * 32 + l32;
+            for (int h = 0; h < 2; ++h) {
+                const bf16x8 pb = __builtin_bit_cast(
+                    bf16x8, u32x4{pw[h * 4], pw[h * 4 + 1], pw[h * 4 + 2], pw[h * 4 + 3]});
+                const bf16x8 dsb = __builtin_bit_cast(
+                    bf16x8, u32x4{dw[h * 4], dw[h * 4 + 1], dw[h * 4 + 2], dw[h * 4 + 3]});
+                const int kk = qb * 2 + h;  // 16-row group of the 64-row tile
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
-                    adv[db] = mfma32(tr_operand(base + LY::DO_TR, d, kk, hi), pb[kk], adv[db]);
-                    adk[db] = mfma32(tr_operand(base + LY::Q_TR, d, kk, hi), dsb[kk], adk[db]);
+                for (int db = 0; db < DB; ++db) {
+                    adv[db] = mfma32(T::tr_operand(dot, db * 32, kk, lane), pb, adv[db]);
+                    adk[db] = mfma32(T::tr_operand(qt, db * 32, kk, lane), dsb, adk[db]);
                 }
             }
         }
-        if (it + 1 < iters) commit(buf ^ 1);
+        wait_lds_loads();
         __syncthreads();
     }
 
-    if (key < g.len) {
+    // sum the two query halves: waves 4..7 park their partials in LDS (one 16-byte
+    // slot per lane and register quad), waves 0..3 add them and write dK/dV
+    f32x4 *park = reinterpret_cast<f32x4 *>(smem) + kw * (2 * DB * 4 * 64);
+    if (qb == 1) {
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int r4 = 0; r4 < 4; ++r4) {
+                park[((0 * DB + db) * 4 + r4) * 64 + lane] =
+                    f32x4{adk[db][4 * r4], adk[db][4 * r4 + 1], adk[db][4 * r4 + 2], adk[db][4 * r4 + 3]};
+                park[((1 * DB + db) * 4 + r4) * 64 + lane] =
+                    f32x4{adv[db][4 * r4], adv[db][4 * r4 + 1], adv[db][4 * r4 + 2], adv[db][4 * r4 + 3]};
+            }
+    }
+    __syncthreads();
+    if (qb == 0 && key < g.len) {
         const uint32_t off = kbase + (uint32_t)key * kstride;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
             for (int rq = 0; rq < 4; ++rq) {
+                const f32x4 pk = park[((0 * DB + db) * 4 + rq) * 64 + lane];
+                const f32x4 pv = park[((1 * DB + db) * 4 + rq) * 64 + lane];
                 const int d0 = db * 32 + 8 * rq + 4 * hi;
-                const u32x2 wk = {pack_bf16(adk[db][4 * rq] * g.scale, adk[db][4 * rq + 1] * g.scale),
-                                  pack_bf16(adk[db][4 * rq + 2] * g.scale, adk[db][4 * rq + 3] * g.scale)};
-                const u32x2 wv = {pack_bf16(adv[db][4 * rq], adv[db][4 * rq + 1]),
-                                  pack_bf16(adv[db][4 * rq + 2], adv[db][4 * rq + 3])};
+                const float sc = g.scale;
+                const u32x2 wk = {pack_bf16((adk[db][4 * rq] + pk[0]) * sc, (adk[db][4 * rq + 1] + pk[1]) * sc),
+                                  pack_bf16((adk[db][4 * rq + 2] + pk[2]) * sc, (adk[db][4 * rq + 3] + pk[3]) * sc)};
+                const u32x2 wv = {pack_bf16(adv[db][4 * rq] + pv[0], adv[db][4 * rq + 1] + pv[1]),
+                                  pack_bf16(adv[db][4 * rq + 2] + pv[2], adv[db][4 * rq + 3] + pv[3])};
                 st8(rdk, off + d0 * 2, wk);
                 st8(rdv, off + d0 * 2, wv);
             }
@@ -206,22 +207,14 @@ __global__ __launch_bounds__(256, 1) void sfa_dkdv_bf16_kernel(
 }
 
 template <int D>
-struct DqLds {
-    static constexpr int RM = kTileRows * (D + 8);
-    static constexpr int TR = D * kTileRows;
-    static constexpr int K_RM = 0, V_RM = RM, K_TR = 2 * RM;
-    static constexpr int BYTES = (2 * RM + TR) * 2;
-};
-
-template <int D>
-__global__ __launch_bounds__(256, 1) void sfa_dq_bf16_kernel(
+__global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
     const bf16 *__restrict__ dO, const float *__restrict__ delta, const float *__restrict__ lse2,
     bf16 *__restrict__ dq, SfaGeom g)
 {
     constexpr int KS = D / 16, DB = D / 32;
-    using LY = DqLds<D>;
-    __shared__ __attribute__((aligned(16))) char smem[2][LY::BYTES];
+    using T = Tile<D>;
+    __shared__ __attribute__((aligned(1024))) char smem[2][2 * T::BYTES];  // [stage][K | V]
 
     const int ntiles = (g.len + kRowsPerWg - 1) / kRowsPerWg;
     const int nprob = g.B * g.Hq * g.streams;
@@ -248,6 +241,14 @@ __global__ __launch_bounds__(256, 1) void sfa_dq_bf16_kernel(
     const int q0 = tile * kRowsPerWg;
     const int row = q0 + wave * 32 + l32;
 
+    const int kend = min(g.len, q0 + kRowsPerWg);
+    const int nkt = (kend + kRows - 1) / kRows;
+    auto issue = [&](int j, int st) {
+        T::load(smem[st], rk, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
+        T::load(smem[st] + T::BYTES, rv, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
+    };
+    issue(0, 0);
+
     bf16x8 qr[KS], dor[KS];
     float lrow = 0.f, drow = 0.f;
     {
@@ -268,32 +269,18 @@ __global__ __launch_bounds__(256, 1) void sfa_dq_bf16_kernel(
 #pragma unroll
     for (int db = 0; db < DB; ++db) adq[db] = f32x16{};
 
-    const int kend = min(g.len, q0 + kRowsPerWg);
-    const int nkt = (kend + kTileRows - 1) / kTileRows;
-    QuadStager<D> stk, stv;
-    auto prefetch = [&](int j) {
-        stk.load(rk, kbase, kstride, j * kTileRows, g.len, tid);
-        stv.load(rv, kbase, kstride, j * kTileRows, g.len, tid);
-    };
-    auto commit = [&](int buf) {
-        bf16 *base = reinterpret_cast<bf16 *>(smem[buf]);
-        stk.store_rm(base + LY::K_RM, tid);
-        stk.store_tr(base + LY::K_TR, tid);
-        stv.store_rm(base + LY::V_RM, tid);
-    };
-
     const float c2 = g.scale_log2;
     const int wrow_min = q0 + wave * 32, wrow_max = wrow_min + 31;
-    prefetch(0);
-    commit(0);
+    wait_lds_loads();
     __syncthreads();
 
     for (int j = 0; j < nkt; ++j) {
-        const int buf = j & 1;
-        if (j + 1 < nkt) prefetch(j + 1);
-        const int kb0 = j * kTileRows;
+        const int st = j & 1;
+        if (j + 1 < nkt) issue(j + 1, st ^ 1);
+        const int kb0 = j * kRows;
         if (kb0 <= wrow_max) {
-            const bf16 *base = reinterpret_cast<const bf16 *>(smem[buf]);
+            const char *kt = smem[st];
+            const char *vt = smem[st] + T::BYTES;
             f32x16 sacc[2], pacc[2];
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb) {
@@ -301,13 +288,11 @@ __global__ __launch_bounds__(256, 1) void sfa_dq_bf16_kernel(
                 pacc[mb] = f32x16{};
 #pragma unroll
                 for (int kk = 0; kk < KS; ++kk) {
-                    sacc[mb] = mfma32(rm_operand<D>(base + LY::K_RM, mb * 32 + l32, kk, hi), qr[kk],
-                                      sacc[mb]);
-                    pacc[mb] = mfma32(rm_operand<D>(base + LY::V_RM, mb * 32 + l32, kk, hi), dor[kk],
-                                      pacc[mb]);
+                    sacc[mb] = mfma32(T::row_operand(kt, mb * 32 + l32, kk, hi), qr[kk], sacc[mb]);
+                    pacc[mb] = mfma32(T::row_operand(vt, mb * 32 + l32, kk, hi), dor[kk], pacc[mb]);
                 }
             }
-            const bool need_mask = kb0 + kTileRows - 1 > wrow_min;
+            const bool need_mask = kb0 + kRows - 1 > wrow_min;
             bf16x8 dsb[4];
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
@@ -332,14 +317,12 @@ __global__ __launch_bounds__(256, 1) void sfa_dq_bf16_kernel(
                     dsb[mb * 2 + h] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
                 }
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const int d = db * 32 + l32;
+            for (int db = 0; db < DB; ++db)
 #pragma unroll
                 for (int kk = 0; kk < 4; ++kk)
-                    adq[db] = mfma32(tr_operand(base + LY::K_TR, d, kk, hi), dsb[kk], adq[db]);
-            }
+                    adq[db] = mfma32(T::tr_operand(kt, db * 32, kk, lane), dsb[kk], adq[db]);
         }
-        if (j + 1 < nkt) commit(buf ^ 1);
+        wait_lds_loads();
         __syncthreads();
     }
 
@@ -364,14 +347,14 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *d
 {
     const int nqt = (g.len + kRowsPerWg - 1) / kRowsPerWg;
     timing_before(dq_name, s);
-    sfa_dq_bf16_kernel<D><<<nqt * g.B * g.Hq * g.streams, 256, 0, s>>>(q, k, v, dO, delta, lse2,
-                                                                        dq, g);
+    sfa_dq_bf16_kernel<D><<<nqt * g.B * g.Hq * g.streams, kDqWaves * 64, 0, s>>>(
+        q, k, v, dO, delta, lse2, dq, g);
     hipError_t e = hipGetLastError();
     timing_after(s);
     if (e != hipSuccess) return e;
     const int nkt = (g.len + kKeysPerWg - 1) / kKeysPerWg;
     timing_before(dkdv_name, s);
-    sfa_dkdv_bf16_kernel<D><<<nkt * g.B * g.Hkv * g.streams, 256, 0, s>>>(q, k, v, dO, delta,
+    sfa_dkdv_bf16_kernel<D><<<nkt * g.B * g.Hkv * g.streams, kDkdvWaves * 64, 0, s>>>(q, k, v, dO, delta,
                                                                            lse2, dk, dv, g);
     e = hipGetLastError();
     timing_after(s);

@@ -1,49 +1,41 @@
 // sfa_fwd_bf16.hip -- Stream-Factorized Attention forward, bf16 in/out, fp32 softmax.
 //
 // Computes, per causal problem (see SfaGeom), O = softmax(scale Q K^T + mask) V and the
-// natural-log row log-sum-exp, the forward of the intra-stream layer (eq. (mask_intra))
+// natural-log row log-sum-exp: the forward of the intra-stream layer (eq. (mask_intra))
 // and of the full cross-stream layer (causal mask of Fig. "masks"(a)).
 //
 // Tiling (gfx950, wave64):
-//   workgroup = 4 waves = 128 query rows of one problem; wave w owns rows 32w..32w+31.
-//   Each lane keeps one query row (column l%32 of the MFMA results): the transposed
-//   score tile S^T = K Q^T (keys x queries) puts a row's scores in one lane, so the
-//   row max / row sum need a single cross-half exchange, and P^T feeds the second
+//   workgroup = 8 waves = 256 query rows of one problem (two waves per SIMD); wave w
+//   owns rows 32w..32w+31 and each lane keeps one query row (column l%32 of the MFMA
+//   results).  The transposed score tile S^T = K Q^T puts a row's scores in one lane,
+//   so the row max / row sum need one cross-half exchange, and P^T feeds the second
 //   MFMA (O^T += V^T P^T) straight from registers.
-//   Key tiles of 64 rows are staged in LDS, double buffered: K row-major (padded) and
-//   V transposed (V^T, keys contiguous per head-dim row, XOR-swizzled 16-byte chunks).
-//   Only tiles at or below the diagonal are visited; the causal mask is applied on the
-//   diagonal tiles alone.  The running max is refreshed only when it grows by more
+//   Key/value tiles of 64 rows are loaded HBM -> LDS by direct-to-LDS buffer loads
+//   into a double buffer (one barrier per tile); K is read row-wise, V through
+//   transposed LDS reads, both from the same swizzled row-major layout.
+//   Only tiles at or below a wave's diagonal are computed; the causal mask is applied
+//   on diagonal tiles alone.  The running max is refreshed only when it grows by more
 //   than 2^8 (log2 units), so the O rescale is rare; results are exact either way
 //   because the normaliser uses the same reference.
-#include "hd_device.h"
+#include "sfa_lds.h"
 
 namespace hd {
 
 namespace {
 
-constexpr int kBM = 128;  // query rows per workgroup
-constexpr int kBN = 64;   // keys per staged tile
+constexpr int kWaves = 8;
+constexpr int kBM = kWaves * 32;           // query rows per workgroup
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
 
-__device__ inline int vt_swizzle(int d) { return ((d >> 1) ^ (d >> 3)) & 7; }
-
 template <int D>
-__global__ __launch_bounds__(256, 2) void sfa_fwd_bf16_kernel(const bf16 *__restrict__ q,
-                                                              const bf16 *__restrict__ k,
-                                                              const bf16 *__restrict__ v,
-                                                              bf16 *__restrict__ o,
-                                                              float *__restrict__ lse, SfaGeom g)
+__global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
+    const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
+    bf16 *__restrict__ o, float *__restrict__ lse, SfaGeom g)
 {
-    constexpr int KS = D / 16;         // MFMA k-steps over the head dim
-    constexpr int DB = D / 32;         // 32-wide head-dim blocks of O
-    constexpr int CH = D / 8;          // 16-byte chunks per row
-    constexpr int KSTR = D + 8;        // padded K row in LDS (elements)
-    constexpr int KCH = kBN * CH / 256;  // K chunks staged per thread
-    constexpr int VUNITS = (kBN / 4) * CH;  // V staging units of 4 keys x 8 dims
-
-    __shared__ __attribute__((aligned(16))) bf16 sk[2][kBN * KSTR];
-    __shared__ __attribute__((aligned(16))) bf16 sv[2][D * kBN];
+    constexpr int KS = D / 16;  // MFMA k-steps over the head dim
+    constexpr int DB = D / 32;  // 32-wide head-dim blocks of O
+    using T = Tile<D>;
+    __shared__ __attribute__((aligned(1024))) char smem[2][2 * T::BYTES];  // [stage][K | V]
 
     const int ntiles = (g.len + kBM - 1) / kBM;
     const int nprob = g.B * g.Hq * g.streams;
@@ -70,6 +62,14 @@ __global__ __launch_bounds__(256, 2) void sfa_fwd_bf16_kernel(const bf16 *__rest
     const int q0 = tile * kBM;
     const int row = q0 + wave * 32 + l32;
 
+    const int kend = min(g.len, q0 + kBM);
+    const int nkt = (kend + kRows - 1) / kRows;
+    auto issue = [&](int j, int st) {
+        T::load(smem[st], rk, kbase0, kstride, j * kRows, g.len, wave, kWaves, lane);
+        T::load(smem[st] + T::BYTES, rv, kbase0, kstride, j * kRows, g.len, wave, kWaves, lane);
+    };
+    issue(0, 0);
+
     // this lane's query row as the B operand of S^T = K Q^T
     bf16x8 qr[KS];
     {
@@ -85,84 +85,28 @@ __global__ __launch_bounds__(256, 2) void sfa_fwd_bf16_kernel(const bf16 *__rest
     float m2 = -INFINITY;  // reference max in log2 units
     float lsum = 0.f;      // this lane half's share of the row sum
 
-    const int kend = min(g.len, q0 + kBM);
-    const int nkt = (kend + kBN - 1) / kBN;
-
-    u32x4 kreg[KCH];
-    u32x4 vreg[4];
-
-    auto load_tile = [&](int j) {
-#pragma unroll
-        for (int c = 0; c < KCH; ++c) {
-            const int idx = tid + c * 256, r = idx / CH, ch = idx % CH;
-            const int key = j * kBN + r;
-            const uint32_t off = key < g.len ? kbase0 + (uint32_t)key * kstride + ch * 16 : kOob;
-            kreg[c] = ld16(rk, off);
-        }
-        if (tid < VUNITS) {
-            const int ch = tid % CH, kq = tid / CH;
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int key = j * kBN + kq * 4 + r;
-                const uint32_t off =
-                    key < g.len ? kbase0 + (uint32_t)key * kstride + ch * 16 : kOob;
-                vreg[r] = ld16(rv, off);
-            }
-        }
-    };
-
-    auto store_tile = [&](int buf) {
-#pragma unroll
-        for (int c = 0; c < KCH; ++c) {
-            const int idx = tid + c * 256, r = idx / CH, ch = idx % CH;
-            *reinterpret_cast<u32x4 *>(&sk[buf][r * KSTR + ch * 8]) = kreg[c];
-        }
-        if (tid < VUNITS) {
-            const int ch = tid % CH, kq = tid / CH;
-            const int pos = swap23(kq * 4);  // keys kq*4 .. +3 land on pos .. pos+3
-            const int c16 = pos >> 3, within = pos & 7;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                const int d = ch * 8 + e;
-                const int w = e >> 1;
-                uint32_t lo, hi2;
-                if ((e & 1) == 0) {
-                    lo = (vreg[0][w] & 0xffffu) | (vreg[1][w] << 16);
-                    hi2 = (vreg[2][w] & 0xffffu) | (vreg[3][w] << 16);
-                } else {
-                    lo = (vreg[0][w] >> 16) | (vreg[1][w] & 0xffff0000u);
-                    hi2 = (vreg[2][w] >> 16) | (vreg[3][w] & 0xffff0000u);
-                }
-                const int phys = d * kBN + ((c16 ^ vt_swizzle(d)) << 3) + within;
-                *reinterpret_cast<u32x2 *>(&sv[buf][phys]) = u32x2{lo, hi2};
-            }
-        }
-    };
-
     const float c2 = g.scale_log2;
     const int wrow_min = q0 + wave * 32, wrow_max = wrow_min + 31;
 
-    load_tile(0);
-    store_tile(0);
+    wait_lds_loads();
     __syncthreads();
 
     for (int j = 0; j < nkt; ++j) {
-        const int buf = j & 1;
-        if (j + 1 < nkt) load_tile(j + 1);
-        const int kbase = j * kBN;
+        const int st = j & 1;
+        if (j + 1 < nkt) issue(j + 1, st ^ 1);
+        const int kbase = j * kRows;
         if (kbase <= wrow_max) {  // wave-uniform: tile holds keys visible to this wave
+            const char *kt = smem[st];
+            const char *vt = smem[st] + T::BYTES;
             f32x16 sacc[2];
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb) {
                 sacc[mb] = f32x16{};
 #pragma unroll
-                for (int kk = 0; kk < KS; ++kk) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
-                        &sk[buf][(mb * 32 + l32) * KSTR + kk * 16 + hi * 8]);
-                    sacc[mb] = mfma32(a, qr[kk], sacc[mb]);
-                }
+                for (int kk = 0; kk < KS; ++kk)
+                    sacc[mb] = mfma32(T::row_operand(kt, mb * 32 + l32, kk, hi), qr[kk], sacc[mb]);
             }
-            if (kbase + kBN - 1 > wrow_min) {  // diagonal tile: causal mask
+            if (kbase + kRows - 1 > wrow_min) {  // diagonal tile: causal mask
 #pragma unroll
                 for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -201,18 +145,12 @@ __global__ __launch_bounds__(256, 2) void sfa_fwd_bf16_kernel(const bf16 *__rest
                     pb[mb * 2 + h] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
                 }
 #pragma unroll
-            for (int db = 0; db < DB; ++db) {
-                const int d = db * 32 + l32;
-                const int swz = vt_swizzle(d);
+            for (int db = 0; db < DB; ++db)
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk) {
-                    const bf16x8 a = *reinterpret_cast<const bf16x8 *>(
-                        &sv[buf][d * kBN + (((kk * 2 + hi) ^ swz) << 3)]);
-                    oacc[db] = mfma32(a, pb[kk], oacc[db]);
-                }
-            }
+                for (int kk = 0; kk < 4; ++kk)
+                    oacc[db] = mfma32(T::tr_operand(vt, db * 32, kk, lane), pb[kk], oacc[db]);
         }
-        if (j + 1 < nkt) store_tile(buf ^ 1);
+        wait_lds_loads();
         __syncthreads();
     }
 
@@ -243,7 +181,7 @@ hipError_t launch_fwd_bf16(const void *q, const void *k, const void *v, void *o,
 {
     const int ntiles = (g.len + kBM - 1) / kBM;
     const int nprob = g.B * g.Hq * g.streams;
-    const dim3 grid(ntiles * nprob), block(256);
+    const dim3 grid(ntiles * nprob), block(kWaves * 64);
     const bf16 *qq = static_cast<const bf16 *>(q), *kk = static_cast<const bf16 *>(k),
                *vv = static_cast<const bf16 *>(v);
     bf16 *oo = static_cast<bf16 *>(o);

@@ -1,0 +1,92 @@
+// sfa_lds.h -- 64-row bf16 tiles staged HBM -> LDS by direct-to-LDS buffer loads, and
+// the MFMA operand reads from them.
+//
+// Tile layout: 64 rows (consecutive rows of one causal problem; the row stride in HBM
+// is free, so intra-stream rows at stride n are gathered directly) x D bf16, row-major,
+// D*2 bytes per row with no padding.  Inside a row the 16-byte chunks are permuted:
+// logical chunk c of row r sits at physical chunk c ^ swz(r), with
+//   swz(r) = ((r & 7) << 1) | ((r >> 3) & 1)   (mod chunks per row).
+// This keeps both read patterns bank-conflict free on 64 x 4-byte banks:
+//   * row reads (16 lanes = 16 consecutive rows, same logical chunk, 16 bytes each):
+//     swz is a bijection on r & 15, so the 16 physical chunks are distinct;
+//   * transposed reads (ds_read_b64_tr_b16: 16 lanes cover 4 consecutive rows x 2
+//     adjacent chunks, 8 bytes each): swz(r) >> 1 differs across any 4 aligned rows, so
+//     the 8 (row, chunk) pieces land on distinct chunks.
+// A direct-to-LDS load writes 64 lanes x 16 bytes to consecutive LDS slots; each lane
+// picks the HBM chunk that belongs in its slot, which realises the permutation.
+#pragma once
+
+#include "hd_device.h"
+
+namespace hd {
+
+constexpr int kRows = 64;  // rows per staged tile
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void lds_void;
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+__device__ inline int chunk_swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
+
+template <int D>
+struct Tile {
+    static constexpr int CH = D / 8;              // 16-byte chunks per row
+    static constexpr int BYTES = kRows * D * 2;   // one tile
+    static constexpr int INSTR = kRows * CH / 64; // direct-to-LDS instructions per tile
+
+    // byte offset of element (row, col) inside the tile
+    __device__ static inline int offset(int row, int col)
+    {
+        const int c = (col >> 3) ^ (chunk_swz(row) & (CH - 1));
+        return row * (D * 2) + c * 16 + (col & 7) * 2;
+    }
+
+    // Issue this wave's share of the direct-to-LDS loads of rows row0 .. row0+63 of a
+    // problem whose row r lives at byte base + r*stride of buffer `rs`; rows >= len
+    // load zeros.  Waves wave, wave+nwaves, ... take the tile's INSTR instructions.
+    __device__ static inline void load(char *lds_tile, rsrc_t rs, uint32_t base,
+                                       uint32_t stride, int row0, int len, int wave,
+                                       int nwaves, int lane)
+    {
+#pragma unroll
+        for (int t = wave; t < INSTR; t += nwaves) {
+            const int slot = t * 64 + lane;
+            const int row = slot / CH;
+            const int c = (slot % CH) ^ (chunk_swz(row) & (CH - 1));
+            const int grow = row0 + row;
+            const uint32_t off = grow < len ? base + (uint32_t)grow * stride + c * 16 : kOob;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(
+                rs, (lds_void *)(lds_tile + t * 1024), 16, off, 0, 0, 0);
+        }
+    }
+
+    // MFMA operand whose k-slots run along D: row `row`, dims kk*16 + half*8 .. +7
+    __device__ static inline bf16x8 row_operand(const char *lds_tile, int row, int kk, int half)
+    {
+        const int c = (kk * 2 + half) ^ (chunk_swz(row) & (CH - 1));
+        return *reinterpret_cast<const bf16x8 *>(lds_tile + row * (D * 2) + c * 16);
+    }
+
+    // MFMA operand whose k-slots run along the tile rows, for output row (dim)
+    // d = d0 + (lane % 32): the rows of 16-row group kk that lane half `half` of an MFMA
+    // result block holds, i.e. rows kk*16 + 4*half + {0..3} and kk*16 + 8 + 4*half +
+    // {0..3}.  Two transposed 8-byte reads: in each 16-lane group, lane i returns element
+    // i%4 of the 4-element pieces addressed by lanes i/4, i/4+4, i/4+8, i/4+12.
+    __device__ static inline bf16x8 tr_operand(const char *lds_tile, int d0, int kk, int lane)
+    {
+        const int s = lane & 15, g = lane >> 4, half = g >> 1;
+        const int col = d0 + 16 * (g & 1) + 4 * (s & 3);
+        const int row = kk * 16 + 4 * half + (s >> 2);
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_v4i16 *)(lds_tile + offset(row, col)));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_v4i16 *)(lds_tile + offset(row + 8, col)));
+        const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+        return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], b[0], b[1]});
+    }
+};
+
+// Wait until every direct-to-LDS load this wave issued has landed.
+__device__ inline void wait_lds_loads() { __builtin_amdgcn_s_waitcnt(0); }
+
+}  // namespace hd
