@@ -190,7 +190,8 @@ size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
     hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, 1.0f, dtype);
     memcpy(g_err, saved, sizeof g_err);
     if (st != HD_OK) return 0;
-    return hd::bwd_workspace_bytes(hd::make_geom(B, L, n, Hq, Hkv, D, mode, 1.0f));
+    return hd::bwd_workspace_bytes(hd::make_geom(B, L, n, Hq, Hkv, D, mode, 1.0f),
+                                   dtype == HD_DTYPE_BF16 ? 2 : 4);
 }
 
 hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *o,
@@ -208,7 +209,7 @@ hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *
         !aligned16(dO) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
         return fail(HD_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
     const hd::SfaGeom g = hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale);
-    const size_t need = hd::bwd_workspace_bytes(g);
+    const size_t need = hd::bwd_workspace_bytes(g, dtype == HD_DTYPE_BF16 ? 2 : 4);
     if (!workspace) return fail(HD_ERR_INVALID_ARG, "null workspace (%zu bytes needed)", need);
     if (reinterpret_cast<uintptr_t>(workspace) & 255)
         return fail(HD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");

@@ -15,8 +15,11 @@
 //          read transposed for those two products.
 //   dQ:    a workgroup owns 256 query rows (32 per wave, one row per lane as in the
 //          forward) and sweeps the key tiles at or below the diagonal:
-//          S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T.
+//          S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T, with K^T read from the
+//          transposed copy in the workspace.
 // All tiles move HBM -> LDS through direct-to-LDS buffer loads into double buffers.
+#include <type_traits>
+
 #include "sfa_lds.h"
 
 namespace hd {
@@ -26,7 +29,59 @@ namespace {
 constexpr int kKeysPerWg = 128;  // dK/dV: 4 key groups of 32, each shared by 2 waves
 constexpr int kDkdvWaves = 8;
 constexpr int kDqWaves = 8;
-constexpr int kRowsPerWg = kDqWaves * 32;  // dQ: 8 waves x 32 rows
+constexpr int kRowsPerWg = kDqWaves * 32;  // dQ: 8 waves (two per SIMD) x 32 rows
+
+// Transposed copies for the backward: for each problem (b, h, s) and each 64-row tile,
+// rows i of x (expanded position i*rowmul + s, head h) become columns of
+// xt[prob][d][len_pad], position i stored at column swap23(i) of its 16-group; columns
+// past len are zero.  blockIdx.y picks the tensor: 0 = q, 1 = dO (H = Hq), 2 = k (Hkv).
+template <int D>
+__global__ __launch_bounds__(256) void transpose_kernel(const bf16 *__restrict__ q,
+                                                        const bf16 *__restrict__ dO,
+                                                        const bf16 *__restrict__ k,
+                                                        bf16 *__restrict__ qt, bf16 *__restrict__ dot,
+                                                        bf16 *__restrict__ kt, SfaGeom g, int len_pad)
+{
+    constexpr int CH = D / 8;
+    constexpr int STR = D + 2;  // padded LDS row (elements)
+    __shared__ uint16_t sm[kRows * STR];
+    const int which = blockIdx.y;
+    const int H = which == 2 ? g.Hkv : g.Hq;
+    const bf16 *x = which == 0 ? q : which == 1 ? dO : k;
+    bf16 *xt = which == 0 ? qt : which == 1 ? dot : kt;
+    const int ntiles = len_pad / kRows;
+    const int nprob = g.B * H * g.streams;
+    if ((int)blockIdx.x >= nprob * ntiles) return;  // uniform: fewer key/value problems
+    const int tile = blockIdx.x % ntiles, prob = blockIdx.x / ntiles;
+    const int s = prob % g.streams, h = (prob / g.streams) % H, b = prob / (g.streams * H);
+    const size_t slice = (size_t)g.N * H * D;
+    const rsrc_t rx = make_rsrc(x + b * slice, (uint32_t)(slice * 2));
+    const uint32_t stride = (uint32_t)g.rowmul * H * D * 2;
+    const uint32_t base = (uint32_t)(s * H + h) * D * 2;
+    const int tid = threadIdx.x;
+    for (int idx = tid; idx < kRows * CH; idx += 256) {
+        const int r = idx / CH, ch = idx % CH, row = tile * kRows + r;
+        const u32x4 v = ld16(rx, row < g.len ? base + (uint32_t)row * stride + ch * 16 : kOob);
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            sm[r * STR + ch * 8 + 2 * w] = (uint16_t)(v[w] & 0xffffu);
+            sm[r * STR + ch * 8 + 2 * w + 1] = (uint16_t)(v[w] >> 16);
+        }
+    }
+    __syncthreads();
+    bf16 *out = xt + ((size_t)prob * D) * len_pad + (size_t)tile * kRows;
+    for (int idx = tid; idx < D * (kRows / 8); idx += 256) {
+        const int d = idx / (kRows / 8), c = idx % (kRows / 8);
+        uint32_t w[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const uint32_t lo = sm[swap23(c * 8 + 2 * e) * STR + d];
+            const uint32_t hi = sm[swap23(c * 8 + 2 * e + 1) * STR + d];
+            w[e] = lo | (hi << 16);
+        }
+        *reinterpret_cast<u32x4 *>(out + (size_t)d * len_pad + c * 8) = u32x4{w[0], w[1], w[2], w[3]};
+    }
+}
 
 template <int D>
 __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
@@ -67,7 +122,8 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
 
     // waves w and w + 4 own the same 32 keys; w takes query rows 0..31 of every
     // 64-row tile and w + 4 rows 32..63; their dK/dV partials are summed at the end
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
     const int l32 = lane & 31, hi = lane >> 5;
     const int kw = wave & 3, qb = wave >> 2;
     const int k0 = ktile * kKeysPerWg;
@@ -90,7 +146,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const char *vtl = kvt + (kKeysPerWg / kRows + (kw >> 1)) * T::BYTES;
     const int krow = (kw & 1) * 32 + l32;                                      // my key's row there
 
-    auto issue = [&](int it, int st) {
+    auto issue = [&](int it, int st) __attribute__((always_inline)) {
         const int gi = it / nqt, qt = qt_first + it % nqt;
         const int hq = hk * g.G + gi;
         const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
@@ -117,8 +173,33 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     wait_lds_loads();
     __syncthreads();
 
-    for (int it = 0; it < iters; ++it) {
-        const int st = it & 1;
+    // P and dS of my 32 keys x 32 queries, packed as bf16 B operands (two 16-query groups)
+    auto softmax = [&](const f32x16 &sacc, const f32x16 &pacc, const float *sl, const float *sdl,
+                       int qlo, uint32_t (&pw)[8], uint32_t (&dw)[8], auto mask)
+        __attribute__((always_inline)) {
+        constexpr bool kMask = decltype(mask)::value;
+#pragma unroll
+        for (int rq = 0; rq < 4; ++rq) {
+            const f32x4 l4 = *reinterpret_cast<const f32x4 *>(&sl[8 * rq + 4 * hi]);
+            const f32x4 d4 = *reinterpret_cast<const f32x4 *>(&sdl[8 * rq + 4 * hi]);
+            float p[4], ds[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const int r = rq * 4 + e;
+                p[e] = fast_exp2(__builtin_fmaf(sacc[r], c2, -l4[e]));
+                if constexpr (kMask) {
+                    if (qlo + 8 * rq + 4 * hi + e < key) p[e] = 0.f;
+                }
+                ds[e] = p[e] * (pacc[r] - d4[e]);
+            }
+            pw[rq * 2] = pack_bf16(p[0], p[1]);
+            pw[rq * 2 + 1] = pack_bf16(p[2], p[3]);
+            dw[rq * 2] = pack_bf16(ds[0], ds[1]);
+            dw[rq * 2 + 1] = pack_bf16(ds[2], ds[3]);
+        }
+    };
+    auto step = [&](int it, auto stage) __attribute__((always_inline)) {
+        constexpr int st = decltype(stage)::value;
         if (it + 1 < iters) issue(it + 1, st ^ 1);
         const int qlo = (qt_first + it % nqt) * kRows + qb * 32;
         if (qlo + 31 >= kw0) {  // wave-uniform: some of my 32 queries see some of my keys
@@ -134,25 +215,11 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                 pacc = mfma32(T::row_operand(dot, qb * 32 + l32, kk, hi),
                               T::row_operand(vtl, krow, kk, hi), pacc);
             }
-            const bool need_mask = qlo < kw0 + 31;
             uint32_t pw[8], dw[8];
-#pragma unroll
-            for (int rq = 0; rq < 4; ++rq) {
-                const f32x4 l4 = *reinterpret_cast<const f32x4 *>(&sl[8 * rq + 4 * hi]);
-                const f32x4 d4 = *reinterpret_cast<const f32x4 *>(&sdl[8 * rq + 4 * hi]);
-                float p[4], ds[4];
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int r = rq * 4 + e;
-                    p[e] = fast_exp2(__builtin_fmaf(sacc[r], c2, -l4[e]));
-                    if (need_mask && qlo + 8 * rq + 4 * hi + e < key) p[e] = 0.f;
-                    ds[e] = p[e] * (pacc[r] - d4[e]);
-                }
-                pw[rq * 2] = pack_bf16(p[0], p[1]);
-                pw[rq * 2 + 1] = pack_bf16(p[2], p[3]);
-                dw[rq * 2] = pack_bf16(ds[0], ds[1]);
-                dw[rq * 2 + 1] = pack_bf16(ds[2], ds[3]);
-            }
+            if (qlo < kw0 + 31)  // diagonal: causal mask
+                softmax(sacc, pacc, sl, sdl, qlo, pw, dw, std::true_type{});
+            else
+                softmax(sacc, pacc, sl, sdl, qlo, pw, dw, std::false_type{});
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const bf16x8 pb = __builtin_bit_cast(
@@ -169,6 +236,10 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
         }
         wait_lds_loads();
         __syncthreads();
+    };
+    for (int it = 0; it < iters; it += 2) {
+        step(it, std::integral_constant<int, 0>{});
+        if (it + 1 < iters) step(it + 1, std::integral_constant<int, 1>{});
     }
 
     // sum the two query halves: waves 4..7 park their partials in LDS (one 16-byte
@@ -210,11 +281,13 @@ template <int D>
 __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
     const bf16 *__restrict__ dO, const float *__restrict__ delta, const float *__restrict__ lse2,
-    bf16 *__restrict__ dq, SfaGeom g)
+    const bf16 *__restrict__ kt, bf16 *__restrict__ dq, SfaGeom g, int len_pad)
 {
     constexpr int KS = D / 16, DB = D / 32;
     using T = Tile<D>;
-    __shared__ __attribute__((aligned(1024))) char smem[2][2 * T::BYTES];  // [stage][K | V]
+    using TT = TileT<D>;
+    // [stage][K rows | V rows | K transposed]
+    __shared__ __attribute__((aligned(1024))) char smem[2][2 * T::BYTES + TT::BYTES];
 
     const int ntiles = (g.len + kRowsPerWg - 1) / kRowsPerWg;
     const int nprob = g.B * g.Hq * g.streams;
@@ -231,23 +304,29 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const rsrc_t rdq = make_rsrc(dq + b * qslice, (uint32_t)(qslice * 2));
     const rsrc_t rk = make_rsrc(k + b * kslice, (uint32_t)(kslice * 2));
     const rsrc_t rv = make_rsrc(v + b * kslice, (uint32_t)(kslice * 2));
+    const size_t ktslice = (size_t)D * len_pad;  // one key/value problem, transposed
+    const rsrc_t rkt = make_rsrc(kt + ((size_t)(b * g.Hkv + hk) * g.streams + s) * ktslice,
+                                 (uint32_t)(ktslice * 2));
     const uint32_t qstride = (uint32_t)g.rowmul * g.Hq * D * 2;
     const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
     const uint32_t kstride = (uint32_t)g.rowmul * g.Hkv * D * 2;
     const uint32_t kbase = (uint32_t)(s * g.Hkv + hk) * D * 2;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
     const int l32 = lane & 31, hi = lane >> 5;
     const int q0 = tile * kRowsPerWg;
     const int row = q0 + wave * 32 + l32;
 
     const int kend = min(g.len, q0 + kRowsPerWg);
     const int nkt = (kend + kRows - 1) / kRows;
-    auto issue = [&](int j, int st) {
-        T::load(smem[st], rk, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
-        T::load(smem[st] + T::BYTES, rv, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
+    auto issue = [&](int j) __attribute__((always_inline)) {
+        char *st = smem[j & 1];
+        T::load(st, rk, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
+        T::load(st + T::BYTES, rv, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
+        TT::load(st + 2 * T::BYTES, rkt, 0, (uint32_t)len_pad * 2, j * kRows, wave, kDqWaves, lane);
     };
-    issue(0, 0);
+    issue(0);
 
     bf16x8 qr[KS], dor[KS];
     float lrow = 0.f, drow = 0.f;
@@ -274,56 +353,68 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     wait_lds_loads();
     __syncthreads();
 
-    for (int j = 0; j < nkt; ++j) {
-        const int st = j & 1;
-        if (j + 1 < nkt) issue(j + 1, st ^ 1);
-        const int kb0 = j * kRows;
-        if (kb0 <= wrow_max) {
-            const char *kt = smem[st];
-            const char *vt = smem[st] + T::BYTES;
-            f32x16 sacc[2], pacc[2];
+    // dS^T of one 32-key half as two B operands; MASK selects the diagonal variant
+    auto softmax = [&](const f32x16 &sacc, const f32x16 &pacc, int k0, bf16x8 (&dsb)[2], auto mask) {
+        constexpr bool kMask = decltype(mask)::value;
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb) {
-                sacc[mb] = f32x16{};
-                pacc[mb] = f32x16{};
+        for (int h = 0; h < 2; ++h) {
+            uint32_t w[4];
 #pragma unroll
-                for (int kk = 0; kk < KS; ++kk) {
-                    sacc[mb] = mfma32(T::row_operand(kt, mb * 32 + l32, kk, hi), qr[kk], sacc[mb]);
-                    pacc[mb] = mfma32(T::row_operand(vt, mb * 32 + l32, kk, hi), dor[kk], pacc[mb]);
-                }
-            }
-            const bool need_mask = kb0 + kRows - 1 > wrow_min;
-            bf16x8 dsb[4];
+            for (int e = 0; e < 4; ++e) {
+                float ds2[2];
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                for (int h = 0; h < 2; ++h) {
-                    uint32_t w[4];
-#pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        float ds2[2];
-#pragma unroll
-                        for (int u = 0; u < 2; ++u) {
-                            const int r = h * 8 + 2 * e + u;
-                            float p = fast_exp2(__builtin_fmaf(sacc[mb][r], c2, -lrow));
-                            if (need_mask) {
-                                const int kidx = kb0 + mb * 32 + 8 * (r >> 2) + 4 * hi + (r & 3);
-                                if (kidx > row) p = 0.f;
-                            }
-                            ds2[u] = p * (pacc[mb][r] - drow);
-                        }
-                        w[e] = pack_bf16(ds2[0], ds2[1]);
+                for (int u = 0; u < 2; ++u) {
+                    const int r = h * 8 + 2 * e + u;
+                    float p = fast_exp2(__builtin_fmaf(sacc[r], c2, -lrow));
+                    if constexpr (kMask) {
+                        if (k0 + 8 * (r >> 2) + 4 * hi + (r & 3) > row) p = 0.f;
                     }
-                    dsb[mb * 2 + h] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+                    ds2[u] = p * (pacc[r] - drow);
                 }
+                w[e] = pack_bf16(ds2[0], ds2[1]);
+            }
+            dsb[h] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
+        }
+    };
+    // One 64-key tile as two 32-key halves (S^T and dP^T, softmax, dQ^T each), which
+    // keeps registers free for operand prefetch.
+    auto tile_body = [&](const char *ktl, const char *vt, const char *ktt, int kb0, bool diag) __attribute__((always_inline)) {
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            f32x16 sacc = f32x16{}, pacc = f32x16{};
+#pragma unroll
+            for (int kk = 0; kk < KS; ++kk) {
+                sacc = mfma32(T::row_operand(ktl, mb * 32 + l32, kk, hi), qr[kk], sacc);
+                pacc = mfma32(T::row_operand(vt, mb * 32 + l32, kk, hi), dor[kk], pacc);
+            }
+            bf16x8 dsb[2];
+            if (diag)
+                softmax(sacc, pacc, kb0 + mb * 32, dsb, std::true_type{});
+            else
+                softmax(sacc, pacc, kb0 + mb * 32, dsb, std::false_type{});
 #pragma unroll
             for (int db = 0; db < DB; ++db)
 #pragma unroll
-                for (int kk = 0; kk < 4; ++kk)
-                    adq[db] = mfma32(T::tr_operand(kt, db * 32, kk, lane), dsb[kk], adq[db]);
+                for (int h = 0; h < 2; ++h)
+                    adq[db] = mfma32(TT::operand(ktt, db * 32 + l32, mb * 2 + h, hi), dsb[h], adq[db]);
+        }
+    };
+    auto step = [&](int j, auto stage) __attribute__((always_inline)) {
+        constexpr int kSt = decltype(stage)::value;
+        if (j + 1 < nkt) issue(j + 1);
+        const int kb0 = j * kRows;
+        if (kb0 <= wrow_max) {
+            const char *ktl = smem[kSt];
+            const char *vt = ktl + T::BYTES;
+            const char *ktt = ktl + 2 * T::BYTES;
+            tile_body(ktl, vt, ktt, kb0, kb0 + kRows - 1 > wrow_min);  // diagonal: mask
         }
         wait_lds_loads();
         __syncthreads();
+    };
+    for (int j = 0; j < nkt; j += 2) {
+        step(j, std::integral_constant<int, 0>{});
+        if (j + 1 < nkt) step(j + 1, std::integral_constant<int, 1>{});
     }
 
     if (row < g.len) {
@@ -342,14 +433,21 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
 
 template <int D>
 hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *dO,
-                      const float *delta, const float *lse2, bf16 *dq, bf16 *dk, bf16 *dv,
-                      const SfaGeom &g, hipStream_t s, const char *dq_name, const char *dkdv_name)
+                      const float *delta, const float *lse2, bf16 *qt, bf16 *dot, bf16 *kt,
+                      int len_pad, bf16 *dq, bf16 *dk, bf16 *dv, const SfaGeom &g, hipStream_t s,
+                      const char *tr_name, const char *dq_name, const char *dkdv_name)
 {
+    timing_before(tr_name, s);
+    transpose_kernel<D><<<dim3(g.B * g.Hq * g.streams * (len_pad / kRows), 3), 256, 0, s>>>(
+        q, dO, k, qt, dot, kt, g, len_pad);
+    hipError_t e = hipGetLastError();
+    timing_after(s);
+    if (e != hipSuccess) return e;
     const int nqt = (g.len + kRowsPerWg - 1) / kRowsPerWg;
     timing_before(dq_name, s);
     sfa_dq_bf16_kernel<D><<<nqt * g.B * g.Hq * g.streams, kDqWaves * 64, 0, s>>>(
-        q, k, v, dO, delta, lse2, dq, g);
-    hipError_t e = hipGetLastError();
+        q, k, v, dO, delta, lse2, kt, dq, g, len_pad);
+    e = hipGetLastError();
     timing_after(s);
     if (e != hipSuccess) return e;
     const int nkt = (g.len + kKeysPerWg - 1) / kKeysPerWg;
@@ -367,22 +465,25 @@ hipError_t launch_bwd_bf16(const void *q, const void *k, const void *v, const vo
                            const float *lse, const void *dO, void *dq, void *dk, void *dv,
                            const SfaGeom &g, void *ws, hipStream_t s)
 {
-    const size_t half = bwd_workspace_bytes(g) / 2;
-    float *delta = static_cast<float *>(ws);
-    float *lse2 = reinterpret_cast<float *>(static_cast<char *>(ws) + half);
+    const BwdWorkspace w = bwd_workspace(g, 2);
+    char *wsb = static_cast<char *>(ws);
+    float *delta = reinterpret_cast<float *>(wsb + w.delta);
+    float *lse2 = reinterpret_cast<float *>(wsb + w.lse2);
+    bf16 *qt = reinterpret_cast<bf16 *>(wsb + w.qt), *dot = reinterpret_cast<bf16 *>(wsb + w.dot),
+         *kt = reinterpret_cast<bf16 *>(wsb + w.kt);
     hipError_t e = launch_bwd_preprocess(o, dO, lse, delta, lse2, g, 2, s);
     if (e != hipSuccess) return e;
     const bf16 *qq = static_cast<const bf16 *>(q), *kk = static_cast<const bf16 *>(k),
                *vv = static_cast<const bf16 *>(v), *dd = static_cast<const bf16 *>(dO);
     bf16 *gq = static_cast<bf16 *>(dq), *gk = static_cast<bf16 *>(dk), *gv = static_cast<bf16 *>(dv);
     if (g.D == 32)
-        return bwd_bf16_d<32>(qq, kk, vv, dd, delta, lse2, gq, gk, gv, g, s, "sfa_dq_bf16_d32",
-                              "sfa_dkdv_bf16_d32");
+        return bwd_bf16_d<32>(qq, kk, vv, dd, delta, lse2, qt, dot, kt, w.len_pad, gq, gk, gv, g, s,
+                              "sfa_bwd_transpose_d32", "sfa_dq_bf16_d32", "sfa_dkdv_bf16_d32");
     if (g.D == 64)
-        return bwd_bf16_d<64>(qq, kk, vv, dd, delta, lse2, gq, gk, gv, g, s, "sfa_dq_bf16_d64",
-                              "sfa_dkdv_bf16_d64");
-    return bwd_bf16_d<128>(qq, kk, vv, dd, delta, lse2, gq, gk, gv, g, s, "sfa_dq_bf16_d128",
-                           "sfa_dkdv_bf16_d128");
+        return bwd_bf16_d<64>(qq, kk, vv, dd, delta, lse2, qt, dot, kt, w.len_pad, gq, gk, gv, g, s,
+                              "sfa_bwd_transpose_d64", "sfa_dq_bf16_d64", "sfa_dkdv_bf16_d64");
+    return bwd_bf16_d<128>(qq, kk, vv, dd, delta, lse2, qt, dot, kt, w.len_pad, gq, gk, gv, g, s,
+                           "sfa_bwd_transpose_d128", "sfa_dq_bf16_d128", "sfa_dkdv_bf16_d128");
 }
 
 }  // namespace hd

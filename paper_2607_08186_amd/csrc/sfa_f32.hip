@@ -337,9 +337,9 @@ hipError_t launch_bwd_f32(const float *q, const float *k, const float *v, const 
                           const float *lse, const float *dO, float *dq, float *dk, float *dv,
                           const SfaGeom &g, void *ws, hipStream_t s)
 {
-    const size_t half = bwd_workspace_bytes(g) / 2;
-    float *delta = static_cast<float *>(ws);
-    float *lse2 = reinterpret_cast<float *>(static_cast<char *>(ws) + half);
+    const BwdWorkspace w = bwd_workspace(g, 4);
+    float *delta = reinterpret_cast<float *>(static_cast<char *>(ws) + w.delta);
+    float *lse2 = reinterpret_cast<float *>(static_cast<char *>(ws) + w.lse2);
     hipError_t e = launch_bwd_preprocess(o, dO, lse, delta, lse2, g, 4, s);
     if (e != hipSuccess) return e;
     if (g.D == 32) return bwd_f32_d<32>(q, k, v, dO, dq, dk, dv, g, delta, lse2, s);

@@ -17,6 +17,8 @@
 //   on diagonal tiles alone.  The running max is refreshed only when it grows by more
 //   than 2^8 (log2 units), so the O rescale is rare; results are exact either way
 //   because the normaliser uses the same reference.
+#include <type_traits>
+
 #include "sfa_lds.h"
 
 namespace hd {
@@ -25,6 +27,7 @@ namespace {
 
 constexpr int kWaves = 8;
 constexpr int kBM = kWaves * 32;           // query rows per workgroup
+constexpr int kStages = 2;                 // K/V tiles in flight (LDS double buffer)
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
 
 template <int D>
@@ -35,7 +38,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     constexpr int KS = D / 16;  // MFMA k-steps over the head dim
     constexpr int DB = D / 32;  // 32-wide head-dim blocks of O
     using T = Tile<D>;
-    __shared__ __attribute__((aligned(1024))) char smem[2][2 * T::BYTES];  // [stage][K | V]
+    __shared__ __attribute__((aligned(1024))) char smem[kStages][2 * T::BYTES];  // [stage][K | V]
 
     const int ntiles = (g.len + kBM - 1) / kBM;
     const int nprob = g.B * g.Hq * g.streams;
@@ -57,18 +60,24 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     const uint32_t kstride = (uint32_t)g.rowmul * g.Hkv * D * 2;
     const uint32_t kbase0 = (uint32_t)(s * g.Hkv + hk) * D * 2;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
     const int l32 = lane & 31, hi = lane >> 5;
     const int q0 = tile * kBM;
     const int row = q0 + wave * 32 + l32;
 
     const int kend = min(g.len, q0 + kBM);
     const int nkt = (kend + kRows - 1) / kRows;
-    auto issue = [&](int j, int st) {
-        T::load(smem[st], rk, kbase0, kstride, j * kRows, g.len, wave, kWaves, lane);
-        T::load(smem[st] + T::BYTES, rv, kbase0, kstride, j * kRows, g.len, wave, kWaves, lane);
+    auto issue = [&](int j) __attribute__((always_inline)) {
+        char *st = smem[j & 1];
+        T::load(st, rk, kbase0, kstride, j * kRows, g.len, wave, kWaves, lane);
+        T::load(st + T::BYTES, rv, kbase0, kstride, j * kRows, g.len, wave, kWaves, lane);
     };
-    issue(0, 0);
+    // loads this wave issues per tile, and a wait for "tile j has landed" given how
+    // many later tiles were issued after it
+    const int per_tile = 2 * loads_per_wave(T::INSTR, wave, kWaves);
+    auto wait_tile = [&](int later) __attribute__((always_inline)) { wait_vmcnt_le(per_tile * later); };
+    for (int j = 0; j < kStages - 1 && j < nkt; ++j) issue(j);
 
     // this lane's query row as the B operand of S^T = K Q^T
     bf16x8 qr[KS];
@@ -88,16 +97,21 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     const float c2 = g.scale_log2;
     const int wrow_min = q0 + wave * 32, wrow_max = wrow_min + 31;
 
-    wait_lds_loads();
+    wait_tile(min(kStages - 2, nkt - 1));
     __syncthreads();
 
-    for (int j = 0; j < nkt; ++j) {
-        const int st = j & 1;
-        if (j + 1 < nkt) issue(j + 1, st ^ 1);
+    // one key tile; the stage index is a compile-time constant so LDS addresses are a
+    // per-lane base plus an immediate offset
+    auto step = [&](int j, auto stage) __attribute__((always_inline)) {
+        constexpr int kSt = decltype(stage)::value;
+        if (j + kStages - 1 < nkt) issue(j + kStages - 1);
         const int kbase = j * kRows;
         if (kbase <= wrow_max) {  // wave-uniform: tile holds keys visible to this wave
-            const char *kt = smem[st];
-            const char *vt = smem[st] + T::BYTES;
+            const char *kt = smem[kSt];
+            const char *vt = kt + T::BYTES;
+            // MFMA bursts run at raised wave priority, the softmax at normal priority, so
+            // the two waves sharing a SIMD tend to alternate matrix and vector work
+            __builtin_amdgcn_s_setprio(1);
             f32x16 sacc[2];
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb) {
@@ -106,6 +120,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
                 for (int kk = 0; kk < KS; ++kk)
                     sacc[mb] = mfma32(T::row_operand(kt, mb * 32 + l32, kk, hi), qr[kk], sacc[mb]);
             }
+            __builtin_amdgcn_s_setprio(0);
             if (kbase + kRows - 1 > wrow_min) {  // diagonal tile: causal mask
 #pragma unroll
                 for (int mb = 0; mb < 2; ++mb)
@@ -144,14 +159,22 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
                     }
                     pb[mb * 2 + h] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
                 }
+            __builtin_amdgcn_s_setprio(1);
 #pragma unroll
             for (int db = 0; db < DB; ++db)
 #pragma unroll
                 for (int kk = 0; kk < 4; ++kk)
                     oacc[db] = mfma32(T::tr_operand(vt, db * 32, kk, lane), pb[kk], oacc[db]);
+            __builtin_amdgcn_s_setprio(0);
         }
-        wait_lds_loads();
+        // tile j+1 must have landed; tiles j+2 .. j+kStages-1 may still be in flight
+        wait_tile(max(0, min(kStages - 2, nkt - 2 - j)));
         __syncthreads();
+    };
+    static_assert(kStages == 2, "the tile loop below alternates two stages");
+    for (int j = 0; j < nkt; j += 2) {
+        step(j, std::integral_constant<int, 0>{});
+        if (j + 1 < nkt) step(j + 1, std::integral_constant<int, 1>{});
     }
 
     const float l = lsum + __shfl_xor(lsum, 32);
