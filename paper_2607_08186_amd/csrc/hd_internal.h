@@ -63,11 +63,11 @@ hipError_t launch_bwd_preprocess(const void *o, const void *dO, const float *lse
 
 // Backward workspace, each part 256-byte aligned:
 //   delta = rowsum(dO * O) and lse2 = lse * log2(e): fp32 [B][Hq][N];
-//   bf16 path only: transposed copies of q, dO (per query problem) and k (per key/value
-//   problem), each [problem][D][len_pad] with len_pad = len rounded up to 64 and the
-//   positions inside every 16-group in swap23 order (zeros past len).
+//   bf16 path only: a transposed copy of k per key/value problem, [problem][D][len_pad]
+//   with len_pad = len rounded up to 64 and the positions inside every 16-group in
+//   swap23 order (zeros past len).
 struct BwdWorkspace {
-    size_t delta, lse2, qt, dot, kt, total;
+    size_t delta, lse2, kt, total;
     int len_pad;
 };
 
@@ -80,16 +80,10 @@ inline BwdWorkspace bwd_workspace(const SfaGeom &g, int esize)
     w.len_pad = (g.len + 63) / 64 * 64;
     w.delta = 0;
     w.lse2 = align256(rows * 4);
-    w.qt = w.lse2 + align256(rows * 4);
-    w.total = w.qt;
-    w.dot = w.kt = w.qt;
-    if (esize == 2) {
-        const size_t qt_bytes = (size_t)g.B * g.Hq * g.streams * g.D * w.len_pad * 2;
-        const size_t kt_bytes = (size_t)g.B * g.Hkv * g.streams * g.D * w.len_pad * 2;
-        w.dot = w.qt + align256(qt_bytes);
-        w.kt = w.dot + align256(qt_bytes);
-        w.total = w.kt + align256(kt_bytes);
-    }
+    w.kt = w.lse2 + align256(rows * 4);
+    w.total = w.kt;
+    if (esize == 2)
+        w.total += align256((size_t)g.B * g.Hkv * g.streams * g.D * w.len_pad * 2);
     return w;
 }
 

@@ -31,31 +31,24 @@ constexpr int kDkdvWaves = 8;
 constexpr int kDqWaves = 8;
 constexpr int kRowsPerWg = kDqWaves * 32;  // dQ: 8 waves (two per SIMD) x 32 rows
 
-// Transposed copies for the backward: for each problem (b, h, s) and each 64-row tile,
-// rows i of x (expanded position i*rowmul + s, head h) become columns of
-// xt[prob][d][len_pad], position i stored at column swap23(i) of its 16-group; columns
-// past len are zero.  blockIdx.y picks the tensor: 0 = q, 1 = dO (H = Hq), 2 = k (Hkv).
+// Transposed copy of k for the dQ pass: for each key/value problem (b, hk, s) and each
+// 64-row tile, rows i of k (expanded position i*rowmul + s) become columns of
+// kt[prob][d][len_pad], position i stored at column swap23(i) of its 16-group; columns
+// past len are zero.
 template <int D>
-__global__ __launch_bounds__(256) void transpose_kernel(const bf16 *__restrict__ q,
-                                                        const bf16 *__restrict__ dO,
-                                                        const bf16 *__restrict__ k,
-                                                        bf16 *__restrict__ qt, bf16 *__restrict__ dot,
-                                                        bf16 *__restrict__ kt, SfaGeom g, int len_pad)
+__global__ __launch_bounds__(256) void transpose_k_kernel(const bf16 *__restrict__ k,
+                                                          bf16 *__restrict__ kt, SfaGeom g,
+                                                          int len_pad)
 {
     constexpr int CH = D / 8;
     constexpr int STR = D + 2;  // padded LDS row (elements)
     __shared__ uint16_t sm[kRows * STR];
-    const int which = blockIdx.y;
-    const int H = which == 2 ? g.Hkv : g.Hq;
-    const bf16 *x = which == 0 ? q : which == 1 ? dO : k;
-    bf16 *xt = which == 0 ? qt : which == 1 ? dot : kt;
+    const int H = g.Hkv;
     const int ntiles = len_pad / kRows;
-    const int nprob = g.B * H * g.streams;
-    if ((int)blockIdx.x >= nprob * ntiles) return;  // uniform: fewer key/value problems
     const int tile = blockIdx.x % ntiles, prob = blockIdx.x / ntiles;
     const int s = prob % g.streams, h = (prob / g.streams) % H, b = prob / (g.streams * H);
     const size_t slice = (size_t)g.N * H * D;
-    const rsrc_t rx = make_rsrc(x + b * slice, (uint32_t)(slice * 2));
+    const rsrc_t rx = make_rsrc(k + b * slice, (uint32_t)(slice * 2));
     const uint32_t stride = (uint32_t)g.rowmul * H * D * 2;
     const uint32_t base = (uint32_t)(s * H + h) * D * 2;
     const int tid = threadIdx.x;
@@ -69,7 +62,7 @@ __global__ __launch_bounds__(256) void transpose_kernel(const bf16 *__restrict__
         }
     }
     __syncthreads();
-    bf16 *out = xt + ((size_t)prob * D) * len_pad + (size_t)tile * kRows;
+    bf16 *out = kt + ((size_t)prob * D) * len_pad + (size_t)tile * kRows;
     for (int idx = tid; idx < D * (kRows / 8); idx += 256) {
         const int d = idx / (kRows / 8), c = idx % (kRows / 8);
         uint32_t w[4];
@@ -433,13 +426,13 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
 
 template <int D>
 hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *dO,
-                      const float *delta, const float *lse2, bf16 *qt, bf16 *dot, bf16 *kt,
-                      int len_pad, bf16 *dq, bf16 *dk, bf16 *dv, const SfaGeom &g, hipStream_t s,
-                      const char *tr_name, const char *dq_name, const char *dkdv_name)
+                      const float *delta, const float *lse2, bf16 *kt, int len_pad, bf16 *dq,
+                      bf16 *dk, bf16 *dv, const SfaGeom &g, hipStream_t s, const char *tr_name,
+                      const char *dq_name, const char *dkdv_name)
 {
     timing_before(tr_name, s);
-    transpose_kernel<D><<<dim3(g.B * g.Hq * g.streams * (len_pad / kRows), 3), 256, 0, s>>>(
-        q, dO, k, qt, dot, kt, g, len_pad);
+    transpose_k_kernel<D><<<g.B * g.Hkv * g.streams * (len_pad / kRows), 256, 0, s>>>(k, kt, g,
+                                                                                     len_pad);
     hipError_t e = hipGetLastError();
     timing_after(s);
     if (e != hipSuccess) return e;
@@ -469,20 +462,19 @@ hipError_t launch_bwd_bf16(const void *q, const void *k, const void *v, const vo
     char *wsb = static_cast<char *>(ws);
     float *delta = reinterpret_cast<float *>(wsb + w.delta);
     float *lse2 = reinterpret_cast<float *>(wsb + w.lse2);
-    bf16 *qt = reinterpret_cast<bf16 *>(wsb + w.qt), *dot = reinterpret_cast<bf16 *>(wsb + w.dot),
-         *kt = reinterpret_cast<bf16 *>(wsb + w.kt);
+    bf16 *kt = reinterpret_cast<bf16 *>(wsb + w.kt);
     hipError_t e = launch_bwd_preprocess(o, dO, lse, delta, lse2, g, 2, s);
     if (e != hipSuccess) return e;
     const bf16 *qq = static_cast<const bf16 *>(q), *kk = static_cast<const bf16 *>(k),
                *vv = static_cast<const bf16 *>(v), *dd = static_cast<const bf16 *>(dO);
     bf16 *gq = static_cast<bf16 *>(dq), *gk = static_cast<bf16 *>(dk), *gv = static_cast<bf16 *>(dv);
     if (g.D == 32)
-        return bwd_bf16_d<32>(qq, kk, vv, dd, delta, lse2, qt, dot, kt, w.len_pad, gq, gk, gv, g, s,
+        return bwd_bf16_d<32>(qq, kk, vv, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
                               "sfa_bwd_transpose_d32", "sfa_dq_bf16_d32", "sfa_dkdv_bf16_d32");
     if (g.D == 64)
-        return bwd_bf16_d<64>(qq, kk, vv, dd, delta, lse2, qt, dot, kt, w.len_pad, gq, gk, gv, g, s,
+        return bwd_bf16_d<64>(qq, kk, vv, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
                               "sfa_bwd_transpose_d64", "sfa_dq_bf16_d64", "sfa_dkdv_bf16_d64");
-    return bwd_bf16_d<128>(qq, kk, vv, dd, delta, lse2, qt, dot, kt, w.len_pad, gq, gk, gv, g, s,
+    return bwd_bf16_d<128>(qq, kk, vv, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
                            "sfa_bwd_transpose_d128", "sfa_dq_bf16_d128", "sfa_dkdv_bf16_d128");
 }
 

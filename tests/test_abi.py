@@ -83,13 +83,11 @@ def test_workspace_size_formula(lib):
     stats = 2 * a256(rows * 4)  # delta and lse2, fp32 per query row
     # fp32: statistics only
     assert lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, 0, 1) == stats
-    # bf16 adds transposed q, dO (per query problem) and k (per key/value problem),
-    # each [D][len rounded up to 64] bf16
+    # bf16 adds a transposed k per key/value problem, [D][len rounded up to 64] bf16
     for mode, len_, streams in ((0, L, n), (1, n * L, 1)):
         lp = math.ceil(len_ / 64) * 64
-        qt = a256(B * Hq * streams * D * lp * 2)
         kt = a256(B * Hkv * streams * D * lp * 2)
-        assert lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 0) == stats + 2 * qt + kt
+        assert lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 0) == stats + kt
     assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 3, 64, 0, 0) == 0  # Hq % Hkv
     assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 2, 48, 0, 0) == 0  # D
 
