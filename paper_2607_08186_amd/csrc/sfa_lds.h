@@ -4,14 +4,16 @@
 // Tile layout: 64 rows (consecutive rows of one causal problem; the row stride in HBM
 // is free, so intra-stream rows at stride n are gathered directly) x D bf16, row-major,
 // D*2 bytes per row with no padding.  Inside a row the 16-byte chunks are permuted:
-// logical chunk c of row r sits at physical chunk c ^ swz(r), with
-//   swz(r) = ((r & 7) << 1) | ((r >> 3) & 1)   (mod chunks per row).
-// This keeps both read patterns bank-conflict free on 64 x 4-byte banks:
-//   * row reads (16 lanes = 16 consecutive rows, same logical chunk, 16 bytes each):
-//     swz is a bijection on r & 15, so the 16 physical chunks are distinct;
-//   * transposed reads (ds_read_b64_tr_b16: 16 lanes cover 4 consecutive rows x 2
-//     adjacent chunks, 8 bytes each): swz(r) >> 1 differs across any 4 aligned rows, so
-//     the 8 (row, chunk) pieces land on distinct chunks.
+// logical chunk c of row r sits at physical chunk c ^ swz(r).  LDS has 64 banks of 4
+// bytes; a 16-byte read serves 16 lanes per cycle, an 8-byte read 32 lanes.  swz is
+// chosen per head dim so that both read patterns are bank-conflict free:
+//   * row reads (16 lanes = 16 consecutive rows, same logical chunk, 16 bytes each);
+//   * transposed reads (ds_read_b64_tr_b16: 32 lanes cover 4 aligned rows x 4 aligned
+//     logical chunks, 8 bytes each), which need the 4 rows to select 4 different
+//     groups of 4 physical chunks.
+//   D = 128 (16 chunks, one row spans all banks): swz(r) = (r & 3) << 2 | (r >> 2) & 3
+//   D = 64  (8 chunks, rows alternate bank halves): swz(r) = (r >> 1 & 1) << 2 | (r >> 2) & 3
+//   D = 32  (4 chunks, 4 rows per bank line):      swz(r) = (r >> 2) & 3
 // A direct-to-LDS load writes 64 lanes x 16 bytes to consecutive LDS slots; each lane
 // picks the HBM chunk that belongs in its slot, which realises the permutation.
 #pragma once
@@ -26,18 +28,24 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
-__device__ inline int chunk_swz(int r) { return ((r & 7) << 1) | ((r >> 3) & 1); }
-
 template <int D>
 struct Tile {
     static constexpr int CH = D / 8;              // 16-byte chunks per row
     static constexpr int BYTES = kRows * D * 2;   // one tile
     static constexpr int INSTR = kRows * CH / 64; // direct-to-LDS instructions per tile
 
+    // physical chunk = logical chunk ^ swz(row)
+    __device__ static inline int swz(int r)
+    {
+        if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+        else if constexpr (D == 64) return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
+        else return (r >> 2) & 3;
+    }
+
     // byte offset of element (row, col) inside the tile
     __device__ static inline int offset(int row, int col)
     {
-        const int c = (col >> 3) ^ (chunk_swz(row) & (CH - 1));
+        const int c = (col >> 3) ^ swz(row);
         return row * (D * 2) + c * 16 + (col & 7) * 2;
     }
 
@@ -52,7 +60,7 @@ struct Tile {
         for (int t = wave; t < INSTR; t += nwaves) {
             const int slot = t * 64 + lane;
             const int row = slot / CH;
-            const int c = (slot % CH) ^ (chunk_swz(row) & (CH - 1));
+            const int c = (slot % CH) ^ swz(row);
             const int grow = row0 + row;
             const uint32_t off = grow < len ? base + (uint32_t)grow * stride + c * 16 : kOob;
             __builtin_amdgcn_raw_ptr_buffer_load_lds(
@@ -63,7 +71,7 @@ struct Tile {
     // MFMA operand whose k-slots run along D: row `row`, dims kk*16 + half*8 .. +7
     __device__ static inline bf16x8 row_operand(const char *lds_tile, int row, int kk, int half)
     {
-        const int c = (kk * 2 + half) ^ (chunk_swz(row) & (CH - 1));
+        const int c = (kk * 2 + half) ^ swz(row);
         return *reinterpret_cast<const bf16x8 *>(lds_tile + row * (D * 2) + c * 16);
     }
 
