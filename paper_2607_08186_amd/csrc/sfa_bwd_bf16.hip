@@ -151,9 +151,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
             const int row = row0 + lane;
             const uint32_t off =
                 row < g.len ? (uint32_t)(((size_t)hq * g.N + (size_t)row * g.rowmul + s) * 4) : kOob;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                wave == 0 ? rl2 : rdl, (lds_void *)(base + 2 * T::BYTES + wave * kRows * 4), 4,
-                off, 0, 0, 0);
+            dma_lds4(wave == 0 ? rl2 : rdl, base + 2 * T::BYTES + wave * kRows * 4, off);
         }
     };
     if (iters > 0) issue(0, 0);
@@ -164,7 +162,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
 
     const float c2 = g.scale_log2;
     wait_lds_loads();
-    __syncthreads();
+    lds_barrier();
 
     // P and dS of my 32 keys x 32 queries, packed as bf16 B operands (two 16-query groups)
     auto softmax = [&](const f32x16 &sacc, const f32x16 &pacc, const float *sl, const float *sdl,
@@ -228,7 +226,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
             }
         }
         wait_lds_loads();
-        __syncthreads();
+        lds_barrier();
     };
     for (int it = 0; it < iters; it += 2) {
         step(it, std::integral_constant<int, 0>{});
@@ -344,7 +342,7 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const float c2 = g.scale_log2;
     const int wrow_min = q0 + wave * 32, wrow_max = wrow_min + 31;
     wait_lds_loads();
-    __syncthreads();
+    lds_barrier();
 
     // dS^T of one 32-key half as two B operands; MASK selects the diagonal variant
     auto softmax = [&](const f32x16 &sacc, const f32x16 &pacc, int k0, bf16x8 (&dsb)[2], auto mask) {
@@ -403,7 +401,7 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
             tile_body(ktl, vt, ktt, kb0, kb0 + kRows - 1 > wrow_min);  // diagonal: mask
         }
         wait_lds_loads();
-        __syncthreads();
+        lds_barrier();
     };
     for (int j = 0; j < nkt; j += 2) {
         step(j, std::integral_constant<int, 0>{});

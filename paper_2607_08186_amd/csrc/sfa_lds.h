@@ -28,6 +28,35 @@ typedef short v4i16 __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
 
+// Direct-to-LDS buffer loads (lane l writes LDS bytes lds + 16 l, resp. 4 l).  They are
+// issued from inline assembly on purpose: the compiler tracks the builtin form as a
+// pending LDS write and then waits for every such load before any LDS read, which
+// would expose the full HBM latency of the prefetch in every tile step.  Completion
+// is instead awaited explicitly (wait_vmcnt_le) before the barrier that publishes a
+// tile.  M0 carries the LDS base; no compiler-generated code in these kernels keeps a
+// value in M0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ inline void dma_lds16(rsrc_t rs, const char *lds, uint32_t voff)
+{
+    const uint32_t m0 = (uint32_t)(uintptr_t)(lds_void *)lds;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+                 :: "s"(m0), "v"(voff), "s"(rs) : "memory", "m0");
+}
+__device__ inline void dma_lds4(rsrc_t rs, const char *lds, uint32_t voff)
+{
+    const uint32_t m0 = (uint32_t)(uintptr_t)(lds_void *)lds;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dword %1, %2, 0 offen lds"
+                 :: "s"(m0), "v"(voff), "s"(rs) : "memory", "m0");
+}
+#pragma clang diagnostic pop
+
+// Workgroup barrier for LDS tiles: this wave's LDS reads have completed
+// (lgkmcnt 0), without __syncthreads' wait for every outstanding global load, so
+// prefetches stay in flight across it.  Tile data written by direct-to-LDS loads
+// must have been waited for (wait_vmcnt_le) by every issuing wave beforehand.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 template <int D>
 struct Tile {
     static constexpr int CH = D / 8;              // 16-byte chunks per row
@@ -63,9 +92,80 @@ struct Tile {
             const int c = (slot % CH) ^ swz(row);
             const int grow = row0 + row;
             const uint32_t off = grow < len ? base + (uint32_t)grow * stride + c * 16 : kOob;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rs, (lds_void *)(lds_tile + t * 1024), 16, off, 0, 0, 0);
+            dma_lds16(rs, lds_tile + t * 1024, off);
         }
+    }
+
+    // Per-lane parts of the addresses, computed once per kernel so that the tile base,
+    // whole 16-row groups and the row-within-tile offsets below are immediates.
+    //
+    // DMA: this wave's share of a tile is slots t*64 + lane for t = wave, wave+nwaves,
+    // ...; slot -> (row, logical chunk).  voff[i] is the HBM byte offset of that chunk
+    // relative to the tile's first row (row stride `stride`).
+    static constexpr int MAXL = (INSTR + 3) / 4;  // loads per wave when >= 4 waves share
+    struct Dma {
+        uint32_t voff[MAXL];
+        int n;  // loads this wave issues per tile
+    };
+    __device__ static inline Dma dma_plan(uint32_t base, uint32_t stride, int wave, int nwaves, int lane)
+    {
+        Dma p;
+        p.n = 0;
+#pragma unroll
+        for (int i = 0; i < MAXL; ++i) {
+            const int t = wave + i * nwaves;
+            const int slot = t * 64 + lane;
+            const int row = slot / CH;
+            const int c = (slot % CH) ^ swz(row);
+            p.voff[i] = base + (uint32_t)row * stride + c * 16;
+            if (t < INSTR) p.n = i + 1;
+        }
+        return p;
+    }
+    // Load rows row0 .. row0+63 (row0 * stride + p.voff < 2^31).  Rows past the end of
+    // the problem must lie past the end of the buffer range, which returns zeros.
+    __device__ static inline void load(char *lds_tile, rsrc_t rs, const Dma &p, uint32_t row0_off,
+                                       int wave, int nwaves)
+    {
+#pragma unroll
+        for (int i = 0; i < MAXL; ++i) {
+            const int t = wave + i * nwaves;
+            if (t < INSTR) dma_lds16(rs, lds_tile + t * 1024, p.voff[i] + row0_off);
+        }
+    }
+
+    // Row reads: byte offsets of row (lane % 32) at k-step kk, lane half `half`; rows
+    // r + 16 m add 16 m rows (swz depends on r % 16 only).
+    __device__ static inline void row_offsets(int l32, int half, uint32_t (&off)[D / 16])
+    {
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk)
+            off[kk] = l32 * (D * 2) + (((kk * 2 + half) ^ swz(l32 & 15)) * 16);
+    }
+    __device__ static inline bf16x8 row_at(const char *lds_tile, uint32_t off, int row_group16)
+    {
+        return *reinterpret_cast<const bf16x8 *>(lds_tile + off + row_group16 * 16 * (D * 2));
+    }
+
+    // Transposed reads (see tr_operand): offsets for 32-dim block db and the two
+    // 8-row halves of a 16-row group; 16-row group kk adds kk*16 rows.
+    __device__ static inline void tr_offsets(int lane, uint32_t (&off)[D / 32][2])
+    {
+        const int s = lane & 15, g = lane >> 4, half = g >> 1;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+            for (int p = 0; p < 2; ++p)
+                off[db][p] = offset(4 * half + (s >> 2) + 8 * p, db * 32 + 16 * (g & 1) + 4 * (s & 3));
+    }
+    __device__ static inline bf16x8 tr_at(const char *lds_tile, const uint32_t (&off)[2], int kk)
+    {
+        const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_v4i16 *)(lds_tile + off[0] + kk * 16 * (D * 2)));
+        const v4i16 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+            (lds_v4i16 *)(lds_tile + off[1] + kk * 16 * (D * 2)));
+        const u32x2 a = __builtin_bit_cast(u32x2, lo), b = __builtin_bit_cast(u32x2, hi);
+        return __builtin_bit_cast(bf16x8, u32x4{a[0], a[1], b[0], b[1]});
     }
 
     // MFMA operand whose k-slots run along D: row `row`, dims kk*16 + half*8 .. +7
@@ -117,8 +217,7 @@ struct TileT {
             const int d = slot >> 3;
             const int c = (slot & 7) ^ swz(d);
             const uint32_t off = base + (uint32_t)d * stride + (uint32_t)row0 * 2 + c * 16;
-            __builtin_amdgcn_raw_ptr_buffer_load_lds(
-                rs, (lds_void *)(lds_tile + t * 1024), 16, off, 0, 0, 0);
+            dma_lds16(rs, lds_tile + t * 1024, off);
         }
     }
 
@@ -130,6 +229,21 @@ struct TileT {
         return *reinterpret_cast<const bf16x8 *>(lds_tile + d * (kRows * 2) + c * 16);
     }
 };
+
+// Scheduling hint for the basic block it ends: P LDS reads up front, then N
+// repetitions of (M MFMAs, R LDS reads, V other vector ALU instructions), so that each
+// MFMA's operands were requested about P reads earlier.
+template <int P, int N, int M, int R, int V>
+__device__ inline void sched_pattern()
+{
+    __builtin_amdgcn_sched_group_barrier(0x100, P, 0);  // LDS read
+#pragma unroll
+    for (int i = 0; i < N; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, M, 0);  // MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, R, 0);  // LDS read
+        __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // VALU
+    }
+}
 
 // Wait until every direct-to-LDS load this wave issued has landed.
 __device__ inline void wait_lds_loads() { __builtin_amdgcn_s_waitcnt(0); }
