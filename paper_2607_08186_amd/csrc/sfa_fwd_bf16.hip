@@ -27,7 +27,7 @@ namespace {
 
 constexpr int kWaves = 8;
 constexpr int kBM = kWaves * 32;           // query rows per workgroup
-constexpr int kSlots = 4;                  // K and V ring slots (64-key tiles)
+constexpr int kLoaders = 2;                // waves 6 and 7 issue the tile loads
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -40,10 +40,10 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     constexpr int KS = D / 16;  // MFMA k-steps over the head dim
     constexpr int DB = D / 32;  // 32-wide head-dim blocks of O
     using T = Tile<D>;
-    // separate K and V rings: every slot is an immediate offset (< 64 KB) from one
-    // per-lane address
-    __shared__ __attribute__((aligned(1024))) char ks[kSlots][T::BYTES];
-    __shared__ __attribute__((aligned(1024))) char vs[kSlots][T::BYTES];
+    // two-slot K and V rings (tile t in slot t % 2); every slot is an immediate offset
+    // from one per-lane address
+    __shared__ __attribute__((aligned(1024))) char ks[2][T::BYTES];
+    __shared__ __attribute__((aligned(1024))) char vs[2][T::BYTES];
 
     const int ntiles = (g.len + kBM - 1) / kBM;
     const int nprob = g.B * g.Hq * g.streams;
@@ -67,6 +67,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
 
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
+    const int group = wave >> 2;  // 0: A, 1: B (one wave of each per SIMD)
     const int l32 = lane & 31, hi = lane >> 5;
     const int q0 = tile * kBM;
     const int row = q0 + wave * 32 + l32;
@@ -86,85 +87,89 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     }
 
     // per-lane address parts (K and V share the row layout)
-    const typename T::Dma dma = T::dma_plan(kbase0, kstride, wave, kWaves, lane);
+    const bool loader = wave >= kWaves - kLoaders;  // waves that see every tile
+    const int lw = loader ? wave - (kWaves - kLoaders) : 0;
+    const auto dma = T::template dma_plan<kLoaders>(kbase0, kstride, lw, lane);
     uint32_t kro[KS], vto[DB][2];
     T::row_offsets(l32, hi, kro);
     T::tr_offsets(lane, vto);
-    auto issue_k = [&](int j) __attribute__((always_inline)) {
-        if (j < nkt) T::load(ks[j % kSlots], rk, dma, (uint32_t)(j * kRows) * kstride, wave, kWaves);
-    };
-    auto issue_v = [&](int j) __attribute__((always_inline)) {
-        if (j < nkt) T::load(vs[j % kSlots], rv, dma, (uint32_t)(j * kRows) * kstride, wave, kWaves);
+    // loader waves queue K of tile t+2 and V of tile t+1 in their vector phase of tile
+    // t and wait for them at the end of their next phase
+    auto issue = [&](int t) __attribute__((always_inline)) {
+        if (loader) {
+            if (t + 2 < nkt)
+                T::load(ks[t & 1], rk, dma, (uint32_t)((t + 2) * kRows) * kstride, lw);
+            if (t + 1 < nkt)
+                T::load(vs[(t + 1) & 1], rv, dma, (uint32_t)((t + 1) * kRows) * kstride, lw);
+        }
     };
 
     f32x16 oacc[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) oacc[db] = f32x16{};
-    float m2 = -INFINITY;         // reference max in log2 units
+    f32x16 sc[2];               // scores of the tile whose softmax comes next
+    bf16x8 pb[4];               // bf16 weights of the tile whose P V product comes next
+    float m2 = -INFINITY;       // reference max in log2 units
     float lsum0 = 0.f, lsum1 = 0.f;  // this lane half's share of the row sum (two chains)
     const float c2 = g.scale_log2;
     const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3f803f80u);
 
-    auto is_diag = [&](int j) __attribute__((always_inline)) { return j * kRows + kRows - 1 > wrow_min; };
-    // S^T of one 64-key tile (two 32-key blocks).  On the tile that holds this wave's
-    // diagonal the accumulators start at -inf for keys past the lane's row, so masked
-    // scores come out as -inf (exp2 -> 0) and nothing downstream needs a mask; other
-    // tiles start from the MFMA's literal zero.
-    auto scores = [&](f32x16 (&sc)[2], const char *kt, int j) __attribute__((always_inline)) {
-        const bf16x8 a0 = T::row_at(kt, kro[0], 0), a1 = T::row_at(kt, kro[0], 2);
-        if (is_diag(j)) {
-            // key = j*64 + mb*32 + 8*(r/4) + 4*hi + r%4, compared against a per-lane
-            // limit so the per-element constants stay immediates
-            const int lim = row - 4 * hi - j * kRows;
-            f32x16 bias[2];
+    auto is_diag = [&](int t) __attribute__((always_inline)) { return t * kRows + kRows - 1 > wrow_min; };
+
+    // Matrix phase of tile t: the scores of tile t+1 (DO_S) and O^T += V^T P^T of
+    // tile t (DO_PV).  On the tile that holds this wave's diagonal the score
+    // accumulators start at -inf for keys past the lane's row, so masked scores come
+    // out as -inf (exp2 -> 0) and the softmax needs no mask; other tiles start from the
+    // MFMA's literal zero.  KSL/VSL: ring slots of K of tile t+1 and V of tile t.
+    auto mfma_phase = [&](int t, auto do_s_, auto do_pv_, auto ksl, auto vsl) __attribute__((always_inline)) {
+        constexpr bool DO_S = decltype(do_s_)::value, DO_PV = decltype(do_pv_)::value;
+        const char *kt = ks[decltype(ksl)::value];
+        const char *vt = vs[decltype(vsl)::value];
+        if constexpr (DO_S) {
+            const bf16x8 a0 = T::row_at(kt, kro[0], 0), a1 = T::row_at(kt, kro[0], 2);
+            if (is_diag(t + 1)) {
+                // key = (t+1)*64 + mb*32 + 8*(r/4) + 4*hi + r%4, compared against a
+                // per-lane limit so the per-element constants stay immediates
+                const int lim = row - 4 * hi - (t + 1) * kRows;
+                f32x16 bias[2];
 #pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
+                for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                for (int r = 0; r < 16; ++r)
-                    bias[mb][r] = mb * 32 + 8 * (r >> 2) + (r & 3) > lim ? -INFINITY : 0.f;
-            sc[0] = mfma32(a0, qr[0], bias[0]);
-            sc[1] = mfma32(a1, qr[0], bias[1]);
-        } else {
-            sc[0] = mfma32(a0, qr[0], f32x16{});
-            sc[1] = mfma32(a1, qr[0], f32x16{});
+                    for (int r = 0; r < 16; ++r)
+                        bias[mb][r] = mb * 32 + 8 * (r >> 2) + (r & 3) > lim ? -INFINITY : 0.f;
+                sc[0] = mfma32(a0, qr[0], bias[0]);
+                sc[1] = mfma32(a1, qr[0], bias[1]);
+            } else {
+                sc[0] = mfma32(a0, qr[0], f32x16{});
+                sc[1] = mfma32(a1, qr[0], f32x16{});
+            }
         }
+        // the S and P V chains interleaved
+        constexpr int NS = DO_S ? 2 * KS - 2 : 0, NP = DO_PV ? 4 * DB : 0;
 #pragma unroll
-        for (int kk = 1; kk < KS; ++kk)
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb)
-                sc[mb] = mfma32(T::row_at(kt, kro[kk], mb * 2), qr[kk], sc[mb]);
+        for (int i = 0; i < (NS > NP ? NS : NP); ++i) {
+            if (i < NP) {
+                const int db = i / 4, kk = i % 4;
+                oacc[db] = mfma32(T::tr_at(vt, vto[db], kk), pb[kk], oacc[db]);
+            }
+            if (i < NS) {
+                const int kk2 = 1 + i / 2, mb = i % 2;
+                sc[mb] = mfma32(T::row_at(kt, kro[kk2], mb * 2), qr[kk2], sc[mb]);
+            }
+        }
+        // operand reads about six ahead of their MFMAs
+        sched_pattern<6, NS + NP, 1, 2, 0>();
+        if constexpr (DO_S) pin(sc[0], sc[1]);
     };
-    auto rowmax = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
+    // Vector phase of tile t: row max, rare rescale, P = exp2(S c2 - m2) as bf16 and
+    // the row sum of those bf16 weights.
+    auto vector_phase = [&]() __attribute__((always_inline)) {
         float mx = -INFINITY;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[mb][r]);
-        return fmaxf(mx, __shfl_xor(mx, 32));
-    };
-
-    // K of tiles 0..2 and V of tiles 0..1 resident before the loop (and the query row)
-    issue_k(0);
-    issue_k(1);
-    issue_v(0);
-    issue_v(1);
-    issue_k(2);
-    wait_vmcnt_le(0);
-    lds_barrier();
-
-    f32x16 sa[2], sb[2];
-    scores(sa, ks[0], 0);
-    float mx = rowmax(sa);
-    lds_barrier();  // every wave is done with K of tile 0 before its slot is refilled
-
-    // One tile j (ring slot kSl): the softmax of tile j runs on the vector unit while
-    // the scores of tile j+1 run on the matrix unit, then O^T += V^T P^T with the row
-    // max of tile j+1 in between.  Scores of a tile past this wave's diagonal (or past
-    // the last tile) are computed from whatever the ring slot holds and discarded.
-    auto tile_step = [&](int j, auto slot, f32x16 (&sc)[2], f32x16 (&sn)[2]) __attribute__((always_inline)) {
-        constexpr int kSl = decltype(slot)::value;
-        constexpr int kNx = (kSl + 1) % kSlots;
-        if (j > jlast) return;  // wave-uniform
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
         const float mcand = fmaxf(m2, mx * c2);
         if (__any(mcand > m2 + kRescaleThreshold)) {
             const float alpha = mcand == -INFINITY ? 1.f : fast_exp2(m2 - mcand);
@@ -174,8 +179,6 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
 #pragma unroll
             for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
         }
-        scores(sn, ks[kNx], j + 1);
-        bf16x8 pb[4];
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -194,38 +197,72 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
                 }
                 pb[mb * 2 + h] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
             }
-        // K reads three MFMAs ahead, a slice of the softmax after each MFMA
-        sched_pattern<3, 2 * KS - 2, 1, 1, 6>();
-        asm volatile("; P V" ::: "memory");
-        const char *vt = vs[kSl];
-#pragma unroll
-        for (int db = 0; db < DB; ++db)
-#pragma unroll
-            for (int kk = 0; kk < 4; ++kk)
-                oacc[db] = mfma32(T::tr_at(vt, vto[db], kk), pb[kk], oacc[db]);
-        mx = rowmax(sn);
-        // transposed V reads three MFMAs ahead, the row max in between
-        sched_pattern<6, 4 * DB, 1, 2, 3>();
+        pin(pb[0], pb[1], pb[2], pb[3]);
     };
-    // Two tiles per barrier.  At entry K of tiles j+1, j+2 and V of tiles j, j+1 are
-    // resident; K of j+3, j+4 and V of j+2, j+3 go to the slots freed by the previous
-    // pair and must have landed at the closing barrier.
-    auto pair_step = [&](int j, auto slot) __attribute__((always_inline)) {
-        constexpr int kSl = decltype(slot)::value;
-        issue_k(j + 3);
-        issue_k(j + 4);
-        issue_v(j + 2);
-        issue_v(j + 3);
-        tile_step(j, std::integral_constant<int, kSl>{}, sa, sb);
-        tile_step(j + 1, std::integral_constant<int, kSl + 1>{}, sb, sa);
-        wait_vmcnt_le(0);
-        lds_barrier();
-    };
-    static_assert(kSlots == 4, "the loop below cycles through four ring slots");
-    for (int j = 0; j < nkt; j += 4) {
-        pair_step(j, std::integral_constant<int, 0>{});
-        if (j + 2 < nkt) pair_step(j + 2, std::integral_constant<int, 2>{});
+
+    // Prologue: K of tiles 0, 1 and V of tile 0 resident (and the query row).
+    if (loader) {
+        T::load(ks[0], rk, dma, 0, lw);
+        if (nkt > 1) T::load(ks[1], rk, dma, (uint32_t)kRows * kstride, lw);
+        T::load(vs[0], rv, dma, 0, lw);
     }
+    wait_vmcnt_le(0);
+    lds_barrier();
+
+    // Ping-pong.  Each wave runs: matrix phase of tile -1 (scores of tile 0), then for
+    // t = 0 .. jlast the vector phase of tile t and the matrix phase of tile t, one
+    // phase per workgroup barrier.  Group B starts one phase after group A, so on every
+    // SIMD one wave feeds the matrix unit while the other uses the vector unit.  Waves
+    // that finish early pass the remaining barriers idle; every wave passes
+    // 2*nkt + 2 of them.  Loads (loader waves, group B, whose jlast is nkt-1): K of
+    // t+2 goes to the slot of K of t, V of t+1 to the slot of V of t-1, both last read
+    // in the matrix phases of tile t-1 (phases 2t, 2t+1); they are queued in phase
+    // 2t+2 and published by the barrier of phase 2t+3, before group A's matrix phase
+    // of tile t+1 (phase 2t+4).
+    using F = std::false_type;
+    using Tr = std::true_type;
+    using Z = std::integral_constant<int, 0>;
+    using O = std::integral_constant<int, 1>;
+    int nb = 0;  // barriers passed
+    auto bar = [&]() __attribute__((always_inline)) { lds_barrier(); ++nb; };
+    if (group == 1) bar();
+    mfma_phase(-1, Tr{}, F{}, Z{}, Z{});
+    bar();
+    int t = 0;
+    for (; t + 1 < jlast; t += 2) {
+        vector_phase();
+        issue(t);
+        bar();
+        mfma_phase(t, Tr{}, Tr{}, O{}, Z{});
+        if (loader) wait_vmcnt_le(0);
+        bar();
+        vector_phase();
+        issue(t + 1);
+        bar();
+        mfma_phase(t + 1, Tr{}, Tr{}, Z{}, O{});
+        if (loader) wait_vmcnt_le(0);
+        bar();
+    }
+    if (t < jlast) {  // t even
+        vector_phase();
+        issue(t);
+        bar();
+        mfma_phase(t, Tr{}, Tr{}, O{}, Z{});
+        if (loader) wait_vmcnt_le(0);
+        bar();
+        ++t;
+    }
+    // t == jlast: last softmax and P V product
+    vector_phase();
+    issue(t);
+    bar();
+    if (t & 1)
+        mfma_phase(t, F{}, Tr{}, Z{}, O{});
+    else
+        mfma_phase(t, F{}, Tr{}, Z{}, Z{});
+    if (loader) wait_vmcnt_le(0);
+    bar();
+    while (nb < 2 * nkt + 2) bar();
 
     const float l = lsum0 + lsum1 + __shfl_xor(lsum0 + lsum1, 32);
     if (row < g.len) {

@@ -55,7 +55,27 @@ __device__ inline void dma_lds4(rsrc_t rs, const char *lds, uint32_t voff)
 // (lgkmcnt 0), without __syncthreads' wait for every outstanding global load, so
 // prefetches stay in flight across it.  Tile data written by direct-to-LDS loads
 // must have been waited for (wait_vmcnt_le) by every issuing wave beforehand.
-__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+// The scheduling barriers keep the compiler from moving any instruction across it.
+__device__ inline void lds_barrier()
+{
+    __builtin_amdgcn_sched_barrier(0);
+    asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    __builtin_amdgcn_sched_barrier(0);
+}
+
+// Force values to be computed at this point of the program (an empty asm that reads
+// them); used to keep work inside the phase it belongs to.
+template <typename T>
+__device__ inline void pin(const T &v)
+{
+    asm volatile("" ::"v"(v));
+}
+template <typename T, typename... Ts>
+__device__ inline void pin(const T &v, const Ts &...rest)
+{
+    pin(v);
+    pin(rest...);
+}
 
 template <int D>
 struct Tile {
@@ -99,21 +119,23 @@ struct Tile {
     // Per-lane parts of the addresses, computed once per kernel so that the tile base,
     // whole 16-row groups and the row-within-tile offsets below are immediates.
     //
-    // DMA: this wave's share of a tile is slots t*64 + lane for t = wave, wave+nwaves,
-    // ...; slot -> (row, logical chunk).  voff[i] is the HBM byte offset of that chunk
-    // relative to the tile's first row (row stride `stride`).
-    static constexpr int MAXL = (INSTR + 3) / 4;  // loads per wave when >= 4 waves share
+    // DMA: with NW waves loading, this wave's share of a tile is slots t*64 + lane for
+    // t = wave, wave+NW, ...; slot -> (row, logical chunk).  voff[i] is the HBM byte
+    // offset of that chunk relative to the tile's first row (row stride `stride`).
+    template <int NW>
     struct Dma {
+        static constexpr int MAXL = (INSTR + NW - 1) / NW;  // loads per wave, at most
         uint32_t voff[MAXL];
         int n;  // loads this wave issues per tile
     };
-    __device__ static inline Dma dma_plan(uint32_t base, uint32_t stride, int wave, int nwaves, int lane)
+    template <int NW>
+    __device__ static inline Dma<NW> dma_plan(uint32_t base, uint32_t stride, int wave, int lane)
     {
-        Dma p;
+        Dma<NW> p;
         p.n = 0;
 #pragma unroll
-        for (int i = 0; i < MAXL; ++i) {
-            const int t = wave + i * nwaves;
+        for (int i = 0; i < Dma<NW>::MAXL; ++i) {
+            const int t = wave + i * NW;
             const int slot = t * 64 + lane;
             const int row = slot / CH;
             const int c = (slot % CH) ^ swz(row);
@@ -124,12 +146,13 @@ struct Tile {
     }
     // Load rows row0 .. row0+63 (row0 * stride + p.voff < 2^31).  Rows past the end of
     // the problem must lie past the end of the buffer range, which returns zeros.
-    __device__ static inline void load(char *lds_tile, rsrc_t rs, const Dma &p, uint32_t row0_off,
-                                       int wave, int nwaves)
+    template <int NW>
+    __device__ static inline void load(char *lds_tile, rsrc_t rs, const Dma<NW> &p, uint32_t row0_off,
+                                       int wave)
     {
 #pragma unroll
-        for (int i = 0; i < MAXL; ++i) {
-            const int t = wave + i * nwaves;
+        for (int i = 0; i < Dma<NW>::MAXL; ++i) {
+            const int t = wave + i * NW;
             if (t < INSTR) dma_lds16(rs, lds_tile + t * 1024, p.voff[i] + row0_off);
         }
     }
@@ -241,7 +264,7 @@ __device__ inline void sched_pattern()
     for (int i = 0; i < N; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, M, 0);  // MFMA
         __builtin_amdgcn_sched_group_barrier(0x100, R, 0);  // LDS read
-        __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // VALU
+        if constexpr (V > 0) __builtin_amdgcn_sched_group_barrier(0x002, V, 0);  // VALU
     }
 }
 
