@@ -57,12 +57,13 @@ hipError_t launch_bwd_f32(const float *q, const float *k, const float *v, const 
                           const float *lse, const float *dO, float *dq, float *dk, float *dv,
                           const SfaGeom &g, void *ws, hipStream_t s);
 
-// delta = rowsum(dO * O) and lse2 = lse * log2(e), both fp32 [B][Hq][N]; esize = 2 or 4.
+// Per query row, fp32 [B][Hq][N]: esize 4 stores delta = rowsum(dO * O) and
+// lse2 = lse * log2(e); esize 2 (bf16 path) stores -delta and -lse / scale.
 hipError_t launch_bwd_preprocess(const void *o, const void *dO, const float *lse, float *delta,
                                  float *lse2, const SfaGeom &g, int esize, hipStream_t s);
 
 // Backward workspace, each part 256-byte aligned:
-//   delta = rowsum(dO * O) and lse2 = lse * log2(e): fp32 [B][Hq][N];
+//   the per-row statistics of launch_bwd_preprocess: fp32 [B][Hq][N];
 //   bf16 path only: a transposed copy of k per key/value problem, [problem][D][len_pad]
 //   with len_pad = len rounded up to 64 and the positions inside every 16-group in
 //   swap23 order (zeros past len).

@@ -1,8 +1,9 @@
 // sfa_bwd_bf16.hip -- Stream-Factorized Attention backward, bf16 in/out, fp32 math.
 //
 // Gradients of O = softmax(scale Q K^T + mask) V with the probabilities recomputed
-// from the forward's log-sum-exp (kept in log2 units in the workspace):
-//   P = exp2(scale*log2(e) q.k - lse2),  dP = dO V^T,  dS = P (dP - Delta),
+// from the forward's log-sum-exp; the workspace holds, per query row, -lse/scale and
+// -Delta:
+//   P = exp2(scale*log2(e) (q.k - lse/scale)),  dP = dO V^T,  dS = P (dP - Delta),
 //   dV = P^T dO,  dK = scale dS^T Q,  dQ = scale dS K,   Delta = rowsum(dO * O).
 // Two deterministic kernels (no atomics):
 //   dK/dV: a workgroup owns 128 keys of one (b, kv-head[, stream]) problem (K and V
@@ -164,24 +165,23 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     wait_lds_loads();
     lds_barrier();
 
-    // P and dS of my 32 keys x 32 queries, packed as bf16 B operands (two 16-query groups)
-    auto softmax = [&](const f32x16 &sacc, const f32x16 &pacc, const float *sl, const float *sdl,
-                       int qlo, uint32_t (&pw)[8], uint32_t (&dw)[8], auto mask)
-        __attribute__((always_inline)) {
+    // P = exp2(c2 (S - lse/scale)) and dS = P (dP - Delta) of my 32 keys x 32 queries,
+    // packed as bf16 B operands (two 16-query groups)
+    auto softmax = [&](const f32x16 &sacc, const f32x16 &pacc, int qlo, uint32_t (&pw)[8],
+                       uint32_t (&dw)[8], auto mask) __attribute__((always_inline)) {
         constexpr bool kMask = decltype(mask)::value;
 #pragma unroll
         for (int rq = 0; rq < 4; ++rq) {
-            const f32x4 l4 = *reinterpret_cast<const f32x4 *>(&sl[8 * rq + 4 * hi]);
-            const f32x4 d4 = *reinterpret_cast<const f32x4 *>(&sdl[8 * rq + 4 * hi]);
             float p[4], ds[4];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 const int r = rq * 4 + e;
-                p[e] = fast_exp2(__builtin_fmaf(sacc[r], c2, -l4[e]));
+                float x = sacc[r];
                 if constexpr (kMask) {
-                    if (qlo + 8 * rq + 4 * hi + e < key) p[e] = 0.f;
+                    if (qlo + 8 * rq + 4 * hi + e < key) x = -INFINITY;  // exp2 -> 0
                 }
-                ds[e] = p[e] * (pacc[r] - d4[e]);
+                p[e] = fast_exp2(x * c2);
+                ds[e] = p[e] * pacc[r];
             }
             pw[rq * 2] = pack_bf16(p[0], p[1]);
             pw[rq * 2 + 1] = pack_bf16(p[2], p[3]);
@@ -198,7 +198,19 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
             const char *dot = qt + T::BYTES;
             const float *sl = reinterpret_cast<const float *>(qt + 2 * T::BYTES) + qb * 32;
             const float *sdl = sl + kRows;
-            f32x16 sacc = f32x16{}, pacc = f32x16{};
+            // S and dP accumulators start at -lse/scale and -Delta of their query rows
+            // (register r of a lane: row 8*(r/4) + 4*hi + r%4 of my 32 queries)
+            f32x16 sacc, pacc;
+#pragma unroll
+            for (int rq = 0; rq < 4; ++rq) {
+                const f32x4 l4 = *reinterpret_cast<const f32x4 *>(&sl[8 * rq + 4 * hi]);
+                const f32x4 d4 = *reinterpret_cast<const f32x4 *>(&sdl[8 * rq + 4 * hi]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    sacc[4 * rq + e] = l4[e];
+                    pacc[4 * rq + e] = d4[e];
+                }
+            }
 #pragma unroll
             for (int kk = 0; kk < KS; ++kk) {
                 sacc = mfma32(T::row_operand(qt, qb * 32 + l32, kk, hi),
@@ -208,9 +220,9 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
             }
             uint32_t pw[8], dw[8];
             if (qlo < kw0 + 31)  // diagonal: causal mask
-                softmax(sacc, pacc, sl, sdl, qlo, pw, dw, std::true_type{});
+                softmax(sacc, pacc, qlo, pw, dw, std::true_type{});
             else
-                softmax(sacc, pacc, sl, sdl, qlo, pw, dw, std::false_type{});
+                softmax(sacc, pacc, qlo, pw, dw, std::false_type{});
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
                 const bf16x8 pb = __builtin_bit_cast(
@@ -328,10 +340,10 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
             qr[kk] = __builtin_bit_cast(bf16x8, ld16(rq, off + (kk * 16 + hi * 8) * 2));
             dor[kk] = __builtin_bit_cast(bf16x8, ld16(rdo, off + (kk * 16 + hi * 8) * 2));
         }
-        if (row < g.len) {
+        if (row < g.len) {  // -lse/scale and -Delta of this row
             const size_t li = ((size_t)b * g.Hq + hq) * g.N + (size_t)row * g.rowmul + s;
-            lrow = lse2[li];
-            drow = delta[li];
+            lrow = -lse2[li] * g.scale_log2;  // lse in log2 units
+            drow = -delta[li];
         }
     }
 

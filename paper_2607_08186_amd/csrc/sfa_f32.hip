@@ -82,9 +82,11 @@ __global__ __launch_bounds__(64) void sfa_fwd_f32_kernel(const float *__restrict
     }
 }
 
-// delta[b][hq][p] = sum_d dO * O, lse2[b][hq][p] = lse * log2(e).  One group of lanes
-// per (b, p, hq) row, 16 bytes per lane, reduced with xor shuffles.
-template <typename T, int D>
+// Per (b, hq, p) query row: delta = sum_d dO * O and lse2 = lse * log2(e); with NEG the
+// kernel stores -delta and -lse / scale instead (the starting values of the dP and S
+// accumulators of the bf16 backward).  One group of lanes per row, 16 bytes per lane,
+// reduced with xor shuffles.
+template <typename T, int D, bool NEG>
 __global__ __launch_bounds__(256) void bwd_preprocess_kernel(const T *__restrict__ o,
                                                              const T *__restrict__ dO,
                                                              const float *__restrict__ lse,
@@ -119,8 +121,13 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(const T *__restrict
         const size_t bp = r / g.Hq;  // b * N + p
         const size_t b = bp / g.N, p = bp % g.N;
         const size_t li = (b * g.Hq + hq) * g.N + p;
-        delta[li] = acc;
-        lse2[li] = lse[li] * kLog2e;
+        if constexpr (NEG) {
+            delta[li] = -acc;
+            lse2[li] = -lse[li] / g.scale;
+        } else {
+            delta[li] = acc;
+            lse2[li] = lse[li] * kLog2e;
+        }
     }
 }
 
@@ -306,18 +313,18 @@ hipError_t launch_bwd_preprocess(const void *o, const void *dO, const float *lse
     const int rpb = 256 / lpr;
     const dim3 grid((unsigned)((rows + rpb - 1) / rpb));
     timing_before(esize == 2 ? "sfa_bwd_preprocess_bf16" : "sfa_bwd_preprocess_f32", s);
-#define HD_PRE(T, DD)                                                                         \
-    bwd_preprocess_kernel<T, DD><<<grid, 256, 0, s>>>(static_cast<const T *>(o),              \
-                                                      static_cast<const T *>(dO), lse, delta, \
-                                                      lse2, g)
+#define HD_PRE(T, DD, NEG)                                                                         \
+    bwd_preprocess_kernel<T, DD, NEG><<<grid, 256, 0, s>>>(static_cast<const T *>(o),              \
+                                                           static_cast<const T *>(dO), lse, delta, \
+                                                           lse2, g)
     if (esize == 2) {
-        if (g.D == 32) HD_PRE(bf16, 32);
-        else if (g.D == 64) HD_PRE(bf16, 64);
-        else HD_PRE(bf16, 128);
+        if (g.D == 32) HD_PRE(bf16, 32, true);
+        else if (g.D == 64) HD_PRE(bf16, 64, true);
+        else HD_PRE(bf16, 128, true);
     } else {
-        if (g.D == 32) HD_PRE(float, 32);
-        else if (g.D == 64) HD_PRE(float, 64);
-        else HD_PRE(float, 128);
+        if (g.D == 32) HD_PRE(float, 32, false);
+        else if (g.D == 64) HD_PRE(float, 64, false);
+        else HD_PRE(float, 128, false);
     }
 #undef HD_PRE
     hipError_t e = hipGetLastError();

@@ -77,11 +77,12 @@ __device__ inline void pin(const T &v, const Ts &...rest)
     pin(rest...);
 }
 
-template <int D>
+template <int D, int R = kRows>
 struct Tile {
-    static constexpr int CH = D / 8;              // 16-byte chunks per row
-    static constexpr int BYTES = kRows * D * 2;   // one tile
-    static constexpr int INSTR = kRows * CH / 64; // direct-to-LDS instructions per tile
+    static_assert(R % 16 == 0, "the swizzle repeats every 16 rows");
+    static constexpr int CH = D / 8;           // 16-byte chunks per row
+    static constexpr int BYTES = R * D * 2;    // one tile of R rows
+    static constexpr int INSTR = R * CH / 64;  // direct-to-LDS instructions per tile
 
     // physical chunk = logical chunk ^ swz(row)
     __device__ static inline int swz(int r)
