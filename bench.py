@@ -37,7 +37,7 @@ def parse():
                              "frontier-mix"] + [f"sweep-n{n}-{m}" for n in (1, 2, 4, 8)
                                                 for m in ("intra", "mix")])
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-tokens", type=int, default=384)
+    ap.add_argument("--cpu-sample-tokens", type=int, default=768)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run a plain device-to-device copy of BYTES (3 times) and exit; "
                          "used to scale HBM traffic counters")
@@ -213,7 +213,8 @@ def main():
         achieved = per_launch / (avg_ms * 1e-3) / 1e12
         roofline = {"kernel": dom[0], "bound": "mfma", "achieved": round(achieved, 2),
                     "peak": W.MI355X_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(achieved / W.MI355X_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                    "frac": round(achieved / W.MI355X_BF16_PEAK_TFLOPS, 4),
+                    "traffic": measured_traffic(dom[0], args.workload),
                     "flop_per_launch": per_launch, "avg_launch_ms": round(avg_ms, 5)}
     else:
         roofline = {"kernel": dom[0], "bound": "hbm", "achieved": None, "peak": 8000.0,
@@ -244,6 +245,45 @@ def main():
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_sample_tokens)
     print(json.dumps(out), flush=True)
+
+
+# sources each kernel family is built from (a change voids stored counter readings)
+KERNEL_SOURCES = {
+    "sfa_dkdv_bf16": ["sfa_bwd_bf16.hip", "sfa_lds.h", "hd_device.h", "hd_internal.h"],
+    "sfa_dq_bf16": ["sfa_bwd_bf16.hip", "sfa_lds.h", "hd_device.h", "hd_internal.h"],
+    "sfa_fwd_bf16": ["sfa_fwd_bf16.hip", "sfa_lds.h", "hd_device.h", "hd_internal.h"],
+}
+
+
+def kernel_source_hash(kernel):
+    import hashlib
+    fam = next((f for f in KERNEL_SOURCES if kernel.startswith(f)), None)
+    if fam is None:
+        return None
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[fam]:
+        with open(os.path.join(ROOT, "paper_2607_08186_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 counter summary
+    (FETCH_SIZE and WRITE_SIZE, each scaled by the factor a plain copy of known size
+    reads), or None when there is none for this kernel and workload or the kernel's
+    sources changed since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{kernel}_{workload}.txt")
+    if not os.path.exists(path):
+        return None
+    kv = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                key, val = line.split(":", 1)
+                kv[key.strip()] = val.strip()
+    if kv.get("source_sha") != kernel_source_hash(kernel):
+        return None
+    return int(float(kv["hbm_bytes_per_launch"]))
 
 
 def cpu_baseline(Ls):

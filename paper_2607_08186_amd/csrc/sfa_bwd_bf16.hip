@@ -124,6 +124,10 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const int kw0 = k0 + kw * 32;
     const int key = kw0 + l32;
 
+    // Sweep: for each query head of the group, the query tiles from the last one down
+    // to the one holding the first key.  Workgroups of one problem that run together
+    // (decode_key_tile keeps a problem's key tiles on one XCD) then read the same Q/dO
+    // tiles at about the same time, so most of those reads hit in L2.
     const int qt_first = k0 / kRows;
     const int qt_end = (g.len + kRows - 1) / kRows;
     const int nqt = qt_end - qt_first;
@@ -141,7 +145,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const int krow = (kw & 1) * 32 + l32;                                      // my key's row there
 
     auto issue = [&](int it, int st) __attribute__((always_inline)) {
-        const int gi = it / nqt, qt = qt_first + it % nqt;
+        const int gi = it / nqt, qt = qt_end - 1 - it % nqt;
         const int hq = hk * g.G + gi;
         const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
         const int row0 = qt * kRows;
@@ -192,7 +196,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     auto step = [&](int it, auto stage) __attribute__((always_inline)) {
         constexpr int st = decltype(stage)::value;
         if (it + 1 < iters) issue(it + 1, st ^ 1);
-        const int qlo = (qt_first + it % nqt) * kRows + qb * 32;
+        const int qlo = (qt_end - 1 - it % nqt) * kRows + qb * 32;
         if (qlo + 31 >= kw0) {  // wave-uniform: some of my 32 queries see some of my keys
             const char *qt = smem + st * STAGE;
             const char *dot = qt + T::BYTES;
