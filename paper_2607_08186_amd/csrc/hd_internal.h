@@ -57,13 +57,14 @@ hipError_t launch_bwd_f32(const float *q, const float *k, const float *v, const 
                           const float *lse, const float *dO, float *dq, float *dk, float *dv,
                           const SfaGeom &g, void *ws, hipStream_t s);
 
-// Per query row, fp32 [B][Hq][N]: esize 4 stores delta = rowsum(dO * O) and
-// lse2 = lse * log2(e); esize 2 (bf16 path) stores -delta and -lse / scale.
-hipError_t launch_bwd_preprocess(const void *o, const void *dO, const float *lse, float *delta,
-                                 float *lse2, const SfaGeom &g, int esize, hipStream_t s);
+// fp32 path: per query row, fp32 [B][Hq][N], delta = rowsum(dO * O) and
+// lse2 = lse * log2(e).
+hipError_t launch_bwd_preprocess_f32(const float *o, const float *dO, const float *lse,
+                                     float *delta, float *lse2, const SfaGeom &g, hipStream_t s);
 
 // Backward workspace, each part 256-byte aligned:
-//   the per-row statistics of launch_bwd_preprocess: fp32 [B][Hq][N];
+//   per-row statistics, fp32 [B][Hq][N] each: for fp32 those of
+//   launch_bwd_preprocess_f32, for bf16 -Delta and -lse/scale (written by the dQ pass);
 //   bf16 path only: a transposed copy of k per key/value problem, [problem][D][len_pad]
 //   with len_pad = len rounded up to 64 and the positions inside every 16-group in
 //   swap23 order (zeros past len).

@@ -287,8 +287,9 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
 template <int D>
 __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
-    const bf16 *__restrict__ dO, const float *__restrict__ delta, const float *__restrict__ lse2,
-    const bf16 *__restrict__ kt, bf16 *__restrict__ dq, SfaGeom g, int len_pad)
+    const bf16 *__restrict__ o, const float *__restrict__ lse, const bf16 *__restrict__ dO,
+    float *__restrict__ nstat_d, float *__restrict__ nstat_l, const bf16 *__restrict__ kt,
+    bf16 *__restrict__ dq, SfaGeom g, int len_pad)
 {
     constexpr int KS = D / 16, DB = D / 32;
     using T = Tile<D>;
@@ -335,19 +336,37 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     };
     issue(0);
 
+    // This lane's query row (dims kk*16 + hi*8 .. +7 of every k-step) of Q and dO, and
+    // the row statistics: lse in log2 units and Delta = rowsum(dO * O), from the
+    // forward's O and lse.  Every query row belongs to exactly one workgroup, which
+    // also stores -Delta and -lse/scale for the dK/dV pass.
     bf16x8 qr[KS], dor[KS];
     float lrow = 0.f, drow = 0.f;
     {
+        const rsrc_t ro = make_rsrc(o + b * qslice, (uint32_t)(qslice * 2));
         const uint32_t off = row < g.len ? qbase + (uint32_t)row * qstride : kOob;
+        float dpart = 0.f;
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk) {
             qr[kk] = __builtin_bit_cast(bf16x8, ld16(rq, off + (kk * 16 + hi * 8) * 2));
-            dor[kk] = __builtin_bit_cast(bf16x8, ld16(rdo, off + (kk * 16 + hi * 8) * 2));
+            const u32x4 dw = ld16(rdo, off + (kk * 16 + hi * 8) * 2);
+            const u32x4 ow = ld16(ro, off + (kk * 16 + hi * 8) * 2);
+            dor[kk] = __builtin_bit_cast(bf16x8, dw);
+#pragma unroll
+            for (int w = 0; w < 4; ++w) {
+                dpart = __builtin_fmaf(bf16_lo(dw[w]), bf16_lo(ow[w]), dpart);
+                dpart = __builtin_fmaf(bf16_hi(dw[w]), bf16_hi(ow[w]), dpart);
+            }
         }
-        if (row < g.len) {  // -lse/scale and -Delta of this row
+        drow = dpart + __shfl_xor(dpart, 32);
+        if (row < g.len) {
             const size_t li = ((size_t)b * g.Hq + hq) * g.N + (size_t)row * g.rowmul + s;
-            lrow = -lse2[li] * g.scale_log2;  // lse in log2 units
-            drow = -delta[li];
+            const float l = lse[li];
+            lrow = l * 1.4426950408889634f;
+            if (hi == 0) {
+                nstat_d[li] = -drow;
+                nstat_l[li] = -l / g.scale;
+            }
         }
     }
 
@@ -439,10 +458,10 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
 }
 
 template <int D>
-hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *dO,
-                      const float *delta, const float *lse2, bf16 *kt, int len_pad, bf16 *dq,
-                      bf16 *dk, bf16 *dv, const SfaGeom &g, hipStream_t s, const char *tr_name,
-                      const char *dq_name, const char *dkdv_name)
+hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o,
+                      const float *lse, const bf16 *dO, float *delta, float *lse2, bf16 *kt,
+                      int len_pad, bf16 *dq, bf16 *dk, bf16 *dv, const SfaGeom &g, hipStream_t s,
+                      const char *tr_name, const char *dq_name, const char *dkdv_name)
 {
     timing_before(tr_name, s);
     transpose_k_kernel<D><<<g.B * g.Hkv * g.streams * (len_pad / kRows), 256, 0, s>>>(k, kt, g,
@@ -453,7 +472,7 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *d
     const int nqt = (g.len + kRowsPerWg - 1) / kRowsPerWg;
     timing_before(dq_name, s);
     sfa_dq_bf16_kernel<D><<<nqt * g.B * g.Hq * g.streams, kDqWaves * 64, 0, s>>>(
-        q, k, v, dO, delta, lse2, kt, dq, g, len_pad);
+        q, k, v, o, lse, dO, delta, lse2, kt, dq, g, len_pad);
     e = hipGetLastError();
     timing_after(s);
     if (e != hipSuccess) return e;
@@ -477,18 +496,17 @@ hipError_t launch_bwd_bf16(const void *q, const void *k, const void *v, const vo
     float *delta = reinterpret_cast<float *>(wsb + w.delta);
     float *lse2 = reinterpret_cast<float *>(wsb + w.lse2);
     bf16 *kt = reinterpret_cast<bf16 *>(wsb + w.kt);
-    hipError_t e = launch_bwd_preprocess(o, dO, lse, delta, lse2, g, 2, s);
-    if (e != hipSuccess) return e;
     const bf16 *qq = static_cast<const bf16 *>(q), *kk = static_cast<const bf16 *>(k),
-               *vv = static_cast<const bf16 *>(v), *dd = static_cast<const bf16 *>(dO);
+               *vv = static_cast<const bf16 *>(v), *dd = static_cast<const bf16 *>(dO),
+               *oo = static_cast<const bf16 *>(o);
     bf16 *gq = static_cast<bf16 *>(dq), *gk = static_cast<bf16 *>(dk), *gv = static_cast<bf16 *>(dv);
     if (g.D == 32)
-        return bwd_bf16_d<32>(qq, kk, vv, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
+        return bwd_bf16_d<32>(qq, kk, vv, oo, lse, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
                               "sfa_bwd_transpose_d32", "sfa_dq_bf16_d32", "sfa_dkdv_bf16_d32");
     if (g.D == 64)
-        return bwd_bf16_d<64>(qq, kk, vv, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
+        return bwd_bf16_d<64>(qq, kk, vv, oo, lse, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
                               "sfa_bwd_transpose_d64", "sfa_dq_bf16_d64", "sfa_dkdv_bf16_d64");
-    return bwd_bf16_d<128>(qq, kk, vv, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
+    return bwd_bf16_d<128>(qq, kk, vv, oo, lse, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
                            "sfa_bwd_transpose_d128", "sfa_dq_bf16_d128", "sfa_dkdv_bf16_d128");
 }
 

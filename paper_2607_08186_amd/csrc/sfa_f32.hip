@@ -1,5 +1,5 @@
-// sfa_f32.hip -- fp32 Stream-Factorized Attention forward/backward, and the backward
-// preprocess shared with the bf16 path.
+// sfa_f32.hip -- fp32 Stream-Factorized Attention forward/backward (with its backward
+// preprocess; the bf16 path forms the same row statistics inside its dQ pass).
 //
 // The fp32 kernels serve small, accuracy-first workloads: one lane owns one query row
 // (forward, dQ) or one key row (dK/dV), tiles of the other operand are staged in LDS
@@ -82,37 +82,26 @@ __global__ __launch_bounds__(64) void sfa_fwd_f32_kernel(const float *__restrict
     }
 }
 
-// Per (b, hq, p) query row: delta = sum_d dO * O and lse2 = lse * log2(e); with NEG the
-// kernel stores -delta and -lse / scale instead (the starting values of the dP and S
-// accumulators of the bf16 backward).  One group of lanes per row, 16 bytes per lane,
-// reduced with xor shuffles.
-template <typename T, int D, bool NEG>
-__global__ __launch_bounds__(256) void bwd_preprocess_kernel(const T *__restrict__ o,
-                                                             const T *__restrict__ dO,
+// Per (b, hq, p) query row: delta = sum_d dO * O and lse2 = lse * log2(e).  One group
+// of lanes per row, 16 bytes per lane, reduced with xor shuffles.
+template <int D>
+__global__ __launch_bounds__(256) void bwd_preprocess_kernel(const float *__restrict__ o,
+                                                             const float *__restrict__ dO,
                                                              const float *__restrict__ lse,
                                                              float *__restrict__ delta,
                                                              float *__restrict__ lse2, SfaGeom g)
 {
-    constexpr int EPL = 16 / sizeof(T);  // elements per lane
-    constexpr int LPR = D / EPL;         // lanes per row
-    constexpr int RPB = 256 / LPR;       // rows per workgroup
+    constexpr int LPR = D / 4;      // lanes per row, 4 floats each
+    constexpr int RPB = 256 / LPR;  // rows per workgroup
     const size_t rows = (size_t)g.B * g.N * g.Hq;
     const size_t r = (size_t)blockIdx.x * RPB + threadIdx.x / LPR;
     const int part = threadIdx.x % LPR;
     float acc = 0.f;
     if (r < rows) {
-        const u32x4 a = *reinterpret_cast<const u32x4 *>(o + r * D + part * EPL);
-        const u32x4 c = *reinterpret_cast<const u32x4 *>(dO + r * D + part * EPL);
-        if constexpr (sizeof(T) == 2) {
+        const u32x4 a = *reinterpret_cast<const u32x4 *>(o + r * D + part * 4);
+        const u32x4 c = *reinterpret_cast<const u32x4 *>(dO + r * D + part * 4);
 #pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                acc = __builtin_fmaf(bf16_lo(a[w]), bf16_lo(c[w]), acc);
-                acc = __builtin_fmaf(bf16_hi(a[w]), bf16_hi(c[w]), acc);
-            }
-        } else {
-#pragma unroll
-            for (int w = 0; w < 4; ++w) acc = __builtin_fmaf(__uint_as_float(a[w]), __uint_as_float(c[w]), acc);
-        }
+        for (int w = 0; w < 4; ++w) acc = __builtin_fmaf(__uint_as_float(a[w]), __uint_as_float(c[w]), acc);
     }
 #pragma unroll
     for (int off = LPR / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
@@ -121,13 +110,8 @@ __global__ __launch_bounds__(256) void bwd_preprocess_kernel(const T *__restrict
         const size_t bp = r / g.Hq;  // b * N + p
         const size_t b = bp / g.N, p = bp % g.N;
         const size_t li = (b * g.Hq + hq) * g.N + p;
-        if constexpr (NEG) {
-            delta[li] = -acc;
-            lse2[li] = -lse[li] / g.scale;
-        } else {
-            delta[li] = acc;
-            lse2[li] = lse[li] * kLog2e;
-        }
+        delta[li] = acc;
+        lse2[li] = lse[li] * kLog2e;
     }
 }
 
@@ -305,28 +289,20 @@ hipError_t bwd_f32_d(const float *q, const float *k, const float *v, const float
 
 }  // namespace
 
-hipError_t launch_bwd_preprocess(const void *o, const void *dO, const float *lse, float *delta,
-                                 float *lse2, const SfaGeom &g, int esize, hipStream_t s)
+hipError_t launch_bwd_preprocess_f32(const float *o, const float *dO, const float *lse,
+                                     float *delta, float *lse2, const SfaGeom &g, hipStream_t s)
 {
     const size_t rows = (size_t)g.B * g.N * g.Hq;
-    const int lpr = g.D * esize / 16;
+    const int lpr = g.D * 4 / 16;
     const int rpb = 256 / lpr;
     const dim3 grid((unsigned)((rows + rpb - 1) / rpb));
-    timing_before(esize == 2 ? "sfa_bwd_preprocess_bf16" : "sfa_bwd_preprocess_f32", s);
-#define HD_PRE(T, DD, NEG)                                                                         \
-    bwd_preprocess_kernel<T, DD, NEG><<<grid, 256, 0, s>>>(static_cast<const T *>(o),              \
-                                                           static_cast<const T *>(dO), lse, delta, \
-                                                           lse2, g)
-    if (esize == 2) {
-        if (g.D == 32) HD_PRE(bf16, 32, true);
-        else if (g.D == 64) HD_PRE(bf16, 64, true);
-        else HD_PRE(bf16, 128, true);
-    } else {
-        if (g.D == 32) HD_PRE(float, 32, false);
-        else if (g.D == 64) HD_PRE(float, 64, false);
-        else HD_PRE(float, 128, false);
-    }
-#undef HD_PRE
+    timing_before("sfa_bwd_preprocess_f32", s);
+    if (g.D == 32)
+        bwd_preprocess_kernel<32><<<grid, 256, 0, s>>>(o, dO, lse, delta, lse2, g);
+    else if (g.D == 64)
+        bwd_preprocess_kernel<64><<<grid, 256, 0, s>>>(o, dO, lse, delta, lse2, g);
+    else
+        bwd_preprocess_kernel<128><<<grid, 256, 0, s>>>(o, dO, lse, delta, lse2, g);
     hipError_t e = hipGetLastError();
     timing_after(s);
     return e;
@@ -347,7 +323,7 @@ hipError_t launch_bwd_f32(const float *q, const float *k, const float *v, const 
     const BwdWorkspace w = bwd_workspace(g, 4);
     float *delta = reinterpret_cast<float *>(static_cast<char *>(ws) + w.delta);
     float *lse2 = reinterpret_cast<float *>(static_cast<char *>(ws) + w.lse2);
-    hipError_t e = launch_bwd_preprocess(o, dO, lse, delta, lse2, g, 4, s);
+    hipError_t e = launch_bwd_preprocess_f32(o, dO, lse, delta, lse2, g, s);
     if (e != hipSuccess) return e;
     if (g.D == 32) return bwd_f32_d<32>(q, k, v, dO, dq, dk, dv, g, delta, lse2, s);
     if (g.D == 64) return bwd_f32_d<64>(q, k, v, dO, dq, dk, dv, g, delta, lse2, s);
