@@ -5,8 +5,8 @@ Only the tests, ``__graft_entry__.smoke()`` and the ``cpu_baseline`` leg of
 Python binding) never imports, links or calls it.
 
 The arithmetic lives in ``sfa_oracle.c`` (fp64, explicit mask from the paper's
-definitions: eq. (expansion), eq. (indices), eq. (mask_intra) and the causal mask of
-Fig. "masks"(a)).  This module only marshals numpy arrays through ctypes and
+definitions: eq. (expansion), eq. (indices), eq. (mask_intra), the causal mask of
+Fig. "masks"(a) and its sliding-window form of Fig. "masks"(b)).  This module only marshals numpy arrays through ctypes and
 builds the shared object with gcc.
 """
 from __future__ import annotations
@@ -21,7 +21,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "sfa_oracle.c")
 _LIB = os.path.join(_HERE, "liboracle.so")
 
-INTRA, MIX = 0, 1
+INTRA, MIX, LOCAL = 0, 1, 2
 _F64, _F32, _BF16 = 0, 1, 2
 
 _lib = None
@@ -45,7 +45,7 @@ def _load():
     lib = ctypes.CDLL(_LIB)
     i64, vp, i32 = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
     dbl = ctypes.c_double
-    dims = [i64] * 6 + [i32, dbl, i32]  # B L n Hq Hkv D mode scale nthreads
+    dims = [i64] * 6 + [i32, i64, dbl, i32]  # B L n Hq Hkv D mode window scale nthreads
     lib.oracle_sfa_fwd.argtypes = [vp, vp, vp, i32, vp, vp] + dims
     lib.oracle_sfa_fwd_rows.argtypes = [vp, vp, vp, i32, vp, i64, vp, vp] + dims
     lib.oracle_sfa_bwd.argtypes = [vp, vp, vp, vp, i32, vp, vp, vp] + dims
@@ -56,7 +56,7 @@ def _load():
         f.restype = None
     lib.oracle_expand_embed.argtypes = [vp, vp, vp, i64, i64, i64, i64, i64, i64]
     lib.oracle_expand_embed.restype = i64
-    lib.oracle_sfa_mask.argtypes = [vp, i64, i64, i32]
+    lib.oracle_sfa_mask.argtypes = [vp, i64, i64, i32, i64]
     lib.oracle_sfa_mask.restype = None
     _lib = lib
     return lib
@@ -89,33 +89,39 @@ def _ptr(a: np.ndarray):
     return a.ctypes.data_as(ctypes.c_void_p)
 
 
-def _dims(q, k, B, L, n, mode, scale, nthreads):
+def _check_window(mode, window):
+    if int(mode) == LOCAL and int(window) < 1:
+        raise ValueError("local mode needs a window of at least 1 expanded position")
+
+
+def _dims(q, k, B, L, n, mode, scale, nthreads, window=0):
     N = n * L
     if q.shape[:2] != (B, N) or k.shape[:2] != (B, N) or q.shape[3] != k.shape[3]:
         raise ValueError("q must be [B][n*L][Hq][D] and k/v [B][n*L][Hkv][D]")
     Hq, D, Hkv = q.shape[2], q.shape[3], k.shape[2]
     if Hq % Hkv:
         raise ValueError("Hq must be a multiple of Hkv")
-    return (B, L, n, Hq, Hkv, D, int(mode), float(scale),
+    _check_window(mode, window)
+    return (B, L, n, Hq, Hkv, D, int(mode), int(window), float(scale),
             int(nthreads or default_threads())), Hq, Hkv, D
 
 
-def sfa_fwd(q, k, v, *, L, n, mode, scale, nthreads=None):
+def sfa_fwd(q, k, v, *, L, n, mode, scale, nthreads=None, window=0):
     """Full forward. Returns (o [B][N][Hq][D], lse [B][Hq][N]) in float64."""
     (q, k, v), code = _prep(q, k, v)
     B = q.shape[0]
-    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads)
+    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads, window)
     o = np.zeros((B, n * L, Hq, D))
     lse = np.zeros((B, Hq, n * L))
     _load().oracle_sfa_fwd(_ptr(q), _ptr(k), _ptr(v), code, _ptr(o), _ptr(lse), *dims)
     return o, lse
 
 
-def sfa_fwd_rows(q, k, v, rows, *, L, n, mode, scale, nthreads=None):
+def sfa_fwd_rows(q, k, v, rows, *, L, n, mode, scale, nthreads=None, window=0):
     """Forward of listed rows; rows is int64 [R][3] of (b, hq, p)."""
     (q, k, v), code = _prep(q, k, v)
     rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
-    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads)
+    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads, window)
     o = np.zeros((len(rows), D))
     lse = np.zeros(len(rows))
     _load().oracle_sfa_fwd_rows(_ptr(q), _ptr(k), _ptr(v), code, _ptr(rows), len(rows),
@@ -123,11 +129,11 @@ def sfa_fwd_rows(q, k, v, rows, *, L, n, mode, scale, nthreads=None):
     return o, lse
 
 
-def sfa_bwd(q, k, v, dout, *, L, n, mode, scale, nthreads=None):
+def sfa_bwd(q, k, v, dout, *, L, n, mode, scale, nthreads=None, window=0):
     """Full backward from (q, k, v, dO). Returns (dq, dk, dv) in float64."""
     (q, k, v, dout), code = _prep(q, k, v, dout)
     B = q.shape[0]
-    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads)
+    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads, window)
     dq = np.zeros((B, n * L, Hq, D))
     dk = np.zeros((B, n * L, Hkv, D))
     dv = np.zeros((B, n * L, Hkv, D))
@@ -136,22 +142,22 @@ def sfa_bwd(q, k, v, dout, *, L, n, mode, scale, nthreads=None):
     return dq, dk, dv
 
 
-def sfa_bwd_dq_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None):
+def sfa_bwd_dq_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None, window=0):
     """dQ of listed query rows (b, hq, p)."""
     (q, k, v, dout), code = _prep(q, k, v, dout)
     rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
-    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads)
+    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads, window)
     dq = np.zeros((len(rows), D))
     _load().oracle_sfa_bwd_dq_rows(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), code, _ptr(rows),
                                    len(rows), _ptr(dq), *dims)
     return dq
 
 
-def sfa_bwd_dkdv_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None):
+def sfa_bwd_dkdv_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None, window=0):
     """dK, dV of listed key rows (b, hk, j), summed over the group's query heads."""
     (q, k, v, dout), code = _prep(q, k, v, dout)
     rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
-    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads)
+    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads, window)
     dk = np.zeros((len(rows), D))
     dv = np.zeros((len(rows), D))
     _load().oracle_sfa_bwd_dkdv_rows(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), code, _ptr(rows),
@@ -171,9 +177,10 @@ def expand_embed(ids, tables):
     return out, int(bad)
 
 
-def sfa_mask(L, n, mode):
+def sfa_mask(L, n, mode, window=0):
     """Explicit [N][N] 0/1 mask straight from the definitions."""
+    _check_window(mode, window)
     N = n * L
     m = np.zeros((N, N), dtype=np.uint8)
-    _load().oracle_sfa_mask(_ptr(m), L, n, int(mode))
+    _load().oracle_sfa_mask(_ptr(m), L, n, int(mode), int(window))
     return m

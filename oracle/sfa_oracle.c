@@ -16,6 +16,10 @@
  *   - full cross-stream ("mixing") mask, Fig. "masks" (a): the standard causal mask
  *     over the expanded sequence, written here in token/stream form:
  *     t(p') < t(p), or t(p') == t(p) and s(p') <= s(p);
+ *   - local cross-stream mask, Fig. "masks" (b): the causal mask above restricted to
+ *     a sliding window of w expanded positions, p - p' < w (its cost, O(nLw), is
+ *     stated in the appendix on layouts; w itself is not given in the paper and is an
+ *     argument here);
  *   - softmax attention under that mask, its log-sum-exp, and the analytic
  *     gradients with respect to q, k and v (standard softmax-attention calculus:
  *     dP = dO v^T, Delta = dO . O, dS = P (dP - Delta), dQ = scale dS K,
@@ -41,7 +45,7 @@
 #include <stdlib.h>
 #include <string.h>
 
-enum { ORC_INTRA = 0, ORC_MIX = 1 };
+enum { ORC_INTRA = 0, ORC_MIX = 1, ORC_LOCAL = 2 };
 enum { ORC_F64 = 0, ORC_F32 = 1, ORC_BF16 = 2 };
 
 /* ---------------------------------------------------------------- inputs */
@@ -51,6 +55,7 @@ typedef struct {
     int dtype;
     int64_t B, L, n, Hq, Hkv, D;
     int mode;
+    int64_t window; /* local cross-stream layers only */
     double scale;
 } problem_t;
 
@@ -72,14 +77,17 @@ static int64_t token_of(int64_t p, int64_t n) { return p / n; }
 static int64_t stream_of(int64_t p, int64_t n) { return p % n; }
 
 /* 1 if key position pk is visible from query position pq */
-static int visible(int mode, int64_t n, int64_t pq, int64_t pk)
+static int visible(int mode, int64_t n, int64_t window, int64_t pq, int64_t pk)
 {
     int64_t t = token_of(pq, n), s = stream_of(pq, n);
     int64_t tk = token_of(pk, n), sk = stream_of(pk, n);
     if (mode == ORC_INTRA) /* eq. (mask_intra): same stream, not later */
         return sk == s && pk <= pq;
     /* full cross-stream layer: causal over the expanded sequence */
-    return tk < t || (tk == t && sk <= s);
+    int causal = tk < t || (tk == t && sk <= s);
+    if (mode == ORC_LOCAL) /* ... and fewer than w expanded positions back */
+        return causal && pq - pk < window;
+    return causal;
 }
 
 static int64_t q_index(const problem_t *P, int64_t b, int64_t p, int64_t h, int64_t d)
@@ -105,7 +113,7 @@ static void row_forward(const problem_t *P, int64_t b, int64_t hq, int64_t p,
     const int64_t hk = hq / (P->Hq / P->Hkv);
     double m = -INFINITY;
     for (int64_t j = 0; j < N; ++j) {
-        if (!visible(P->mode, P->n, p, j)) { x[j] = -INFINITY; continue; }
+        if (!visible(P->mode, P->n, P->window, p, j)) { x[j] = -INFINITY; continue; }
         double dot = 0.0;
         for (int64_t d = 0; d < D; ++d)
             dot += load_elem(P->q, P->dtype, q_index(P, b, p, hq, d)) *
@@ -120,7 +128,7 @@ static void row_forward(const problem_t *P, int64_t b, int64_t hq, int64_t p,
         x[j] = (x[j] == -INFINITY) ? 0.0 : exp(x[j] - m) / l;
     for (int64_t d = 0; d < D; ++d) o[d] = 0.0;
     for (int64_t j = 0; j < N; ++j) {
-        if (!visible(P->mode, P->n, p, j)) continue;
+        if (!visible(P->mode, P->n, P->window, p, j)) continue;
         for (int64_t d = 0; d < D; ++d)
             o[d] += x[j] * load_elem(P->v, P->dtype, kv_index(P, b, j, hk, d));
     }
@@ -146,7 +154,7 @@ static void row_backward(const problem_t *P, int64_t b, int64_t hq, int64_t p,
     if (dq)
         for (int64_t d = 0; d < D; ++d) dq[d] = 0.0;
     for (int64_t j = 0; j < N; ++j) {
-        if (!visible(P->mode, P->n, p, j)) continue;
+        if (!visible(P->mode, P->n, P->window, p, j)) continue;
         int64_t slot = j;
         if (only_key) { /* restrict dk/dv accumulation to listed keys */
             slot = -1;
@@ -226,18 +234,18 @@ static void *fwd_job(void *arg)
 
 static problem_t make_problem(const void *q, const void *k, const void *v, const void *dout,
                               int dtype, int64_t B, int64_t L, int64_t n, int64_t Hq,
-                              int64_t Hkv, int64_t D, int mode, double scale)
+                              int64_t Hkv, int64_t D, int mode, int64_t window, double scale)
 {
-    problem_t P = {q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, scale};
+    problem_t P = {q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, window, scale};
     return P;
 }
 
 /* Full forward: o [B][N][Hq][D], lse [B][Hq][N]. */
 void oracle_sfa_fwd(const void *q, const void *k, const void *v, int dtype, double *o,
                     double *lse, int64_t B, int64_t L, int64_t n, int64_t Hq, int64_t Hkv,
-                    int64_t D, int mode, double scale, int nthreads)
+                    int64_t D, int mode, int64_t window, double scale, int nthreads)
 {
-    problem_t P = make_problem(q, k, v, NULL, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    problem_t P = make_problem(q, k, v, NULL, dtype, B, L, n, Hq, Hkv, D, mode, window, scale);
     job_t J = {&P, 0, 0, {o, lse}, NULL, 0};
     run_jobs(fwd_job, &J, B * Hq, nthreads);
 }
@@ -262,9 +270,9 @@ static void *fwd_rows_job(void *arg)
 void oracle_sfa_fwd_rows(const void *q, const void *k, const void *v, int dtype,
                          const int64_t *rows, int64_t nrows, double *o_rows,
                          double *lse_rows, int64_t B, int64_t L, int64_t n, int64_t Hq,
-                         int64_t Hkv, int64_t D, int mode, double scale, int nthreads)
+                         int64_t Hkv, int64_t D, int mode, int64_t window, double scale, int nthreads)
 {
-    problem_t P = make_problem(q, k, v, NULL, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    problem_t P = make_problem(q, k, v, NULL, dtype, B, L, n, Hq, Hkv, D, mode, window, scale);
     job_t J = {&P, 0, 0, {o_rows, lse_rows}, rows, nrows};
     run_jobs(fwd_rows_job, &J, nrows, nthreads);
 }
@@ -309,9 +317,9 @@ static void *bwd_job(void *arg)
 /* Full backward from (q, k, v, dO): dq [B][N][Hq][D], dk/dv [B][N][Hkv][D]. */
 void oracle_sfa_bwd(const void *q, const void *k, const void *v, const void *dout, int dtype,
                     double *dq, double *dk, double *dv, int64_t B, int64_t L, int64_t n,
-                    int64_t Hq, int64_t Hkv, int64_t D, int mode, double scale, int nthreads)
+                    int64_t Hq, int64_t Hkv, int64_t D, int mode, int64_t window, double scale, int nthreads)
 {
-    problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, window, scale);
     job_t J = {&P, 0, 0, {dq, dk, dv}, NULL, 0};
     run_jobs(bwd_job, &J, B * Hkv, nthreads);
 }
@@ -340,9 +348,9 @@ static void *dq_rows_job(void *arg)
 void oracle_sfa_bwd_dq_rows(const void *q, const void *k, const void *v, const void *dout,
                             int dtype, const int64_t *rows, int64_t nrows, double *dq_rows,
                             int64_t B, int64_t L, int64_t n, int64_t Hq, int64_t Hkv,
-                            int64_t D, int mode, double scale, int nthreads)
+                            int64_t D, int mode, int64_t window, double scale, int nthreads)
 {
-    problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, window, scale);
     job_t J = {&P, 0, 0, {dq_rows}, rows, nrows};
     run_jobs(dq_rows_job, &J, nrows, nthreads);
 }
@@ -361,7 +369,7 @@ static void *dkdv_rows_job(void *arg)
         for (int64_t d = 0; d < D; ++d) dk[r * D + d] = dv[r * D + d] = 0.0;
         for (int64_t hq = hk * G; hq < (hk + 1) * G; ++hq)
             for (int64_t p = 0; p < N; ++p) {
-                if (!visible(P->mode, P->n, p, j)) continue;
+                if (!visible(P->mode, P->n, P->window, p, j)) continue;
                 double lse;
                 row_forward(P, b, hq, p, x, o, &lse);
                 row_backward(P, b, hq, p, x, o, NULL, &dk[r * D], &dv[r * D], &j, 1);
@@ -376,9 +384,9 @@ static void *dkdv_rows_job(void *arg)
 void oracle_sfa_bwd_dkdv_rows(const void *q, const void *k, const void *v, const void *dout,
                               int dtype, const int64_t *rows, int64_t nrows, double *dk_rows,
                               double *dv_rows, int64_t B, int64_t L, int64_t n, int64_t Hq,
-                              int64_t Hkv, int64_t D, int mode, double scale, int nthreads)
+                              int64_t Hkv, int64_t D, int mode, int64_t window, double scale, int nthreads)
 {
-    problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, scale);
+    problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, window, scale);
     job_t J = {&P, 0, 0, {dk_rows, dv_rows}, rows, nrows};
     run_jobs(dkdv_rows_job, &J, nrows, nthreads);
 }
@@ -413,9 +421,9 @@ int64_t oracle_expand_embed(const int32_t *ids, const void *tables, void *out, i
 }
 
 /* Mask as bytes [N][N] straight from the definition (for probes and pins). */
-void oracle_sfa_mask(unsigned char *mask, int64_t L, int64_t n, int mode)
+void oracle_sfa_mask(unsigned char *mask, int64_t L, int64_t n, int mode, int64_t window)
 {
     const int64_t N = n * L;
     for (int64_t p = 0; p < N; ++p)
-        for (int64_t j = 0; j < N; ++j) mask[p * N + j] = (unsigned char)visible(mode, n, p, j);
+        for (int64_t j = 0; j < N; ++j) mask[p * N + j] = (unsigned char)visible(mode, n, window, p, j);
 }

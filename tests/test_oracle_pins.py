@@ -16,7 +16,7 @@ import torch.nn.functional as F
 
 from paper_2607_08186_amd import synth
 
-INTRA, MIX = 0, 1
+INTRA, MIX, LOCAL = 0, 1, 2
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
@@ -114,13 +114,14 @@ def test_masks_match_hand_written_golden(oracle_mod):
     want = {}
     cur = None
     for ln in lines:
-        if ln in ("intra", "mix"):
+        if ln in ("intra", "mix", "local3"):
             cur = ln
             want[cur] = []
         else:
             want[cur].append([int(c) for c in ln])
     np.testing.assert_array_equal(oracle_mod.sfa_mask(3, 2, INTRA), np.array(want["intra"]))
     np.testing.assert_array_equal(oracle_mod.sfa_mask(3, 2, MIX), np.array(want["mix"]))
+    np.testing.assert_array_equal(oracle_mod.sfa_mask(3, 2, LOCAL, 3), np.array(want["local3"]))
 
 
 @pytest.mark.parametrize("L,n", [(5, 3), (16, 4), (7, 1), (4, 8)])
@@ -355,3 +356,129 @@ def test_expand_bad_ids_zero_and_counted(oracle_mod):
     np.testing.assert_array_equal(out[0, 6], tables[0, 3])
     np.testing.assert_array_equal(out[0, 7], tables[1, 3])
     np.testing.assert_array_equal(out[1, 3], tables[1, 2])
+
+
+# ------------------------------------------------------------------ local layers
+
+
+def _torch_masked(q, k, v, do, scale, keep):
+    """Library attention with an explicit boolean keep-mask [S][S] (True = visible)."""
+    Hq, Hkv = q.shape[2], k.shape[2]
+    G = Hq // Hkv
+    tq = torch.tensor(q).permute(0, 2, 1, 3).contiguous().requires_grad_(True)
+    tk = torch.tensor(k).permute(0, 2, 1, 3).contiguous().requires_grad_(True)
+    tv = torch.tensor(v).permute(0, 2, 1, 3).contiguous().requires_grad_(True)
+    kk = tk.repeat_interleave(G, dim=1)
+    vv = tv.repeat_interleave(G, dim=1)
+    keep_t = torch.tensor(keep)
+    o = F.scaled_dot_product_attention(tq, kk, vv, attn_mask=keep_t, scale=scale)
+    o.backward(torch.tensor(do).permute(0, 2, 1, 3))
+    logits = scale * torch.matmul(tq.detach(), kk.detach().transpose(-1, -2))
+    lse = torch.logsumexp(logits.masked_fill(~keep_t, float("-inf")), dim=-1)
+    back = lambda t: t.permute(0, 2, 1, 3).detach().numpy()
+    return back(o), lse.numpy(), back(tq.grad), back(tk.grad), back(tv.grad)
+
+
+def _band(S, w):
+    i = np.arange(S)
+    return (i[None, :] <= i[:, None]) & (i[:, None] - i[None, :] < w)
+
+
+@pytest.mark.parametrize("L,n,w", [(5, 3, 1), (16, 4, 7), (7, 1, 3), (4, 8, 13), (6, 2, 100)])
+def test_local_mask_is_window_of_prefix(oracle_mod, L, n, w):
+    """LOCAL row p sees exactly range(max(0, p - w + 1), p + 1)."""
+    N = n * L
+    m = oracle_mod.sfa_mask(L, n, LOCAL, w)
+    for p in range(N):
+        want = np.zeros(N, np.uint8)
+        want[max(0, p - w + 1): p + 1] = 1
+        np.testing.assert_array_equal(m[p], want)
+
+
+@pytest.mark.parametrize("shape,w", [((1, 9, 1, 2, 2, 6), 4), ((2, 5, 3, 4, 2, 8), 6),
+                                     ((1, 6, 4, 3, 3, 5), 9), ((1, 8, 2, 2, 1, 4), 1)])
+def test_local_equals_sliding_window_attention(oracle_mod, shape, w):
+    """LOCAL(w) == library attention under a sliding-window band over the expanded rows."""
+    B, L, n, Hq, Hkv, D = shape
+    q, k, v, do = _rand(21, *shape)
+    scale = 1.0 / math.sqrt(D)
+    kw = dict(L=L, n=n, mode=LOCAL, scale=scale, window=w)
+    o, lse = oracle_mod.sfa_fwd(q, k, v, **kw)
+    dq, dk, dv = oracle_mod.sfa_bwd(q, k, v, do, **kw)
+    ro, rlse, rdq, rdk, rdv = _torch_masked(q, k, v, do, scale, _band(n * L, w))
+    for got, ref in ((o, ro), (lse, rlse), (dq, rdq), (dk, rdk), (dv, rdv)):
+        np.testing.assert_allclose(got, ref, atol=1e-12, rtol=0)
+
+
+def test_local_wide_window_equals_mix(oracle_mod):
+    B, L, n, Hq, Hkv, D = 1, 6, 3, 2, 1, 4
+    q, k, v, do = _rand(22, B, L, n, Hq, Hkv, D)
+    a = oracle_mod.sfa_fwd(q, k, v, L=L, n=n, mode=LOCAL, scale=0.4, window=n * L)
+    b = oracle_mod.sfa_fwd(q, k, v, L=L, n=n, mode=MIX, scale=0.4)
+    np.testing.assert_array_equal(a[0], b[0])
+    np.testing.assert_array_equal(a[1], b[1])
+    ga = oracle_mod.sfa_bwd(q, k, v, do, L=L, n=n, mode=LOCAL, scale=0.4, window=10 * n * L)
+    gb = oracle_mod.sfa_bwd(q, k, v, do, L=L, n=n, mode=MIX, scale=0.4)
+    for x, y in zip(ga, gb):
+        np.testing.assert_array_equal(x, y)
+
+
+def test_local_window_one_closed_form(oracle_mod):
+    """w = 1: every row sees only itself, so O = v of its own row, lse = scale q.k, dV
+    collects the group's dO, and dQ = dK = 0 (P = 1 makes dS = 0)."""
+    B, L, n, Hq, Hkv, D = 1, 5, 2, 4, 2, 3
+    q, k, v, do = _rand(23, B, L, n, Hq, Hkv, D)
+    G = Hq // Hkv
+    kw = dict(L=L, n=n, mode=LOCAL, scale=0.7, window=1)
+    o, lse = oracle_mod.sfa_fwd(q, k, v, **kw)
+    dq, dk, dv = oracle_mod.sfa_bwd(q, k, v, do, **kw)
+    kr = np.repeat(k, G, axis=2)
+    vr = np.repeat(v, G, axis=2)
+    np.testing.assert_allclose(o, vr, atol=1e-14)
+    np.testing.assert_allclose(lse, 0.7 * np.einsum("bphd,bphd->bhp", q, kr), atol=1e-13)
+    np.testing.assert_allclose(dv, do.reshape(B, n * L, Hkv, G, D).sum(3), atol=1e-13)
+    np.testing.assert_allclose(dq, 0, atol=1e-13)
+    np.testing.assert_allclose(dk, 0, atol=1e-13)
+
+
+def test_local_finite_differences_every_entry_small(oracle_mod):
+    B, L, n, Hq, Hkv, D = 1, 4, 3, 2, 1, 4
+    q, k, v, do = _rand(24, B, L, n, Hq, Hkv, D)
+    scale = 1.0 / math.sqrt(D)
+    kw = dict(L=L, n=n, mode=LOCAL, scale=scale, window=5)
+    grads = oracle_mod.sfa_bwd(q, k, v, do, **kw)
+    h = 1e-6
+
+    def f(qq, kk, vv):
+        o, _ = oracle_mod.sfa_fwd(qq, kk, vv, nthreads=1, **kw)
+        return float((do * o).sum())
+
+    for idx, g in enumerate(grads):
+        x = [q, k, v][idx]
+        for e in range(x.size):
+            args = [q.copy(), k.copy(), v.copy()]
+            args[idx].flat[e] += h
+            fp = f(*args)
+            args[idx].flat[e] -= 2 * h
+            fd = (fp - f(*args)) / (2 * h)
+            assert abs(fd - g.flat[e]) <= 1e-6 * max(np.abs(g).max(), 1.0)
+
+
+def test_local_row_sampled_entry_points_match_full(oracle_mod):
+    B, L, n, Hq, Hkv, D = 2, 6, 3, 4, 2, 5
+    q, k, v, do = _rand(25, B, L, n, Hq, Hkv, D)
+    kw = dict(L=L, n=n, mode=LOCAL, scale=0.5, window=7)
+    o, lse = oracle_mod.sfa_fwd(q, k, v, **kw)
+    dq, dk, dv = oracle_mod.sfa_bwd(q, k, v, do, **kw)
+    rows = np.array([[0, 1, 0], [1, 3, 17], [0, 2, 9], [1, 0, 11]])
+    ro, rl = oracle_mod.sfa_fwd_rows(q, k, v, rows, **kw)
+    rdq = oracle_mod.sfa_bwd_dq_rows(q, k, v, do, rows, **kw)
+    for i, (b, h, p) in enumerate(rows):
+        np.testing.assert_allclose(ro[i], o[b, p, h], atol=1e-14)
+        np.testing.assert_allclose(rl[i], lse[b, h, p], atol=1e-14)
+        np.testing.assert_allclose(rdq[i], dq[b, p, h], atol=1e-14)
+    krows = np.array([[0, 1, 0], [1, 0, 17], [0, 1, 9]])
+    rdk, rdv = oracle_mod.sfa_bwd_dkdv_rows(q, k, v, do, krows, **kw)
+    for i, (b, h, j) in enumerate(krows):
+        np.testing.assert_allclose(rdk[i], dk[b, j, h], atol=1e-14)
+        np.testing.assert_allclose(rdv[i], dv[b, j, h], atol=1e-14)
