@@ -33,9 +33,12 @@ def parse():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="stack36",
-                    choices=["stack36", "qwen8b-intra", "qwen8b-mix", "frontier-intra",
-                             "frontier-mix"] + [f"sweep-n{n}-{m}" for n in (1, 2, 4, 8)
-                                                for m in ("intra", "mix")])
+                    choices=["stack36"] + [f"{w}-{m}" for w in ("qwen8b", "frontier")
+                                           for m in ("intra", "mix", "local")]
+                    + [f"sweep-n{n}-{m}" for n in (1, 2, 4, 8) for m in ("intra", "mix", "local")])
+    ap.add_argument("--window", type=int, default=None,
+                    help="window of local layers in expanded positions "
+                         "(default: the workloads' 4096)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-tokens", type=int, default=768)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -55,11 +58,11 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_calibration_bytes": nbytes, "launches": 3}))
 
 
-def per_kernel_flops(shape, mode):
+def per_kernel_flops(shape, mode, window):
     """Algorithmic flop per kernel family for one layer (useful pairs only)."""
     from paper_2607_08186_amd import workloads as W
 
-    pairs = W.visible_pairs(shape, mode)
+    pairs = W.visible_pairs(shape, mode, window)
     D = shape.D
     # forward: S = QK^T and O = PV; dK/dV pass: S, dP, dV, dK; dQ pass: dQ only
     # (it recomputes S and dP, which the useful count does not credit twice)
@@ -99,6 +102,9 @@ def main():
     stream = torch.cuda.current_stream()
 
     # ---------------------------------------------------------------- workload
+    window = args.window if args.window is not None else W.LOCAL_WINDOW
+    if window < 1:
+        raise SystemExit("--window must be >= 1")
     if args.workload == "stack36":
         shape = W.QWEN8B.shape
         modes = W.stack_modes()
@@ -110,7 +116,7 @@ def main():
         spike = None
     else:
         parts = args.workload.split("-")
-        m = W.INTRA if parts[-1] == "intra" else W.MIX
+        m = {"intra": W.INTRA, "mix": W.MIX, "local": W.LOCAL}[parts[-1]]
         if parts[0] == "qwen8b":
             wl = W.QWEN8B
         elif parts[0] == "frontier":
@@ -119,6 +125,8 @@ def main():
             wl = {w.shape.n: w for w in W.SWEEP}[int(parts[1][1:])]
         shape, modes, with_embed = wl.shape, [m], False
         wl_desc = f"{wl.name} {W.MODE_NAMES[m]} fwd+bwd"
+        if m == W.LOCAL:
+            wl_desc += f" (window {window} expanded positions)"
         std, spike = wl.qkv_std, wl.k_spike
     s = shape
     nl = len(modes)
@@ -164,12 +172,21 @@ def main():
             hd.hd_expand_embed(ids, tables, emb, 1, s.L, s.n, W.STACK_VOCAB, W.STACK_DMODEL,
                                stream=stream)
         for ly in layers:
-            hd.hd_sfa_fwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L, s.n, s.Hq,
-                          s.Hkv, s.D, ly["mode"], scale, stream=stream)
+            if ly["mode"] == W.LOCAL:
+                hd.hd_sfa_fwd_local(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L,
+                                    s.n, s.Hq, s.Hkv, s.D, window, scale, stream=stream)
+            else:
+                hd.hd_sfa_fwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L, s.n,
+                              s.Hq, s.Hkv, s.D, ly["mode"], scale, stream=stream)
         for ly in reversed(layers):
-            hd.hd_sfa_bwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq, dk, dv,
-                          s.B, s.L, s.n, s.Hq, s.Hkv, s.D, ly["mode"], scale, ws, ws_bytes,
-                          stream=stream)
+            if ly["mode"] == W.LOCAL:
+                hd.hd_sfa_bwd_local(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq,
+                                    dk, dv, s.B, s.L, s.n, s.Hq, s.Hkv, s.D, window, scale, ws,
+                                    ws_bytes, stream=stream)
+            else:
+                hd.hd_sfa_bwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq, dk,
+                              dv, s.B, s.L, s.n, s.Hq, s.Hkv, s.D, ly["mode"], scale, ws,
+                              ws_bytes, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -187,14 +204,14 @@ def main():
     hd.hd_timing_enable(False)
     ktimes = hd.hd_timing_collect()
 
-    flop_step = sum(W.useful_flop(s, m) for m in modes)
+    flop_step = sum(W.useful_flop(s, m, window=window) for m in modes)
     ms_per_step = elapsed * 1e3 / args.steps
     value = flop_step * args.steps / elapsed / 1e12
 
     # ------------------------------------------------------ per-kernel roofline
     fam_flops = {}
     for m in modes:
-        for fam, f in per_kernel_flops(s, m).items():
+        for fam, f in per_kernel_flops(s, m, window).items():
             fam_flops[fam] = fam_flops.get(fam, 0) + f
     per_kernel = []
     fam_ms = {}
@@ -237,6 +254,7 @@ def main():
         "data": "synthetic (seeded device normal draws; no dataset or weights)",
         "config": {"workload": wl_desc, "B": s.B, "L": s.L, "n": s.n, "Hq": s.Hq,
                    "Hkv": s.Hkv, "D": s.D, "layers": nl,
+                   **({"window": window} if W.LOCAL in modes else {}),
                    "useful_tflop_per_step": round(flop_step / 1e12, 4)},
         "frac_of_peak": round(value / W.MI355X_BF16_PEAK_TFLOPS, 4),
         "roofline": roofline, "breakdown": breakdown, "per_kernel": per_kernel,

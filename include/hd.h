@@ -48,8 +48,12 @@ typedef enum {
  *   HD_SFA_MIX   -- full cross-stream layer, Fig. "masks" panel (a): the standard
  *                   causal mask over the expanded sequence, i.e. t' < t, or t' == t
  *                   and s' <= s (p' <= p).
+ *   HD_SFA_LOCAL -- local cross-stream layer, Fig. "masks" panel (b): the causal mask
+ *                   of HD_SFA_MIX restricted to a sliding window of w expanded
+ *                   positions, p - w < p' <= p.  The paper gives no w, so it is an
+ *                   explicit argument of the *_local entry points below.
  */
-typedef enum { HD_SFA_INTRA = 0, HD_SFA_MIX = 1 } hd_sfa_mode_t;
+typedef enum { HD_SFA_INTRA = 0, HD_SFA_MIX = 1, HD_SFA_LOCAL = 2 } hd_sfa_mode_t;
 
 typedef enum { HD_DTYPE_BF16 = 0, HD_DTYPE_F32 = 1 } hd_dtype_t;
 
@@ -84,15 +88,28 @@ hd_status_t hd_expand_embed(const int32_t *ids, const void *tables, void *out, i
  * Every row sees at least its own key, so no row is empty and no output is NaN for
  * finite inputs.  INTRA reads only the keys of the query's own stream.
  * Errors: INVALID_ARG for null pointers, any size <= 0, Hq % Hkv != 0, bad scale,
- *         misalignment or oversize tensors; UNSUPPORTED for D not in {32, 64, 128}.
+ *         misalignment or oversize tensors, or mode HD_SFA_LOCAL (which needs a window:
+ *         hd_sfa_fwd_local); UNSUPPORTED for D not in {32, 64, 128}.
  */
 hd_status_t hd_sfa_fwd(const void *q, const void *k, const void *v, void *o, float *lse,
                        int B, int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode,
                        float scale, hd_dtype_t dtype, hd_stream_t stream);
 
 /*
- * hd_sfa_bwd_workspace_bytes -- device workspace hd_sfa_bwd needs for these sizes
- * (per-row softmax statistics).  Returns 0 for arguments hd_sfa_bwd would reject.
+ * hd_sfa_fwd_local -- hd_sfa_fwd for a local cross-stream layer (Fig. "masks" panel
+ * (b)): query p sees keys p' with p - window < p' <= p, so every row sees its own key
+ * and at most `window` keys in all.  window >= N gives the HD_SFA_MIX result.  Only the
+ * key tiles that meet a query tile's window are read, so the cost is O(N * window).
+ * Arguments, layouts and errors as hd_sfa_fwd, plus INVALID_ARG for window < 1.
+ */
+hd_status_t hd_sfa_fwd_local(const void *q, const void *k, const void *v, void *o, float *lse,
+                             int B, int L, int n, int Hq, int Hkv, int D, int window,
+                             float scale, hd_dtype_t dtype, hd_stream_t stream);
+
+/*
+ * hd_sfa_bwd_workspace_bytes -- device workspace hd_sfa_bwd (and, for mode
+ * HD_SFA_LOCAL, hd_sfa_bwd_local) needs for these sizes (per-row softmax statistics,
+ * and for bf16 a transposed copy of k).  Returns 0 for arguments those would reject.
  */
 size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
                                   hd_sfa_mode_t mode, hd_dtype_t dtype);
@@ -115,6 +132,18 @@ hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *
                        int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode, float scale,
                        hd_dtype_t dtype, void *workspace, size_t workspace_bytes,
                        hd_stream_t stream);
+
+/*
+ * hd_sfa_bwd_local -- hd_sfa_bwd for a local cross-stream layer (Fig. "masks" panel
+ * (b)) of the given window; lse as written by hd_sfa_fwd_local with the same window,
+ * workspace sized by hd_sfa_bwd_workspace_bytes(..., HD_SFA_LOCAL, dtype).
+ * Arguments, layouts and errors as hd_sfa_bwd, plus INVALID_ARG for window < 1.
+ */
+hd_status_t hd_sfa_bwd_local(const void *q, const void *k, const void *v, const void *o,
+                             const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                             int B, int L, int n, int Hq, int Hkv, int D, int window,
+                             float scale, hd_dtype_t dtype, void *workspace,
+                             size_t workspace_bytes, hd_stream_t stream);
 
 /* Static name of a status code ("HD_OK", ...). */
 const char *hd_status_str(hd_status_t s);

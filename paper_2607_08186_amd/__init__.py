@@ -4,12 +4,12 @@ through the C ABI of include/hd.h (libhd.so) and this thin Python binding.
 
 The library is loaded lazily on the first call; a missing build raises ImportError.
 """
-from .binding import (HD_DTYPE_BF16, HD_DTYPE_F32, HD_SFA_INTRA, HD_SFA_MIX, HDError,
-                      expand_embed, hd_expand_embed, hd_sfa_bwd, hd_sfa_bwd_workspace_bytes,
-                      hd_sfa_fwd, hd_timing_collect, hd_timing_enable, sfa_backward,
-                      sfa_forward)
+from .binding import (HD_DTYPE_BF16, HD_DTYPE_F32, HD_SFA_INTRA, HD_SFA_LOCAL, HD_SFA_MIX,
+                      HDError, expand_embed, hd_expand_embed, hd_sfa_bwd, hd_sfa_bwd_local,
+                      hd_sfa_bwd_workspace_bytes, hd_sfa_fwd, hd_sfa_fwd_local,
+                      hd_timing_collect, hd_timing_enable, sfa_backward, sfa_forward)
 
-__all__ = ["HD_DTYPE_BF16", "HD_DTYPE_F32", "HD_SFA_INTRA", "HD_SFA_MIX", "HDError",
-           "expand_embed", "hd_expand_embed", "hd_sfa_bwd", "hd_sfa_bwd_workspace_bytes",
-           "hd_sfa_fwd", "hd_timing_collect", "hd_timing_enable", "sfa_backward",
-           "sfa_forward"]
+__all__ = ["HD_DTYPE_BF16", "HD_DTYPE_F32", "HD_SFA_INTRA", "HD_SFA_LOCAL", "HD_SFA_MIX",
+           "HDError", "expand_embed", "hd_expand_embed", "hd_sfa_bwd", "hd_sfa_bwd_local",
+           "hd_sfa_bwd_workspace_bytes", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_timing_collect",
+           "hd_timing_enable", "sfa_backward", "sfa_forward"]

@@ -14,12 +14,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libhd.so")
 
 HD_OK, HD_ERR_INVALID_ARG, HD_ERR_UNSUPPORTED, HD_ERR_HIP = 0, 1, 2, 3
-HD_SFA_INTRA, HD_SFA_MIX = 0, 1
+HD_SFA_INTRA, HD_SFA_MIX, HD_SFA_LOCAL = 0, 1, 2
 HD_DTYPE_BF16, HD_DTYPE_F32 = 0, 1
 
 # every symbol include/hd.h declares
-EXPORTS = ("hd_expand_embed", "hd_sfa_fwd", "hd_sfa_bwd_workspace_bytes", "hd_sfa_bwd",
-           "hd_status_str", "hd_last_error", "hd_timing_enable", "hd_timing_collect")
+EXPORTS = ("hd_expand_embed", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
+           "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
+           "hd_timing_enable", "hd_timing_collect")
 
 
 class HDError(RuntimeError):
@@ -55,7 +56,11 @@ def lib() -> ctypes.CDLL:
     L.hd_sfa_bwd_workspace_bytes.argtypes = [i32] * 8
     L.hd_sfa_bwd_workspace_bytes.restype = sz
     L.hd_sfa_bwd.argtypes = [vp] * 9 + [i32] * 7 + [f32, i32, vp, sz, vp]
-    for f in (L.hd_expand_embed, L.hd_sfa_fwd, L.hd_sfa_bwd, L.hd_timing_enable):
+    # the *_local variants take the window where the others take the mode
+    L.hd_sfa_fwd_local.argtypes = L.hd_sfa_fwd.argtypes
+    L.hd_sfa_bwd_local.argtypes = L.hd_sfa_bwd.argtypes
+    for f in (L.hd_expand_embed, L.hd_sfa_fwd, L.hd_sfa_fwd_local, L.hd_sfa_bwd,
+              L.hd_sfa_bwd_local, L.hd_timing_enable):
         f.restype = i32
     L.hd_status_str.argtypes = [i32]
     L.hd_status_str.restype = ctypes.c_char_p
@@ -117,6 +122,13 @@ def hd_sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, mode, scale, dtype=None, st
                             int(mode), float(scale), _dtype_code(q, dtype), _stream(stream)))
 
 
+def hd_sfa_fwd_local(q, k, v, o, lse, B, L, n, Hq, Hkv, D, window, scale, dtype=None,
+                     stream=None):
+    _check(lib().hd_sfa_fwd_local(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, L, n, Hq,
+                                  Hkv, D, int(window), float(scale), _dtype_code(q, dtype),
+                                  _stream(stream)))
+
+
 def hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, dtype) -> int:
     return int(lib().hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, int(mode), int(dtype)))
 
@@ -127,6 +139,14 @@ def hd_sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, mode, scale
                             _ptr(dk), _ptr(dv), B, L, n, Hq, Hkv, D, int(mode), float(scale),
                             _dtype_code(q, dtype), _ptr(workspace), int(workspace_bytes),
                             _stream(stream)))
+
+
+def hd_sfa_bwd_local(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, window, scale,
+                     workspace, workspace_bytes, dtype=None, stream=None):
+    _check(lib().hd_sfa_bwd_local(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dO),
+                                  _ptr(dq), _ptr(dk), _ptr(dv), B, L, n, Hq, Hkv, D, int(window),
+                                  float(scale), _dtype_code(q, dtype), _ptr(workspace),
+                                  int(workspace_bytes), _stream(stream)))
 
 
 def hd_timing_enable(enable: bool):
@@ -153,19 +173,34 @@ def _shape(q, k, n):
     return B, N // n, Hq, Hkv, D
 
 
-def sfa_forward(q, k, v, *, n, mode, scale=None, stream=None):
-    """q [B][n*L][Hq][D], k/v [B][n*L][Hkv][D] -> (o, lse [B][Hq][n*L] fp32)."""
+def sfa_forward(q, k, v, *, n, mode, scale=None, window=None, stream=None):
+    """q [B][n*L][Hq][D], k/v [B][n*L][Hkv][D] -> (o, lse [B][Hq][n*L] fp32).
+    ``window`` is required for, and only accepted with, mode HD_SFA_LOCAL."""
     import torch
 
     B, L, Hq, Hkv, D = _shape(q, k, n)
     scale = scale if scale is not None else D ** -0.5
     o = torch.empty_like(q)
     lse = torch.empty((B, Hq, n * L), dtype=torch.float32, device=q.device)
-    hd_sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, mode, scale, stream=stream)
+    if _local(mode, window):
+        hd_sfa_fwd_local(q, k, v, o, lse, B, L, n, Hq, Hkv, D, window, scale, stream=stream)
+    else:
+        hd_sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, mode, scale, stream=stream)
     return o, lse
 
 
-def sfa_backward(q, k, v, o, lse, dO, *, n, mode, scale=None, workspace=None, stream=None):
+def _local(mode, window):
+    if int(mode) == HD_SFA_LOCAL:
+        if window is None:
+            raise ValueError("mode HD_SFA_LOCAL needs a window")
+        return True
+    if window is not None:
+        raise ValueError("a window is only meaningful with mode HD_SFA_LOCAL")
+    return False
+
+
+def sfa_backward(q, k, v, o, lse, dO, *, n, mode, scale=None, window=None, workspace=None,
+                 stream=None):
     """-> (dq, dk, dv).  A workspace tensor (uint8, 256-byte aligned) may be passed in."""
     import torch
 
@@ -176,8 +211,12 @@ def sfa_backward(q, k, v, o, lse, dO, *, n, mode, scale=None, workspace=None, st
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
-    hd_sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, mode, scale, workspace,
-               workspace.numel(), stream=stream)
+    if _local(mode, window):
+        hd_sfa_bwd_local(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, window, scale,
+                         workspace, workspace.numel(), stream=stream)
+    else:
+        hd_sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, mode, scale, workspace,
+                   workspace.numel(), stream=stream)
     return dq, dk, dv
 
 

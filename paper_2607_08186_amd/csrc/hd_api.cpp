@@ -48,8 +48,8 @@ hd_status_t check_sfa(int B, int L, int n, int Hq, int Hkv, int D, int mode, flo
                     B, L, n, Hq, Hkv, D);
     if (Hq % Hkv != 0)
         return fail(HD_ERR_INVALID_ARG, "Hq=%d is not a multiple of Hkv=%d", Hq, Hkv);
-    if (mode != HD_SFA_INTRA && mode != HD_SFA_MIX)
-        return fail(HD_ERR_INVALID_ARG, "mode %d is neither HD_SFA_INTRA nor HD_SFA_MIX", mode);
+    if (mode != HD_SFA_INTRA && mode != HD_SFA_MIX && mode != HD_SFA_LOCAL)
+        return fail(HD_ERR_INVALID_ARG, "unknown mode %d", mode);
     if (!std::isfinite(scale) || !(scale > 0.f))
         return fail(HD_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", (double)scale);
     if (dtype != HD_DTYPE_BF16 && dtype != HD_DTYPE_F32)
@@ -161,17 +161,18 @@ hd_status_t hd_expand_embed(const int32_t *ids, const void *tables, void *out, i
                       "hd_expand_embed launch");
 }
 
-hd_status_t hd_sfa_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int B,
-                       int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode, float scale,
-                       hd_dtype_t dtype, hd_stream_t stream)
+namespace {
+
+hd_status_t sfa_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int B, int L,
+                    int n, int Hq, int Hkv, int D, int mode, int window, float scale,
+                    hd_dtype_t dtype, hd_stream_t stream)
 {
-    g_err[0] = 0;
     if (!q || !k || !v || !o || !lse) return fail(HD_ERR_INVALID_ARG, "null tensor pointer");
     hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, scale, dtype);
     if (st != HD_OK) return st;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
         return fail(HD_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
-    const hd::SfaGeom g = hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale);
+    const hd::SfaGeom g = hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale, window);
     hipError_t e;
     if (dtype == HD_DTYPE_BF16)
         e = hd::launch_fwd_bf16(q, k, v, o, lse, g, (hipStream_t)stream);
@@ -179,7 +180,29 @@ hd_status_t hd_sfa_fwd(const void *q, const void *k, const void *v, void *o, flo
         e = hd::launch_fwd_f32(static_cast<const float *>(q), static_cast<const float *>(k),
                                static_cast<const float *>(v), static_cast<float *>(o), lse, g,
                                (hipStream_t)stream);
-    return hip_status(e, "hd_sfa_fwd launch");
+    return hip_status(e, "sfa forward launch");
+}
+
+}  // namespace
+
+hd_status_t hd_sfa_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int B,
+                       int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode, float scale,
+                       hd_dtype_t dtype, hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (mode == HD_SFA_LOCAL)
+        return fail(HD_ERR_INVALID_ARG, "local layers take a window: use hd_sfa_fwd_local");
+    return sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, mode, 0, scale, dtype, stream);
+}
+
+hd_status_t hd_sfa_fwd_local(const void *q, const void *k, const void *v, void *o, float *lse,
+                             int B, int L, int n, int Hq, int Hkv, int D, int window, float scale,
+                             hd_dtype_t dtype, hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (window < 1) return fail(HD_ERR_INVALID_ARG, "window must be >= 1 (got %d)", window);
+    return sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, HD_SFA_LOCAL, window, scale, dtype,
+                   stream);
 }
 
 size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
@@ -194,13 +217,13 @@ size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
                                    dtype == HD_DTYPE_BF16 ? 2 : 4);
 }
 
-hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *o,
-                       const float *lse, const void *dO, void *dq, void *dk, void *dv, int B,
-                       int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode, float scale,
-                       hd_dtype_t dtype, void *workspace, size_t workspace_bytes,
-                       hd_stream_t stream)
+namespace {
+
+hd_status_t sfa_bwd(const void *q, const void *k, const void *v, const void *o, const float *lse,
+                    const void *dO, void *dq, void *dk, void *dv, int B, int L, int n, int Hq,
+                    int Hkv, int D, int mode, int window, float scale, hd_dtype_t dtype,
+                    void *workspace, size_t workspace_bytes, hd_stream_t stream)
 {
-    g_err[0] = 0;
     if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv)
         return fail(HD_ERR_INVALID_ARG, "null tensor pointer");
     hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, scale, dtype);
@@ -208,7 +231,7 @@ hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) ||
         !aligned16(dO) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
         return fail(HD_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
-    const hd::SfaGeom g = hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale);
+    const hd::SfaGeom g = hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale, window);
     const size_t need = hd::bwd_workspace_bytes(g, dtype == HD_DTYPE_BF16 ? 2 : 4);
     if (!workspace) return fail(HD_ERR_INVALID_ARG, "null workspace (%zu bytes needed)", need);
     if (reinterpret_cast<uintptr_t>(workspace) & 255)
@@ -226,7 +249,34 @@ hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *
                                static_cast<const float *>(dO), static_cast<float *>(dq),
                                static_cast<float *>(dk), static_cast<float *>(dv), g, workspace,
                                (hipStream_t)stream);
-    return hip_status(e, "hd_sfa_bwd launch");
+    return hip_status(e, "sfa backward launch");
+}
+
+}  // namespace
+
+hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *o,
+                       const float *lse, const void *dO, void *dq, void *dk, void *dv, int B,
+                       int L, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode, float scale,
+                       hd_dtype_t dtype, void *workspace, size_t workspace_bytes,
+                       hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (mode == HD_SFA_LOCAL)
+        return fail(HD_ERR_INVALID_ARG, "local layers take a window: use hd_sfa_bwd_local");
+    return sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, mode, 0, scale, dtype,
+                   workspace, workspace_bytes, stream);
+}
+
+hd_status_t hd_sfa_bwd_local(const void *q, const void *k, const void *v, const void *o,
+                             const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                             int B, int L, int n, int Hq, int Hkv, int D, int window, float scale,
+                             hd_dtype_t dtype, void *workspace, size_t workspace_bytes,
+                             hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (window < 1) return fail(HD_ERR_INVALID_ARG, "window must be >= 1 (got %d)", window);
+    return sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, HD_SFA_LOCAL, window,
+                   scale, dtype, workspace, workspace_bytes, stream);
 }
 
 hd_status_t hd_timing_enable(int enable)

@@ -15,15 +15,21 @@ namespace hd {
 struct SfaGeom {
     int B, L, n, Hq, Hkv, D, G;  // G = Hq / Hkv
     int N;                       // n * L
-    int mode;                    // 0 intra, 1 mix
+    int mode;                    // 0 intra, 1 mix (full cross-stream), 2 local cross-stream
     int len;                     // rows per problem
-    int rowmul;                  // n (intra) or 1 (mix)
-    int streams;                 // n (intra) or 1 (mix): problems per head
+    int rowmul;                  // n (intra) or 1 (mix, local)
+    int streams;                 // n (intra) or 1 (mix, local): problems per head
+    int window;                  // local: row p sees keys p-window+1 .. p; else a huge value
     float scale;                 // softmax scale
     float scale_log2;            // scale * log2(e)
 };
 
-inline SfaGeom make_geom(int B, int L, int n, int Hq, int Hkv, int D, int mode, float scale)
+constexpr int kNoWindow = 1 << 30;
+
+// Problem geometry of one call.  Local cross-stream layers decompose like the full
+// cross-stream layer (one problem per (b, hq) over all N rows) with a window.
+inline SfaGeom make_geom(int B, int L, int n, int Hq, int Hkv, int D, int mode, float scale,
+                         int window = 0)
 {
     SfaGeom g;
     g.B = B; g.L = L; g.n = n; g.Hq = Hq; g.Hkv = Hkv; g.D = D; g.G = Hq / Hkv;
@@ -32,6 +38,7 @@ inline SfaGeom make_geom(int B, int L, int n, int Hq, int Hkv, int D, int mode, 
     g.len = mode == 0 ? L : n * L;
     g.rowmul = mode == 0 ? n : 1;
     g.streams = mode == 0 ? n : 1;
+    g.window = mode == 2 ? window : kNoWindow;
     g.scale = scale;
     g.scale_log2 = scale * 1.4426950408889634f;
     return g;

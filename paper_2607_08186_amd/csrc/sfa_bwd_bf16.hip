@@ -129,7 +129,10 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     // (decode_key_tile keeps a problem's key tiles on one XCD) then read the same Q/dO
     // tiles at about the same time, so most of those reads hit in L2.
     const int qt_first = k0 / kRows;
-    const int qt_end = (g.len + kRows - 1) / kRows;
+    // last query tile that sees a key of this workgroup: the end of the sequence, or for
+    // local layers the window's end past the last key
+    const int qt_end = (int)min((int64_t)(g.len + kRows - 1) / kRows,
+                                ((int64_t)k0 + kKeysPerWg - 2 + g.window) / kRows + 1);
     const int nqt = qt_end - qt_first;
     const int iters = g.G * nqt;
 
@@ -181,8 +184,9 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
             for (int e = 0; e < 4; ++e) {
                 const int r = rq * 4 + e;
                 float x = sacc[r];
-                if constexpr (kMask) {
-                    if (qlo + 8 * rq + 4 * hi + e < key) x = -INFINITY;  // exp2 -> 0
+                if constexpr (kMask) {  // causal and, for local layers, windowed
+                    const int qd = qlo + 8 * rq + 4 * hi + e - key;  // query - key
+                    if (qd < 0 || qd >= g.window) x = -INFINITY;  // exp2 -> 0
                 }
                 p[e] = fast_exp2(x * c2);
                 ds[e] = p[e] * pacc[r];
@@ -197,7 +201,8 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
         constexpr int st = decltype(stage)::value;
         if (it + 1 < iters) issue(it + 1, st ^ 1);
         const int qlo = (qt_end - 1 - it % nqt) * kRows + qb * 32;
-        if (qlo + 31 >= kw0) {  // wave-uniform: some of my 32 queries see some of my keys
+        // wave-uniform: some of my 32 queries see some of my keys
+        if (qlo + 31 >= kw0 && qlo - kw0 < 31 + g.window) {
             const char *qt = smem + st * STAGE;
             const char *dot = qt + T::BYTES;
             const float *sl = reinterpret_cast<const float *>(qt + 2 * T::BYTES) + qb * 32;
@@ -223,7 +228,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                               T::row_operand(vtl, krow, kk, hi), pacc);
             }
             uint32_t pw[8], dw[8];
-            if (qlo < kw0 + 31)  // diagonal: causal mask
+            if (qlo < kw0 + 31 || qlo + 31 - kw0 >= g.window)  // diagonal or window edge
                 softmax(sacc, pacc, qlo, pw, dw, std::true_type{});
             else
                 softmax(sacc, pacc, qlo, pw, dw, std::false_type{});
@@ -328,13 +333,16 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
 
     const int kend = min(g.len, q0 + kRowsPerWg);
     const int nkt = (kend + kRows - 1) / kRows;
+    // first key tile any row of the workgroup sees (0 unless the layer is local); the
+    // LDS stage of tile j is (j - jf) % 2
+    const int jf = max(0, q0 - g.window + 1) / kRows;
     auto issue = [&](int j) __attribute__((always_inline)) {
-        char *st = smem[j & 1];
+        char *st = smem[(j - jf) & 1];
         T::load(st, rk, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
         T::load(st + T::BYTES, rv, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
         TT::load(st + 2 * T::BYTES, rkt, 0, (uint32_t)len_pad * 2, j * kRows, wave, kDqWaves, lane);
     };
-    issue(0);
+    issue(jf);
 
     // This lane's query row (dims kk*16 + hi*8 .. +7 of every k-step) of Q and dO, and
     // the row statistics: lse in log2 units and Delta = rowsum(dO * O), from the
@@ -392,8 +400,9 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
                 for (int u = 0; u < 2; ++u) {
                     const int r = h * 8 + 2 * e + u;
                     float p = fast_exp2(__builtin_fmaf(sacc[r], c2, -lrow));
-                    if constexpr (kMask) {
-                        if (k0 + 8 * (r >> 2) + 4 * hi + (r & 3) > row) p = 0.f;
+                    if constexpr (kMask) {  // causal and, for local layers, windowed
+                        const int key = k0 + 8 * (r >> 2) + 4 * hi + (r & 3);
+                        if (key > row || row - key >= g.window) p = 0.f;
                     }
                     ds2[u] = p * (pacc[r] - drow);
                 }
@@ -429,16 +438,18 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
         constexpr int kSt = decltype(stage)::value;
         if (j + 1 < nkt) issue(j + 1);
         const int kb0 = j * kRows;
-        if (kb0 <= wrow_max) {
+        // wave-uniform: the tile holds a key that some row of this wave sees
+        if (kb0 <= wrow_max && wrow_min - (kb0 + kRows - 1) < g.window) {
             const char *ktl = smem[kSt];
             const char *vt = ktl + T::BYTES;
             const char *ktt = ktl + 2 * T::BYTES;
-            tile_body(ktl, vt, ktt, kb0, kb0 + kRows - 1 > wrow_min);  // diagonal: mask
+            // mask on the diagonal tile and on tiles reaching a window before a row
+            tile_body(ktl, vt, ktt, kb0, kb0 + kRows - 1 > wrow_min || wrow_max - kb0 >= g.window);
         }
         wait_lds_loads();
         lds_barrier();
     };
-    for (int j = 0; j < nkt; j += 2) {
+    for (int j = jf; j < nkt; j += 2) {
         step(j, std::integral_constant<int, 0>{});
         if (j + 1 < nkt) step(j + 1, std::integral_constant<int, 1>{});
     }

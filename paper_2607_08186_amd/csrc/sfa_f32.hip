@@ -44,7 +44,9 @@ __global__ __launch_bounds__(64) void sfa_fwd_f32_kernel(const float *__restrict
     }
     float m = -INFINITY, l = 0.f;
     const int kend = min(g.len, tile * kRows + kRows);
-    for (int j0 = 0; j0 < kend; j0 += kRows) {
+    // first key any row of the tile sees (local layers: window)
+    const int kbeg = max(0, tile * kRows - g.window + 1) / kRows * kRows;
+    for (int j0 = kbeg; j0 < kend; j0 += kRows) {
         __syncthreads();
         const int key = j0 + tid;
 #pragma unroll
@@ -55,7 +57,7 @@ __global__ __launch_bounds__(64) void sfa_fwd_f32_kernel(const float *__restrict
         __syncthreads();
         if (row >= g.len) continue;
         const int jn = min(kRows, row - j0 + 1);  // causal: keys j0 .. row
-        for (int jj = 0; jj < jn; ++jj) {
+        for (int jj = max(0, row - g.window + 1 - j0); jj < jn; ++jj) {
             float dot = 0.f;
 #pragma unroll
             for (int d = 0; d < D; ++d) dot = __builtin_fmaf(qv[d], sk[jj][d], dot);
@@ -149,7 +151,8 @@ __global__ __launch_bounds__(64) void sfa_dq_f32_kernel(const float *__restrict_
     const float l2 = row < g.len ? lse2[li] : 0.f;
     const float dl = row < g.len ? delta[li] : 0.f;
     const int kend = min(g.len, tile * kRows + kRows);
-    for (int j0 = 0; j0 < kend; j0 += kRows) {
+    const int kbeg = max(0, tile * kRows - g.window + 1) / kRows * kRows;
+    for (int j0 = kbeg; j0 < kend; j0 += kRows) {
         __syncthreads();
         const int key = j0 + tid;
 #pragma unroll
@@ -160,7 +163,7 @@ __global__ __launch_bounds__(64) void sfa_dq_f32_kernel(const float *__restrict_
         __syncthreads();
         if (row >= g.len) continue;
         const int jn = min(kRows, row - j0 + 1);
-        for (int jj = 0; jj < jn; ++jj) {
+        for (int jj = max(0, row - g.window + 1 - j0); jj < jn; ++jj) {
             float dot = 0.f, dp = 0.f;
 #pragma unroll
             for (int d = 0; d < D; ++d) {
@@ -216,7 +219,9 @@ __global__ __launch_bounds__(64) void sfa_dkdv_f32_kernel(const float *__restric
         const int hq = hk * g.G + gi;
         const size_t qoff = (size_t)b * g.N * g.Hq * D + (size_t)(s * g.Hq + hq) * D;
         const size_t lbase = ((size_t)b * g.Hq + hq) * g.N + s;
-        for (int i0 = tile * kRows; i0 < g.len; i0 += kRows) {
+        // queries that see a key of this tile (local layers: up to the window's end)
+        const int qend = (int)min((int64_t)g.len, (int64_t)tile * kRows + kRows - 1 + g.window);
+        for (int i0 = tile * kRows; i0 < qend; i0 += kRows) {
             __syncthreads();
             const int qrow = i0 + tid;
 #pragma unroll
@@ -229,7 +234,9 @@ __global__ __launch_bounds__(64) void sfa_dkdv_f32_kernel(const float *__restric
             __syncthreads();
             if (key >= g.len) continue;
             const int in = min(kRows, g.len - i0);
-            for (int ii = max(0, key - i0); ii < in; ++ii) {  // causal: query >= key
+            // causal and windowed: key <= query < key + window
+            const int iend = (int)min((int64_t)in, (int64_t)key + g.window - i0);
+            for (int ii = max(0, key - i0); ii < iend; ++ii) {
                 float dot = 0.f, dp = 0.f;
 #pragma unroll
                 for (int d = 0; d < D; ++d) {

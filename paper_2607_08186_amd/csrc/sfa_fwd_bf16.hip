@@ -75,7 +75,11 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
 
     const int kend = min(g.len, q0 + kBM);
     const int nkt = (kend + kRows - 1) / kRows;
-    const int jlast = min(nkt - 1, wrow_max / kRows);  // last tile with keys this wave sees
+    // Tiles are numbered from jf, the first one holding a key that a row of this
+    // workgroup sees (0 unless the layer is local); t below is relative to jf.
+    const int jf = max(0, q0 - g.window + 1) / kRows;
+    const int ntl = nkt - jf;
+    const int jlast = min(nkt - 1, wrow_max / kRows) - jf;  // last tile with keys this wave sees
 
     // this lane's query row as the B operand of S^T = K Q^T
     bf16x8 qr[KS];
@@ -97,10 +101,10 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     // t and wait for them at the end of their next phase
     auto issue = [&](int t) __attribute__((always_inline)) {
         if (loader) {
-            if (t + 2 < nkt)
-                T::load(ks[t & 1], rk, dma, (uint32_t)((t + 2) * kRows) * kstride, lw);
-            if (t + 1 < nkt)
-                T::load(vs[(t + 1) & 1], rv, dma, (uint32_t)((t + 1) * kRows) * kstride, lw);
+            if (t + 2 < ntl)
+                T::load(ks[t & 1], rk, dma, (uint32_t)((jf + t + 2) * kRows) * kstride, lw);
+            if (t + 1 < ntl)
+                T::load(vs[(t + 1) & 1], rv, dma, (uint32_t)((jf + t + 1) * kRows) * kstride, lw);
         }
     };
 
@@ -114,7 +118,12 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     const float c2 = g.scale_log2;
     const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3f803f80u);
 
-    auto is_diag = [&](int t) __attribute__((always_inline)) { return t * kRows + kRows - 1 > wrow_min; };
+    // the tile holds keys past this wave's first row (diagonal) or, in a local layer,
+    // keys at least a window before its last row
+    auto needs_mask = [&](int t) __attribute__((always_inline)) {
+        const int kb = (jf + t) * kRows;
+        return kb + kRows - 1 > wrow_min || kb <= wrow_max - g.window;
+    };
 
     // Matrix phase of tile t: the scores of tile t+1 (DO_S) and O^T += V^T P^T of
     // tile t (DO_PV).  On the tile that holds this wave's diagonal the score
@@ -127,16 +136,20 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
         const char *vt = vs[decltype(vsl)::value];
         if constexpr (DO_S) {
             const bf16x8 a0 = T::row_at(kt, kro[0], 0), a1 = T::row_at(kt, kro[0], 2);
-            if (is_diag(t + 1)) {
-                // key = (t+1)*64 + mb*32 + 8*(r/4) + 4*hi + r%4, compared against a
-                // per-lane limit so the per-element constants stay immediates
-                const int lim = row - 4 * hi - (t + 1) * kRows;
+            if (needs_mask(t + 1)) {
+                // key = kb + c with c = mb*32 + 8*(r/4) + r%4 + 4*hi; masked if key > row
+                // or row - key >= window, compared against a per-lane limit so the
+                // per-element constants stay immediates
+                const int lim = row - 4 * hi - (jf + t + 1) * kRows;
+                const int lo = lim - g.window;
                 f32x16 bias[2];
 #pragma unroll
                 for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                    for (int r = 0; r < 16; ++r)
-                        bias[mb][r] = mb * 32 + 8 * (r >> 2) + (r & 3) > lim ? -INFINITY : 0.f;
+                    for (int r = 0; r < 16; ++r) {
+                        const int c = mb * 32 + 8 * (r >> 2) + (r & 3);
+                        bias[mb][r] = c > lim || c <= lo ? -INFINITY : 0.f;
+                    }
                 sc[0] = mfma32(a0, qr[0], bias[0]);
                 sc[1] = mfma32(a1, qr[0], bias[1]);
             } else {
@@ -179,6 +192,9 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
 #pragma unroll
             for (int db = 0; db < DB; ++db) oacc[db] *= alpha;
         }
+        // a row that has seen only masked keys so far (local layers) keeps m2 = -inf;
+        // its weights are then exp2(-inf) = 0, not NaN
+        const float m2e = m2 == -INFINITY ? 0.f : m2;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
@@ -186,8 +202,8 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
                 uint32_t w[4];
 #pragma unroll
                 for (int e = 0; e < 4; ++e) {
-                    const float p0 = fast_exp2(__builtin_fmaf(sc[mb][h * 8 + 2 * e], c2, -m2));
-                    const float p1 = fast_exp2(__builtin_fmaf(sc[mb][h * 8 + 2 * e + 1], c2, -m2));
+                    const float p0 = fast_exp2(__builtin_fmaf(sc[mb][h * 8 + 2 * e], c2, -m2e));
+                    const float p1 = fast_exp2(__builtin_fmaf(sc[mb][h * 8 + 2 * e + 1], c2, -m2e));
                     w[e] = pack_bf16(p0, p1);
                     // the row sum adds the bf16 weights that the P V product uses
                     if (mb == 0)
@@ -202,9 +218,9 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
 
     // Prologue: K of tiles 0, 1 and V of tile 0 resident (and the query row).
     if (loader) {
-        T::load(ks[0], rk, dma, 0, lw);
-        if (nkt > 1) T::load(ks[1], rk, dma, (uint32_t)kRows * kstride, lw);
-        T::load(vs[0], rv, dma, 0, lw);
+        T::load(ks[0], rk, dma, (uint32_t)(jf * kRows) * kstride, lw);
+        if (ntl > 1) T::load(ks[1], rk, dma, (uint32_t)((jf + 1) * kRows) * kstride, lw);
+        T::load(vs[0], rv, dma, (uint32_t)(jf * kRows) * kstride, lw);
     }
     wait_vmcnt_le(0);
     lds_barrier();
@@ -214,7 +230,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     // phase per workgroup barrier.  Group B starts one phase after group A, so on every
     // SIMD one wave feeds the matrix unit while the other uses the vector unit.  Waves
     // that finish early pass the remaining barriers idle; every wave passes
-    // 2*nkt + 2 of them.  Loads (loader waves, group B, whose jlast is nkt-1): K of
+    // 2*ntl + 2 of them.  Loads (loader waves, group B, whose jlast is ntl-1): K of
     // t+2 goes to the slot of K of t, V of t+1 to the slot of V of t-1, both last read
     // in the matrix phases of tile t-1 (phases 2t, 2t+1); they are queued in phase
     // 2t+2 and published by the barrier of phase 2t+3, before group A's matrix phase
@@ -262,7 +278,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
         mfma_phase(t, F{}, Tr{}, Z{}, Z{});
     if (loader) wait_vmcnt_le(0);
     bar();
-    while (nb < 2 * nkt + 2) bar();
+    while (nb < 2 * ntl + 2) bar();
 
     const float l = lsum0 + lsum1 + __shfl_xor(lsum0 + lsum1, 32);
     if (row < g.len) {

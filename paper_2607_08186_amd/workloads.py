@@ -9,8 +9,13 @@ from __future__ import annotations
 import math
 from dataclasses import dataclass, field
 
-INTRA, MIX = 0, 1
-MODE_NAMES = {INTRA: "intra", MIX: "mix"}
+INTRA, MIX, LOCAL = 0, 1, 2
+MODE_NAMES = {INTRA: "intra", MIX: "mix", LOCAL: "local"}
+
+# Window of the local cross-stream layers in these workloads, in expanded positions
+# (p - w < p' <= p).  The paper names local layers (Fig. "masks" (b), cost O(nLw)) but
+# gives no w; 4096 expanded positions is a 1024-token window of the base model at n=4.
+LOCAL_WINDOW = 4096
 
 # bf16 dense MFMA peak of one MI355X (256 CU x 2.4 GHz x 4096 flop/clk/CU)
 MI355X_BF16_PEAK_TFLOPS = 2516.6
@@ -66,10 +71,14 @@ def stack_modes():
     return [MIX if i in STACK_MIX_LAYERS else INTRA for i in range(STACK_LAYERS)]
 
 
-def visible_pairs(s: Shape, mode: int) -> int:
-    """Visible (query, key) pairs summed over batch and query heads."""
+def visible_pairs(s: Shape, mode: int, window: int = LOCAL_WINDOW) -> int:
+    """Visible (query, key) pairs summed over batch and query heads (``window`` only
+    matters for local layers: row p sees min(p + 1, w) keys)."""
     if mode == INTRA:
         return s.B * s.Hq * s.n * s.L * (s.L + 1) // 2
+    if mode == LOCAL:
+        w = min(window, s.N)
+        return s.B * s.Hq * (w * (w + 1) // 2 + (s.N - w) * w)
     return s.B * s.Hq * s.N * (s.N + 1) // 2
 
 
@@ -78,10 +87,10 @@ FWD_FLOP_PER_PAIR_D = 4
 BWD_FLOP_PER_PAIR_D = 10
 
 
-def useful_flop(s: Shape, mode: int, phase: str = "fwdbwd") -> int:
+def useful_flop(s: Shape, mode: int, phase: str = "fwdbwd", window: int = LOCAL_WINDOW) -> int:
     c = {"fwd": FWD_FLOP_PER_PAIR_D, "bwd": BWD_FLOP_PER_PAIR_D,
          "fwdbwd": FWD_FLOP_PER_PAIR_D + BWD_FLOP_PER_PAIR_D}[phase]
-    return c * s.D * visible_pairs(s, mode)
+    return c * s.D * visible_pairs(s, mode, window)
 
 
 def stack_useful_flop(s: Shape = QWEN8B.shape) -> int:

@@ -35,13 +35,15 @@ def bits(t):
     return t.detach().cpu().view(torch.int16).numpy().view(np.uint16)
 
 
-def run_sfa(ins, n, mode, scale, backward=True):
-    """Forward (+ backward) through the C ABI; returns device tensors."""
+def run_sfa(ins, n, mode, scale, backward=True, window=None):
+    """Forward (+ backward) through the C ABI; returns device tensors.  ``window`` is
+    the window of a local layer (mode 2) and None otherwise."""
     q, k, v, do = (to_dev(ins[x]) for x in ("q", "k", "v", "dout"))
-    o, lse = hd.sfa_forward(q, k, v, n=n, mode=mode, scale=scale)
+    o, lse = hd.sfa_forward(q, k, v, n=n, mode=mode, scale=scale, window=window)
     out = {"o": o, "lse": lse}
     if backward:
-        dq, dk, dv = hd.sfa_backward(q, k, v, o, lse, do, n=n, mode=mode, scale=scale)
+        dq, dk, dv = hd.sfa_backward(q, k, v, o, lse, do, n=n, mode=mode, scale=scale,
+                                     window=window)
         out.update(dq=dq, dk=dk, dv=dv)
     torch.cuda.synchronize()
     return out

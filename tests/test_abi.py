@@ -62,6 +62,34 @@ def test_fwd_validation(lib, kw, code):
     assert lib.hd_last_error().decode() != ""
 
 
+def fwd_local(lib, **kw):
+    a = dict(q=FAKE, k=FAKE, v=FAKE, o=FAKE, lse=FAKE, B=1, L=8, n=2, Hq=4, Hkv=2, D=64,
+             window=5, scale=0.125, dtype=0)
+    a.update(kw)
+    return lib.hd_sfa_fwd_local(a["q"], a["k"], a["v"], a["o"], a["lse"], a["B"], a["L"],
+                                a["n"], a["Hq"], a["Hkv"], a["D"], a["window"], a["scale"],
+                                a["dtype"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(window=0), INVALID), (dict(window=-3), INVALID), (dict(q=None), INVALID),
+    (dict(Hkv=3), INVALID), (dict(scale=0.0), INVALID), (dict(D=96), UNSUPPORTED),
+    (dict(o=FAKE + 8), INVALID), (dict(dtype=4), INVALID),
+])
+def test_fwd_local_validation(lib, kw, code):
+    assert fwd_local(lib, **kw) == code
+    assert lib.hd_last_error().decode() != ""
+
+
+def test_local_mode_needs_local_entry_points(lib):
+    """A local layer without a window is an error, not a silent full causal layer."""
+    assert fwd(lib, mode=binding.HD_SFA_LOCAL) == INVALID
+    assert "hd_sfa_fwd_local" in lib.hd_last_error().decode()
+    st, _ = bwd(lib, mode=binding.HD_SFA_LOCAL)
+    assert st == INVALID
+    assert "hd_sfa_bwd_local" in lib.hd_last_error().decode()
+
+
 def bwd(lib, ws_bytes=None, ws=FAKE * 16, **kw):
     a = dict(B=1, L=8, n=2, Hq=4, Hkv=2, D=64, mode=1, scale=0.125, dtype=0)
     a.update(kw)
@@ -88,6 +116,10 @@ def test_workspace_size_formula(lib):
         lp = math.ceil(len_ / 64) * 64
         kt = a256(B * Hkv * streams * D * lp * 2)
         assert lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 0) == stats + kt
+    for dtype in (0, 1):  # a local layer decomposes like the full cross-stream layer
+        assert (lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, 2, dtype)
+                == lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, 1, dtype))
+    assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 2, 64, 3, 0) == 0  # mode
     assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 3, 64, 0, 0) == 0  # Hq % Hkv
     assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 2, 48, 0, 0) == 0  # D
 
@@ -100,6 +132,23 @@ def test_workspace_size_formula(lib):
 def test_bwd_validation(lib, kw, code):
     st, _ = bwd(lib, **kw)
     assert st == code
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(window=0), INVALID), (dict(dv=None), INVALID), (dict(ws=None), INVALID),
+    (dict(ws_bytes=16), INVALID), (dict(D=48), UNSUPPORTED), (dict(dq=FAKE + 2), INVALID),
+])
+def test_bwd_local_validation(lib, kw, code):
+    a = dict(B=1, L=8, n=2, Hq=4, Hkv=2, D=64, window=5, scale=0.125, dtype=0, ws=FAKE * 16)
+    a.update(kw)
+    need = lib.hd_sfa_bwd_workspace_bytes(a["B"], a["L"], a["n"], a["Hq"], a["Hkv"], a["D"],
+                                          binding.HD_SFA_LOCAL, a["dtype"])
+    ptrs = [kw.get(name, FAKE) for name in ["q", "k", "v", "o", "lse", "dO", "dq", "dk", "dv"]]
+    st = lib.hd_sfa_bwd_local(*ptrs, a["B"], a["L"], a["n"], a["Hq"], a["Hkv"], a["D"],
+                              a["window"], a["scale"], a["dtype"], a["ws"],
+                              kw.get("ws_bytes", need), None)
+    assert st == code
+    assert lib.hd_last_error().decode() != ""
 
 
 @pytest.mark.parametrize("args,code", [

@@ -16,7 +16,7 @@ from tests import gpu_helpers as G
 
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
-INTRA, MIX = 0, 1
+INTRA, MIX, LOCAL = 0, 1, 2
 CASES = [workloads.QWEN8B, *workloads.SWEEP, workloads.FRONTIER]
 
 
@@ -35,16 +35,17 @@ def _tail_key_rows(rng, B, Hkv, N, n, count):
     return np.array(sorted(rows), dtype=np.int64)
 
 
-@pytest.mark.parametrize("mode", [INTRA, MIX], ids=["intra", "mix"])
+@pytest.mark.parametrize("mode", [INTRA, MIX, LOCAL], ids=["intra", "mix", "local"])
 @pytest.mark.parametrize("wl", CASES, ids=[w.name for w in CASES])
 def test_fullsize_sampled(wl, mode):
     s = wl.shape
     seed = synth.seed_for(wl.name, mode, "parity")
-    print(f"fullsize {wl.name} mode={mode} seed={seed}", flush=True)
+    window = workloads.LOCAL_WINDOW if mode == LOCAL else None
+    print(f"fullsize {wl.name} mode={mode} window={window} seed={seed}", flush=True)
     ins = synth.sfa_inputs(s.B, s.L, s.n, s.Hq, s.Hkv, s.D, seed=seed, dtype="bf16",
                            qkv_std=wl.qkv_std, dout_std=wl.dout_std, k_spike=wl.k_spike)
-    got = G.run_sfa(ins, s.n, mode, s.scale)
-    kw = dict(L=s.L, n=s.n, mode=mode, scale=s.scale)
+    got = G.run_sfa(ins, s.n, mode, s.scale, window=window)
+    kw = dict(L=s.L, n=s.n, mode=mode, scale=s.scale, window=window or 0)
     rng = np.random.default_rng(seed & 0xFFFFFFFF)
 
     rows = _sample_rows(rng, s.B, s.Hq, s.N, 40)
@@ -68,7 +69,7 @@ def test_fullsize_sampled(wl, mode):
     # gradient sums over all keys, per (b, kv-head) and per stream for intra
     dout = synth.bf16_bits_to_f32(ins["dout"]).astype(np.float64)
     Gq = s.Hq // s.Hkv
-    groups = [slice(None)] if mode == MIX else [slice(st, None, s.n) for st in range(s.n)]
+    groups = [slice(None)] if mode != INTRA else [slice(st, None, s.n) for st in range(s.n)]
     for sl in groups:
         want = dout[:, sl].reshape(s.B, -1, s.Hkv, Gq, s.D).sum(axis=(1, 3))
         got_v = dv[:, sl].sum(axis=1)
