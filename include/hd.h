@@ -107,12 +107,24 @@ hd_status_t hd_sfa_fwd_local(const void *q, const void *k, const void *v, void *
                              float scale, hd_dtype_t dtype, hd_stream_t stream);
 
 /*
- * hd_sfa_bwd_workspace_bytes -- device workspace hd_sfa_bwd (and, for mode
- * HD_SFA_LOCAL, hd_sfa_bwd_local) needs for these sizes (per-row softmax statistics,
- * and for bf16 a transposed copy of k).  Returns 0 for arguments those would reject.
+ * hd_sfa_bwd_workspace_bytes -- device workspace hd_sfa_bwd needs for these sizes:
+ * two fp32 statistics per query row ([B][Hq][N] each), and for bf16 the tiles of
+ * dS = P (dP - Delta) in bf16, 16 KB per 64 query rows x 128 keys that hold a visible
+ * pair (about B*Hq*N*N bytes for HD_SFA_MIX, B*Hq*n*L*L for HD_SFA_INTRA).  For
+ * HD_SFA_LOCAL it returns the HD_SFA_MIX size, which is enough for every window;
+ * hd_sfa_bwd_local_workspace_bytes gives the (smaller) size for one window.
+ * Returns 0 for arguments hd_sfa_bwd would reject.
  */
 size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
                                   hd_sfa_mode_t mode, hd_dtype_t dtype);
+
+/*
+ * hd_sfa_bwd_local_workspace_bytes -- workspace hd_sfa_bwd_local needs for a local
+ * cross-stream layer of the given window (for bf16 about 2*B*Hq*N*window bytes of dS
+ * tiles when the window is well below N).  Returns 0 for arguments hd_sfa_bwd_local would reject.
+ */
+size_t hd_sfa_bwd_local_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D, int window,
+                                        hd_dtype_t dtype);
 
 /*
  * hd_sfa_bwd -- gradients of the forward above, recomputing the attention
@@ -124,7 +136,9 @@ size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
  * q, o, dO, dq  device [B][N][Hq][D] of `dtype`;  k, v, dk, dv  device [B][N][Hkv][D].
  * lse           device float [B][Hq][N] exactly as written by hd_sfa_fwd.
  * workspace     device, 256-byte aligned, at least hd_sfa_bwd_workspace_bytes(...)
- *               bytes; contents on entry are ignored and on exit unspecified.
+ *               bytes; contents on entry are ignored and on exit unspecified.  The
+ *               bf16 path stores dS there in its dK/dV pass and its dQ pass reads it
+ *               back, so dQ costs one product instead of a recomputation of S and dP.
  * Errors: as hd_sfa_fwd, plus INVALID_ARG for a missing or short workspace.
  */
 hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *o,
@@ -136,7 +150,7 @@ hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *
 /*
  * hd_sfa_bwd_local -- hd_sfa_bwd for a local cross-stream layer (Fig. "masks" panel
  * (b)) of the given window; lse as written by hd_sfa_fwd_local with the same window,
- * workspace sized by hd_sfa_bwd_workspace_bytes(..., HD_SFA_LOCAL, dtype).
+ * workspace of at least hd_sfa_bwd_local_workspace_bytes(..., window, dtype) bytes.
  * Arguments, layouts and errors as hd_sfa_bwd, plus INVALID_ARG for window < 1.
  */
 hd_status_t hd_sfa_bwd_local(const void *q, const void *k, const void *v, const void *o,

@@ -19,7 +19,7 @@ HD_DTYPE_BF16, HD_DTYPE_F32 = 0, 1
 
 # every symbol include/hd.h declares
 EXPORTS = ("hd_expand_embed", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
-           "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
+           "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
            "hd_timing_enable", "hd_timing_collect")
 
 
@@ -55,6 +55,8 @@ def lib() -> ctypes.CDLL:
     L.hd_sfa_fwd.argtypes = [vp, vp, vp, vp, vp] + [i32] * 7 + [f32, i32, vp]
     L.hd_sfa_bwd_workspace_bytes.argtypes = [i32] * 8
     L.hd_sfa_bwd_workspace_bytes.restype = sz
+    L.hd_sfa_bwd_local_workspace_bytes.argtypes = [i32] * 8
+    L.hd_sfa_bwd_local_workspace_bytes.restype = sz
     L.hd_sfa_bwd.argtypes = [vp] * 9 + [i32] * 7 + [f32, i32, vp, sz, vp]
     # the *_local variants take the window where the others take the mode
     L.hd_sfa_fwd_local.argtypes = L.hd_sfa_fwd.argtypes
@@ -133,6 +135,11 @@ def hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, dtype) -> int:
     return int(lib().hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, int(mode), int(dtype)))
 
 
+def hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, window, dtype) -> int:
+    return int(lib().hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, int(window),
+                                                      int(dtype)))
+
+
 def hd_sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, mode, scale, workspace,
                workspace_bytes, dtype=None, stream=None):
     _check(lib().hd_sfa_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dO), _ptr(dq),
@@ -207,7 +214,10 @@ def sfa_backward(q, k, v, o, lse, dO, *, n, mode, scale=None, window=None, works
     B, L, Hq, Hkv, D = _shape(q, k, n)
     scale = scale if scale is not None else D ** -0.5
     dtype = _dtype_code(q, None)
-    need = hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, dtype)
+    if _local(mode, window):
+        need = hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, window, dtype)
+    else:
+        need = hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, dtype)
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)

@@ -213,8 +213,23 @@ size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
     hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, 1.0f, dtype);
     memcpy(g_err, saved, sizeof g_err);
     if (st != HD_OK) return 0;
-    return hd::bwd_workspace_bytes(hd::make_geom(B, L, n, Hq, Hkv, D, mode, 1.0f),
+    // without a window a local layer gets the size of the full causal layer, which
+    // bounds that of every window
+    return hd::bwd_workspace_bytes(hd::make_geom(B, L, n, Hq, Hkv, D, mode, 1.0f, hd::kNoWindow),
                                    dtype == HD_DTYPE_BF16 ? 2 : 4);
+}
+
+size_t hd_sfa_bwd_local_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D, int window,
+                                        hd_dtype_t dtype)
+{
+    char saved[sizeof g_err];
+    memcpy(saved, g_err, sizeof g_err);
+    hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, HD_SFA_LOCAL, 1.0f, dtype);
+    memcpy(g_err, saved, sizeof g_err);
+    if (st != HD_OK || window < 1) return 0;
+    return hd::bwd_workspace_bytes(
+        hd::make_geom(B, L, n, Hq, Hkv, D, HD_SFA_LOCAL, 1.0f, window),
+        dtype == HD_DTYPE_BF16 ? 2 : 4);
 }
 
 namespace {

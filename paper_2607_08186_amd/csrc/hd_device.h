@@ -46,6 +46,12 @@ __device__ inline void st8(rsrc_t r, uint32_t off, u32x2 v)
 {
     __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(__attribute__((__vector_size__(8))) unsigned int, v), r, off, 0, 0);
 }
+// Non-temporal store (cache policy "nt"): data written once and read back much later
+// by another kernel, marked so that it does not push reused lines out of L2.
+__device__ inline void st16_nt(rsrc_t r, uint32_t off, u32x4 v)
+{
+    __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(__attribute__((__vector_size__(16))) unsigned int, v), r, off, 0, 2);
+}
 __device__ inline void st4(rsrc_t r, uint32_t off, uint32_t v)
 {
     __builtin_amdgcn_raw_buffer_store_b32(v, r, off, 0, 0);

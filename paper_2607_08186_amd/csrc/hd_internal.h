@@ -69,15 +69,67 @@ hipError_t launch_bwd_f32(const float *q, const float *k, const float *v, const 
 hipError_t launch_bwd_preprocess_f32(const float *o, const float *dO, const float *lse,
                                      float *delta, float *lse2, const SfaGeom &g, hipStream_t s);
 
+// dS tiles of the bf16 backward.  The dK/dV pass stores dS = P (dP - Delta), rounded
+// to bf16 (the precision its own dK MFMA uses), and the dQ pass reads it back, so dQ
+// costs one product instead of a recomputation of S and dP.  A tile covers 64 query
+// rows x 128 keys of one causal problem (query tile qt, key tile kt); its 16 KB are
+// laid out [query half (2)][key (128)][query (32)], i.e. for query row r (0..63) and
+// key c (0..127) of the tile the element sits at ((r >> 5) * 128 + c) * 32 + (r & 31).
+// Only tiles holding a visible pair are stored, per problem in query-tile order:
+//   causal (no window, or window >= len): query tile qt holds key tiles 0 .. qt/2,
+//     so its first tile is m(m+1) (qt = 2m) or (m+1)^2 (qt = 2m+1);
+//   local (window < len): key tiles kt_lo(qt) .. qt/2, at most `band` of them, each
+//     query tile owning `band` slots.
+constexpr int kDsRows = 64;                      // query rows per dS tile
+constexpr int kDsKeys = 128;                     // keys per dS tile
+constexpr int kDsTileBytes = kDsRows * kDsKeys * 2;
+
+// index of tile (qt, kt) inside its problem; kt_lo = ds_kt_lo(g, qt)
+__host__ __device__ inline int64_t ds_tile_index(int band, int kt_lo, int qt, int kt)
+{
+    if (band == 0) {
+        const int64_t m = qt >> 1;
+        return ((qt & 1) ? (m + 1) * (m + 1) : m * (m + 1)) + kt;
+    }
+    return (int64_t)qt * band + (kt - kt_lo);
+}
+
+// Slots per query tile of a local layer, or 0 for triangular packing: used without a
+// window (or one >= len) and whenever the band would not be smaller, so the triangular
+// size bounds every window.
+__host__ __device__ inline int ds_band(const SfaGeom &g)
+{
+    if (g.window >= g.len) return 0;
+    const int nkt = (g.len + kDsKeys - 1) / kDsKeys;
+    const int nqt = (g.len + kDsRows - 1) / kDsRows;
+    int band = (g.window - 1 + kDsKeys - 1) / kDsKeys + 1;
+    band = band < nkt ? band : nkt;
+    return (int64_t)nqt * band < ds_tile_index(0, 0, nqt, 0) ? band : 0;
+}
+
+// first key tile that query tile qt sees (used by the band index only)
+__host__ __device__ inline int ds_kt_lo(const SfaGeom &g, int qt)
+{
+    if (g.window >= g.len) return 0;
+    const int first = qt * kDsRows - g.window + 1;
+    return first > 0 ? first / kDsKeys : 0;
+}
+
+// dS tiles per causal problem
+inline int64_t ds_tiles_per_problem(const SfaGeom &g)
+{
+    const int nqt = (g.len + kDsRows - 1) / kDsRows;
+    const int band = ds_band(g);
+    return band == 0 ? ds_tile_index(0, 0, nqt, 0) : (int64_t)nqt * band;
+}
+
 // Backward workspace, each part 256-byte aligned:
 //   per-row statistics, fp32 [B][Hq][N] each: for fp32 those of
-//   launch_bwd_preprocess_f32, for bf16 -Delta and -lse/scale (written by the dQ pass);
-//   bf16 path only: a transposed copy of k per key/value problem, [problem][D][len_pad]
-//   with len_pad = len rounded up to 64 and the positions inside every 16-group in
-//   swap23 order (zeros past len).
+//   launch_bwd_preprocess_f32, for bf16 -Delta and -lse/scale;
+//   bf16 path only: the dS tiles of every problem (b, hq[, s]), problem-major.
 struct BwdWorkspace {
-    size_t delta, lse2, kt, total;
-    int len_pad;
+    size_t delta, lse2, ds, total;
+    int64_t ds_tiles;  // dS tiles per problem
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -86,13 +138,15 @@ inline BwdWorkspace bwd_workspace(const SfaGeom &g, int esize)
 {
     BwdWorkspace w;
     const size_t rows = (size_t)g.B * g.Hq * g.N;
-    w.len_pad = (g.len + 63) / 64 * 64;
     w.delta = 0;
     w.lse2 = align256(rows * 4);
-    w.kt = w.lse2 + align256(rows * 4);
-    w.total = w.kt;
-    if (esize == 2)
-        w.total += align256((size_t)g.B * g.Hkv * g.streams * g.D * w.len_pad * 2);
+    w.ds = w.lse2 + align256(rows * 4);
+    w.total = w.ds;
+    w.ds_tiles = 0;
+    if (esize == 2) {
+        w.ds_tiles = ds_tiles_per_problem(g);
+        w.total += (size_t)g.B * g.Hq * g.streams * (size_t)w.ds_tiles * kDsTileBytes;
+    }
     return w;
 }
 

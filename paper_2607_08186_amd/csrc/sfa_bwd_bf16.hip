@@ -5,7 +5,8 @@
 // -Delta:
 //   P = exp2(scale*log2(e) (q.k - lse/scale)),  dP = dO V^T,  dS = P (dP - Delta),
 //   dV = P^T dO,  dK = scale dS^T Q,  dQ = scale dS K,   Delta = rowsum(dO * O).
-// Two deterministic kernels (no atomics):
+// Three deterministic kernels (no atomics):
+//   stats: -Delta and -lse/scale of every query row.
 //   dK/dV: a workgroup owns 128 keys of one (b, kv-head[, stream]) problem (K and V
 //          resident in LDS), 32 per pair of waves, and sweeps the query tiles that see
 //          them for every query head of the group, so the grouped-query sum happens in
@@ -13,12 +14,14 @@
 //          partials once at the end.  Scores are formed as
 //          S = Q K^T (one key per lane), which makes P and dS the B operands of
 //          dV^T += dO^T P and dK^T += Q^T dS; Q and dO tiles are staged row-major and
-//          read transposed for those two products.
-//   dQ:    a workgroup owns 256 query rows (32 per wave, one row per lane as in the
-//          forward) and sweeps the key tiles at or below the diagonal:
-//          S^T = K Q^T, dP^T = V dO^T, dQ^T += K^T dS^T, with K^T read from the
-//          transposed copy in the workspace.
-// All tiles move HBM -> LDS through direct-to-LDS buffer loads into double buffers.
+//          read transposed for those two products.  The bf16 dS it forms is also
+//          stored, as 64 x 128 tiles in the workspace.
+//   dQ:    dQ = scale dS K from the stored tiles: a workgroup owns 256 query rows (32
+//          per wave, one row per lane) and streams the dS tiles and key rows at or
+//          below the diagonal through a three-stage LDS ring, dQ^T += K^T dS^T with
+//          both operands read transposed from LDS.  No S or dP is recomputed, so this
+//          pass is bound by the dS reads from HBM.
+// All tiles move HBM -> LDS through direct-to-LDS buffer loads.
 #include <type_traits>
 
 #include "sfa_lds.h"
@@ -32,48 +35,40 @@ constexpr int kDkdvWaves = 8;
 constexpr int kDqWaves = 8;
 constexpr int kRowsPerWg = kDqWaves * 32;  // dQ: 8 waves (two per SIMD) x 32 rows
 
-// Transposed copy of k for the dQ pass: for each key/value problem (b, hk, s) and each
-// 64-row tile, rows i of k (expanded position i*rowmul + s) become columns of
-// kt[prob][d][len_pad], position i stored at column swap23(i) of its 16-group; columns
-// past len are zero.
+// Row statistics for the dK/dV pass: -Delta = -rowsum(dO * O) (fp32 sum of the bf16
+// products) and -lse/scale, both fp32 [B][Hq][N].  D/8 lanes per query row, 16 bytes
+// each; rows are taken in [b][p][hq] order so the O and dO reads are contiguous.
 template <int D>
-__global__ __launch_bounds__(256) void transpose_k_kernel(const bf16 *__restrict__ k,
-                                                          bf16 *__restrict__ kt, SfaGeom g,
-                                                          int len_pad)
+__global__ __launch_bounds__(256) void bwd_stats_bf16_kernel(const bf16 *__restrict__ o,
+                                                             const bf16 *__restrict__ dO,
+                                                             const float *__restrict__ lse,
+                                                             float *__restrict__ nstat_d,
+                                                             float *__restrict__ nstat_l, SfaGeom g)
 {
-    constexpr int CH = D / 8;
-    constexpr int STR = D + 2;  // padded LDS row (elements)
-    __shared__ uint16_t sm[kRows * STR];
-    const int H = g.Hkv;
-    const int ntiles = len_pad / kRows;
-    const int tile = blockIdx.x % ntiles, prob = blockIdx.x / ntiles;
-    const int s = prob % g.streams, h = (prob / g.streams) % H, b = prob / (g.streams * H);
-    const size_t slice = (size_t)g.N * H * D;
-    const rsrc_t rx = make_rsrc(k + b * slice, (uint32_t)(slice * 2));
-    const uint32_t stride = (uint32_t)g.rowmul * H * D * 2;
-    const uint32_t base = (uint32_t)(s * H + h) * D * 2;
-    const int tid = threadIdx.x;
-    for (int idx = tid; idx < kRows * CH; idx += 256) {
-        const int r = idx / CH, ch = idx % CH, row = tile * kRows + r;
-        const u32x4 v = ld16(rx, row < g.len ? base + (uint32_t)row * stride + ch * 16 : kOob);
+    constexpr int LPR = D / 8;
+    const int64_t rows = (int64_t)g.B * g.N * g.Hq;
+    const int64_t r = ((int64_t)blockIdx.x * 256 + threadIdx.x) / LPR;
+    const int part = threadIdx.x % LPR;
+    float acc = 0.f;
+    if (r < rows) {
+        const u32x4 ow = *reinterpret_cast<const u32x4 *>(o + r * D + part * 8);
+        const u32x4 dw = *reinterpret_cast<const u32x4 *>(dO + r * D + part * 8);
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
-            sm[r * STR + ch * 8 + 2 * w] = (uint16_t)(v[w] & 0xffffu);
-            sm[r * STR + ch * 8 + 2 * w + 1] = (uint16_t)(v[w] >> 16);
+            acc = __builtin_fmaf(bf16_lo(dw[w]), bf16_lo(ow[w]), acc);
+            acc = __builtin_fmaf(bf16_hi(dw[w]), bf16_hi(ow[w]), acc);
         }
     }
-    __syncthreads();
-    bf16 *out = kt + ((size_t)prob * D) * len_pad + (size_t)tile * kRows;
-    for (int idx = tid; idx < D * (kRows / 8); idx += 256) {
-        const int d = idx / (kRows / 8), c = idx % (kRows / 8);
-        uint32_t w[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-            const uint32_t lo = sm[swap23(c * 8 + 2 * e) * STR + d];
-            const uint32_t hi = sm[swap23(c * 8 + 2 * e + 1) * STR + d];
-            w[e] = lo | (hi << 16);
-        }
-        *reinterpret_cast<u32x4 *>(out + (size_t)d * len_pad + c * 8) = u32x4{w[0], w[1], w[2], w[3]};
+    for (int m = LPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+    if (r < rows && part == 0) {
+        const int hq = (int)(r % g.Hq);
+        const int64_t bp = r / g.Hq;
+        const int p = (int)(bp % g.N);
+        const int b = (int)(bp / g.N);
+        const size_t li = ((size_t)b * g.Hq + hq) * g.N + p;
+        nstat_d[li] = -acc;
+        nstat_l[li] = -lse[li] / g.scale;
     }
 }
 
@@ -81,7 +76,7 @@ template <int D>
 __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
     const bf16 *__restrict__ dO, const float *__restrict__ delta, const float *__restrict__ lse2,
-    bf16 *__restrict__ dk, bf16 *__restrict__ dv, SfaGeom g)
+    bf16 *__restrict__ dk, bf16 *__restrict__ dv, bf16 *__restrict__ ds, int64_t ds_tiles, SfaGeom g)
 {
     constexpr int DB = D / 32, KS = D / 16;
     using T = Tile<D>;
@@ -129,6 +124,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     // (decode_key_tile keeps a problem's key tiles on one XCD) then read the same Q/dO
     // tiles at about the same time, so most of those reads hit in L2.
     const int qt_first = k0 / kRows;
+    const int band = ds_band(g);
     // last query tile that sees a key of this workgroup: the end of the sequence, or for
     // local layers the window's end past the last key
     const int qt_end = (int)min((int64_t)(g.len + kRows - 1) / kRows,
@@ -143,12 +139,19 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
         T::load(kvt + (kKeysPerWg / kRows + t) * T::BYTES, rv, kbase, kstride, k0 + t * kRows,
                 g.len, wave, kDkdvWaves, lane);
     }
+    // dS tiles of query head hq[, stream s]: this wave writes the 32 x 32 block of its
+    // keys and query half of tile (query tile qt, this key tile); the tile's byte
+    // offset inside the problem is its index times kDsTileBytes
+    auto ds_problem = [&](int gi) __attribute__((always_inline)) {
+        const int64_t prob_q = ((int64_t)b * g.Hq + hk * g.G + gi) * g.streams + s;
+        return ds + prob_q * ds_tiles * (kDsTileBytes / 2);
+    };
+    const uint32_t dsoff = (uint32_t)(qb * kDsKeys + kw * 32 + l32) * 64 + hi * 32;
     const char *ktl = kvt + (kw >> 1) * T::BYTES;                              // tile of my keys
     const char *vtl = kvt + (kKeysPerWg / kRows + (kw >> 1)) * T::BYTES;
     const int krow = (kw & 1) * 32 + l32;                                      // my key's row there
 
-    auto issue = [&](int it, int st) __attribute__((always_inline)) {
-        const int gi = it / nqt, qt = qt_end - 1 - it % nqt;
+    auto issue = [&](int gi, int qt, int st) __attribute__((always_inline)) {
         const int hq = hk * g.G + gi;
         const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
         const int row0 = qt * kRows;
@@ -162,7 +165,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
             dma_lds4(wave == 0 ? rl2 : rdl, base + 2 * T::BYTES + wave * kRows * 4, off);
         }
     };
-    if (iters > 0) issue(0, 0);
+    if (iters > 0) issue(0, qt_end - 1, 0);
 
     f32x16 adk[DB], adv[DB];
 #pragma unroll
@@ -197,10 +200,21 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
             dw[rq * 2 + 1] = pack_bf16(ds[2], ds[3]);
         }
     };
+    // Sweep position (query head gi, query tile qt) of the current step; the next step
+    // takes the tile below, or the last tile of the next head.
+    int cur_gi = 0, cur_qt = qt_end - 1;
+    const bf16 *ds_head = ds_problem(0);
     auto step = [&](int it, auto stage) __attribute__((always_inline)) {
         constexpr int st = decltype(stage)::value;
-        if (it + 1 < iters) issue(it + 1, st ^ 1);
-        const int qlo = (qt_end - 1 - it % nqt) * kRows + qb * 32;
+        const bool wrap = cur_qt == qt_first;
+        const int nxt_gi = wrap ? cur_gi + 1 : cur_gi;
+        const int nxt_qt = wrap ? qt_end - 1 : cur_qt - 1;
+        if (it + 1 < iters) issue(nxt_gi, nxt_qt, st ^ 1);
+        const int qlo = cur_qt * kRows + qb * 32;
+        const rsrc_t rds = make_rsrc(
+            ds_head + ds_tile_index(band, ds_kt_lo(g, cur_qt), cur_qt, ktile) * (kDsTileBytes / 2),
+            kDsTileBytes);
+        uint32_t dsw[8];
         // wave-uniform: some of my 32 queries see some of my keys
         if (qlo + 31 >= kw0 && qlo - kw0 < 31 + g.window) {
             const char *qt = smem + st * STAGE;
@@ -245,9 +259,34 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                     adk[db] = mfma32(T::tr_operand(qt, db * 32, kk, lane), dsb, adk[db]);
                 }
             }
+            // dw[2 rq .. 2 rq + 1]: queries 8 rq + 4 hi .. +3 of my key.  Swap the upper
+            // octets of half 0 with the lower octets of half 1, so that half 0 holds
+            // queries 0..15 and half 1 queries 16..31: 32 contiguous bytes per lane.
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const auto sw = __builtin_amdgcn_permlane32_swap(dw[i], dw[4 + i], false, false);
+                dw[i] = sw[0];
+                dw[4 + i] = sw[1];
+            }
+            dsw[0] = dw[0]; dsw[1] = dw[1]; dsw[2] = dw[4]; dsw[3] = dw[5];
+            dsw[4] = dw[2]; dsw[5] = dw[3]; dsw[6] = dw[6]; dsw[7] = dw[7];
+        } else {
+            // no visible pair in this block: its part of the tile is zero
+#pragma unroll
+            for (int i = 0; i < 8; ++i) dsw[i] = 0u;
         }
-        wait_lds_loads();
+        st16_nt(rds, dsoff, u32x4{dsw[0], dsw[1], dsw[2], dsw[3]});
+        st16_nt(rds, dsoff + 16, u32x4{dsw[4], dsw[5], dsw[6], dsw[7]});
+        // the next tile's loads were issued before this step's two dS stores; vector
+        // memory operations complete in order, so once at most those stores are
+        // outstanding the tile has landed
+        __builtin_amdgcn_sched_barrier(0);
+        asm volatile("" ::: "memory");
+        wait_vmcnt_le(2);
         lds_barrier();
+        cur_gi = nxt_gi;
+        cur_qt = nxt_qt;
+        if (wrap) ds_head = ds_problem(nxt_gi);
     };
     for (int it = 0; it < iters; it += 2) {
         step(it, std::integral_constant<int, 0>{});
@@ -291,16 +330,16 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
 
 template <int D>
 __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
-    const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
-    const bf16 *__restrict__ o, const float *__restrict__ lse, const bf16 *__restrict__ dO,
-    float *__restrict__ nstat_d, float *__restrict__ nstat_l, const bf16 *__restrict__ kt,
-    bf16 *__restrict__ dq, SfaGeom g, int len_pad)
+    const bf16 *__restrict__ k, const bf16 *__restrict__ ds, bf16 *__restrict__ dq, SfaGeom g,
+    int64_t ds_tiles)
 {
-    constexpr int KS = D / 16, DB = D / 32;
+    constexpr int DB = D / 32;
+    constexpr int kStages = 3;
     using T = Tile<D>;
-    using TT = TileT<D>;
-    // [stage][K rows | V rows | K transposed]
-    __shared__ __attribute__((aligned(1024))) char smem[2][2 * T::BYTES + TT::BYTES];
+    // a wave's dS slab of one 64-key step: 64 keys x 32 queries, 64 bytes per key
+    constexpr int kSlab = kRows * 64;
+    constexpr int kStage = T::BYTES + kDqWaves * kSlab;  // K rows | dS slabs
+    __shared__ __attribute__((aligned(1024))) char smem[kStages][kStage];
 
     const int ntiles = (g.len + kRowsPerWg - 1) / kRowsPerWg;
     const int nprob = g.B * g.Hq * g.streams;
@@ -312,14 +351,8 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const int hk = hq / g.G;
 
     const size_t qslice = (size_t)g.N * g.Hq * D, kslice = (size_t)g.N * g.Hkv * D;
-    const rsrc_t rq = make_rsrc(q + b * qslice, (uint32_t)(qslice * 2));
-    const rsrc_t rdo = make_rsrc(dO + b * qslice, (uint32_t)(qslice * 2));
     const rsrc_t rdq = make_rsrc(dq + b * qslice, (uint32_t)(qslice * 2));
     const rsrc_t rk = make_rsrc(k + b * kslice, (uint32_t)(kslice * 2));
-    const rsrc_t rv = make_rsrc(v + b * kslice, (uint32_t)(kslice * 2));
-    const size_t ktslice = (size_t)D * len_pad;  // one key/value problem, transposed
-    const rsrc_t rkt = make_rsrc(kt + ((size_t)(b * g.Hkv + hk) * g.streams + s) * ktslice,
-                                 (uint32_t)(ktslice * 2));
     const uint32_t qstride = (uint32_t)g.rowmul * g.Hq * D * 2;
     const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
     const uint32_t kstride = (uint32_t)g.rowmul * g.Hkv * D * 2;
@@ -330,128 +363,79 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const int l32 = lane & 31, hi = lane >> 5;
     const int q0 = tile * kRowsPerWg;
     const int row = q0 + wave * 32 + l32;
+    const int wrow_min = q0 + wave * 32, wrow_max = wrow_min + 31;
+    // my rows are half (wave & 1) of dS query tile qt
+    const int qt = wrow_min / kDsRows;
+    const int band = ds_band(g);
+    const int kt_lo = ds_kt_lo(g, qt);
+    const bf16 *ds_prob = ds + (int64_t)prob * ds_tiles * (kDsTileBytes / 2);
 
     const int kend = min(g.len, q0 + kRowsPerWg);
     const int nkt = (kend + kRows - 1) / kRows;
-    // first key tile any row of the workgroup sees (0 unless the layer is local); the
-    // LDS stage of tile j is (j - jf) % 2
+    // first key tile any row of the workgroup sees (0 unless the layer is local)
     const int jf = max(0, q0 - g.window + 1) / kRows;
-    auto issue = [&](int j) __attribute__((always_inline)) {
-        char *st = smem[(j - jf) & 1];
-        T::load(st, rk, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
-        T::load(st + T::BYTES, rv, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
-        TT::load(st + 2 * T::BYTES, rkt, 0, (uint32_t)len_pad * 2, j * kRows, wave, kDqWaves, lane);
+    // wave-uniform: 64-key tile j holds a key that a row of this wave sees (then the dS
+    // tile that holds it exists)
+    auto active = [&](int j) __attribute__((always_inline)) {
+        const int kb0 = j * kRows;
+        return wrow_min < g.len && kb0 <= wrow_max && wrow_min - (kb0 + kRows - 1) < g.window;
     };
-    issue(jf);
+    const int kloads = loads_per_wave(T::INSTR, wave, kDqWaves);
+    auto nloads = [&](int j) __attribute__((always_inline)) {
+        return j < nkt ? kloads + (active(j) ? 4 : 0) : 0;
+    };
+    auto issue = [&](int j) __attribute__((always_inline)) {
+        if (j >= nkt) return;
+        char *st = smem[(j - jf) % kStages];
+        T::load(st, rk, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
+        if (active(j)) {
+            const int64_t t = ds_tile_index(band, kt_lo, qt, j >> 1);
+            const rsrc_t rt = make_rsrc(ds_prob + t * (kDsTileBytes / 2), kDsTileBytes);
+            char *slab = st + T::BYTES + wave * kSlab;
+            const uint32_t off = (uint32_t)((wave & 1) * kDsKeys + (j & 1) * kRows) * 64 + lane * 16;
+#pragma unroll
+            for (int oc = 0; oc < 4; ++oc) dma_lds16_nt(rt, slab + oc * 1024, off + oc * 1024);
+        }
+    };
 
-    // This lane's query row (dims kk*16 + hi*8 .. +7 of every k-step) of Q and dO, and
-    // the row statistics: lse in log2 units and Delta = rowsum(dO * O), from the
-    // forward's O and lse.  Every query row belongs to exactly one workgroup, which
-    // also stores -Delta and -lse/scale for the dK/dV pass.
-    bf16x8 qr[KS], dor[KS];
-    float lrow = 0.f, drow = 0.f;
-    {
-        const rsrc_t ro = make_rsrc(o + b * qslice, (uint32_t)(qslice * 2));
-        const uint32_t off = row < g.len ? qbase + (uint32_t)row * qstride : kOob;
-        float dpart = 0.f;
-#pragma unroll
-        for (int kk = 0; kk < KS; ++kk) {
-            qr[kk] = __builtin_bit_cast(bf16x8, ld16(rq, off + (kk * 16 + hi * 8) * 2));
-            const u32x4 dw = ld16(rdo, off + (kk * 16 + hi * 8) * 2);
-            const u32x4 ow = ld16(ro, off + (kk * 16 + hi * 8) * 2);
-            dor[kk] = __builtin_bit_cast(bf16x8, dw);
-#pragma unroll
-            for (int w = 0; w < 4; ++w) {
-                dpart = __builtin_fmaf(bf16_lo(dw[w]), bf16_lo(ow[w]), dpart);
-                dpart = __builtin_fmaf(bf16_hi(dw[w]), bf16_hi(ow[w]), dpart);
-            }
-        }
-        drow = dpart + __shfl_xor(dpart, 32);
-        if (row < g.len) {
-            const size_t li = ((size_t)b * g.Hq + hq) * g.N + (size_t)row * g.rowmul + s;
-            const float l = lse[li];
-            lrow = l * 1.4426950408889634f;
-            if (hi == 0) {
-                nstat_d[li] = -drow;
-                nstat_l[li] = -l / g.scale;
-            }
-        }
-    }
+    // B operand dS^T (k-slots along keys, one query per lane): lane i of 16-lane group
+    // gr reads the 8-byte pieces of key rows 4*(gr>>1) + (i>>2) (+8) and queries
+    // 16*(gr&1) + 4*(i&3) .. +3, which the transposed read turns into query
+    // 16*(gr&1) + i with 4 keys, in the key order of T::tr_operand's A operand.  The
+    // 32 lanes of a half read 4 rows x 8 pieces: 32 distinct 8-byte bank slots.
+    const int sl = lane & 15, gr = lane >> 4;
+    const uint32_t dso = (uint32_t)((4 * (gr >> 1) + (sl >> 2)) * 64 + (16 * (gr & 1) + 4 * (sl & 3)) * 2);
+    uint32_t kto[DB][2];
+    T::tr_offsets(lane, kto);
 
     f32x16 adq[DB];
 #pragma unroll
     for (int db = 0; db < DB; ++db) adq[db] = f32x16{};
 
-    const float c2 = g.scale_log2;
-    const int wrow_min = q0 + wave * 32, wrow_max = wrow_min + 31;
-    wait_lds_loads();
+    issue(jf);
+    issue(jf + 1);
+    wait_vmcnt_le(nloads(jf + 1));
     lds_barrier();
-
-    // dS^T of one 32-key half as two B operands; MASK selects the diagonal variant
-    auto softmax = [&](const f32x16 &sacc, const f32x16 &pacc, int k0, bf16x8 (&dsb)[2], auto mask) {
-        constexpr bool kMask = decltype(mask)::value;
+    for (int j = jf; j < nkt; ++j) {
+        issue(j + 2);
+        if (active(j)) {
+            const char *kt = smem[(j - jf) % kStages];
+            const char *slab = kt + T::BYTES + wave * kSlab;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            uint32_t w[4];
+            for (int kk = 0; kk < kRows / 16; ++kk) {
+                const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_v4i16 *)(slab + dso + kk * 1024));
+                const v4i16 hi8 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+                    (lds_v4i16 *)(slab + dso + kk * 1024 + 512));
+                const u32x2 x = __builtin_bit_cast(u32x2, lo), y = __builtin_bit_cast(u32x2, hi8);
+                const bf16x8 bop = __builtin_bit_cast(bf16x8, u32x4{x[0], x[1], y[0], y[1]});
 #pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                float ds2[2];
-#pragma unroll
-                for (int u = 0; u < 2; ++u) {
-                    const int r = h * 8 + 2 * e + u;
-                    float p = fast_exp2(__builtin_fmaf(sacc[r], c2, -lrow));
-                    if constexpr (kMask) {  // causal and, for local layers, windowed
-                        const int key = k0 + 8 * (r >> 2) + 4 * hi + (r & 3);
-                        if (key > row || row - key >= g.window) p = 0.f;
-                    }
-                    ds2[u] = p * (pacc[r] - drow);
-                }
-                w[e] = pack_bf16(ds2[0], ds2[1]);
+                for (int db = 0; db < DB; ++db) adq[db] = mfma32(T::tr_at(kt, kto[db], kk), bop, adq[db]);
             }
-            dsb[h] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
         }
-    };
-    // One 64-key tile as two 32-key halves (S^T and dP^T, softmax, dQ^T each), which
-    // keeps registers free for operand prefetch.
-    auto tile_body = [&](const char *ktl, const char *vt, const char *ktt, int kb0, bool diag) __attribute__((always_inline)) {
-#pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            f32x16 sacc = f32x16{}, pacc = f32x16{};
-#pragma unroll
-            for (int kk = 0; kk < KS; ++kk) {
-                sacc = mfma32(T::row_operand(ktl, mb * 32 + l32, kk, hi), qr[kk], sacc);
-                pacc = mfma32(T::row_operand(vt, mb * 32 + l32, kk, hi), dor[kk], pacc);
-            }
-            bf16x8 dsb[2];
-            if (diag)
-                softmax(sacc, pacc, kb0 + mb * 32, dsb, std::true_type{});
-            else
-                softmax(sacc, pacc, kb0 + mb * 32, dsb, std::false_type{});
-#pragma unroll
-            for (int db = 0; db < DB; ++db)
-#pragma unroll
-                for (int h = 0; h < 2; ++h)
-                    adq[db] = mfma32(TT::operand(ktt, db * 32 + l32, mb * 2 + h, hi), dsb[h], adq[db]);
-        }
-    };
-    auto step = [&](int j, auto stage) __attribute__((always_inline)) {
-        constexpr int kSt = decltype(stage)::value;
-        if (j + 1 < nkt) issue(j + 1);
-        const int kb0 = j * kRows;
-        // wave-uniform: the tile holds a key that some row of this wave sees
-        if (kb0 <= wrow_max && wrow_min - (kb0 + kRows - 1) < g.window) {
-            const char *ktl = smem[kSt];
-            const char *vt = ktl + T::BYTES;
-            const char *ktt = ktl + 2 * T::BYTES;
-            // mask on the diagonal tile and on tiles reaching a window before a row
-            tile_body(ktl, vt, ktt, kb0, kb0 + kRows - 1 > wrow_min || wrow_max - kb0 >= g.window);
-        }
-        wait_lds_loads();
+        // tile j + 1 has landed once at most the loads of tile j + 2 are outstanding
+        wait_vmcnt_le(nloads(j + 2));
         lds_barrier();
-    };
-    for (int j = jf; j < nkt; j += 2) {
-        step(j, std::integral_constant<int, 0>{});
-        if (j + 1 < nkt) step(j + 1, std::integral_constant<int, 1>{});
     }
 
     if (row < g.len) {
@@ -470,27 +454,29 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
 
 template <int D>
 hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o,
-                      const float *lse, const bf16 *dO, float *delta, float *lse2, bf16 *kt,
-                      int len_pad, bf16 *dq, bf16 *dk, bf16 *dv, const SfaGeom &g, hipStream_t s,
-                      const char *tr_name, const char *dq_name, const char *dkdv_name)
+                      const float *lse, const bf16 *dO, float *delta, float *lse2, bf16 *ds,
+                      int64_t ds_tiles, bf16 *dq, bf16 *dk, bf16 *dv, const SfaGeom &g,
+                      hipStream_t s, const char *st_name, const char *dq_name,
+                      const char *dkdv_name)
 {
-    timing_before(tr_name, s);
-    transpose_k_kernel<D><<<g.B * g.Hkv * g.streams * (len_pad / kRows), 256, 0, s>>>(k, kt, g,
-                                                                                     len_pad);
+    const int64_t rows = (int64_t)g.B * g.N * g.Hq;
+    timing_before(st_name, s);
+    bwd_stats_bf16_kernel<D><<<(unsigned)((rows * (D / 8) + 255) / 256), 256, 0, s>>>(
+        o, dO, lse, delta, lse2, g);
     hipError_t e = hipGetLastError();
-    timing_after(s);
-    if (e != hipSuccess) return e;
-    const int nqt = (g.len + kRowsPerWg - 1) / kRowsPerWg;
-    timing_before(dq_name, s);
-    sfa_dq_bf16_kernel<D><<<nqt * g.B * g.Hq * g.streams, kDqWaves * 64, 0, s>>>(
-        q, k, v, o, lse, dO, delta, lse2, kt, dq, g, len_pad);
-    e = hipGetLastError();
     timing_after(s);
     if (e != hipSuccess) return e;
     const int nkt = (g.len + kKeysPerWg - 1) / kKeysPerWg;
     timing_before(dkdv_name, s);
-    sfa_dkdv_bf16_kernel<D><<<nkt * g.B * g.Hkv * g.streams, kDkdvWaves * 64, 0, s>>>(q, k, v, dO, delta,
-                                                                           lse2, dk, dv, g);
+    sfa_dkdv_bf16_kernel<D><<<nkt * g.B * g.Hkv * g.streams, kDkdvWaves * 64, 0, s>>>(
+        q, k, v, dO, delta, lse2, dk, dv, ds, ds_tiles, g);
+    e = hipGetLastError();
+    timing_after(s);
+    if (e != hipSuccess) return e;
+    const int nqt = (g.len + kRowsPerWg - 1) / kRowsPerWg;
+    timing_before(dq_name, s);
+    sfa_dq_bf16_kernel<D><<<nqt * g.B * g.Hq * g.streams, kDqWaves * 64, 0, s>>>(k, ds, dq, g,
+                                                                                 ds_tiles);
     e = hipGetLastError();
     timing_after(s);
     return e;
@@ -506,19 +492,19 @@ hipError_t launch_bwd_bf16(const void *q, const void *k, const void *v, const vo
     char *wsb = static_cast<char *>(ws);
     float *delta = reinterpret_cast<float *>(wsb + w.delta);
     float *lse2 = reinterpret_cast<float *>(wsb + w.lse2);
-    bf16 *kt = reinterpret_cast<bf16 *>(wsb + w.kt);
+    bf16 *ds = reinterpret_cast<bf16 *>(wsb + w.ds);
     const bf16 *qq = static_cast<const bf16 *>(q), *kk = static_cast<const bf16 *>(k),
                *vv = static_cast<const bf16 *>(v), *dd = static_cast<const bf16 *>(dO),
                *oo = static_cast<const bf16 *>(o);
     bf16 *gq = static_cast<bf16 *>(dq), *gk = static_cast<bf16 *>(dk), *gv = static_cast<bf16 *>(dv);
     if (g.D == 32)
-        return bwd_bf16_d<32>(qq, kk, vv, oo, lse, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
-                              "sfa_bwd_transpose_d32", "sfa_dq_bf16_d32", "sfa_dkdv_bf16_d32");
+        return bwd_bf16_d<32>(qq, kk, vv, oo, lse, dd, delta, lse2, ds, w.ds_tiles, gq, gk, gv, g,
+                              s, "sfa_bwd_stats_d32", "sfa_dq_bf16_d32", "sfa_dkdv_bf16_d32");
     if (g.D == 64)
-        return bwd_bf16_d<64>(qq, kk, vv, oo, lse, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
-                              "sfa_bwd_transpose_d64", "sfa_dq_bf16_d64", "sfa_dkdv_bf16_d64");
-    return bwd_bf16_d<128>(qq, kk, vv, oo, lse, dd, delta, lse2, kt, w.len_pad, gq, gk, gv, g, s,
-                           "sfa_bwd_transpose_d128", "sfa_dq_bf16_d128", "sfa_dkdv_bf16_d128");
+        return bwd_bf16_d<64>(qq, kk, vv, oo, lse, dd, delta, lse2, ds, w.ds_tiles, gq, gk, gv, g,
+                              s, "sfa_bwd_stats_d64", "sfa_dq_bf16_d64", "sfa_dkdv_bf16_d64");
+    return bwd_bf16_d<128>(qq, kk, vv, oo, lse, dd, delta, lse2, ds, w.ds_tiles, gq, gk, gv, g, s,
+                           "sfa_bwd_stats_d128", "sfa_dq_bf16_d128", "sfa_dkdv_bf16_d128");
 }
 
 }  // namespace hd

@@ -43,6 +43,13 @@ __device__ inline void dma_lds16(rsrc_t rs, const char *lds, uint32_t voff)
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
                  :: "s"(m0), "v"(voff), "s"(rs) : "memory", "m0");
 }
+// Same with the non-temporal cache policy, for data read exactly once.
+__device__ inline void dma_lds16_nt(rsrc_t rs, const char *lds, uint32_t voff)
+{
+    const uint32_t m0 = (uint32_t)(uintptr_t)(lds_void *)lds;
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tbuffer_load_dwordx4 %1, %2, 0 offen nt lds"
+                 :: "s"(m0), "v"(voff), "s"(rs) : "memory", "m0");
+}
 __device__ inline void dma_lds4(rsrc_t rs, const char *lds, uint32_t voff)
 {
     const uint32_t m0 = (uint32_t)(uintptr_t)(lds_void *)lds;

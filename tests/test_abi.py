@@ -104,6 +104,23 @@ def bwd(lib, ws_bytes=None, ws=FAKE * 16, **kw):
                           None), need
 
 
+def _ds_tiles(len_, window=None):
+    """dS tiles (64 query rows x 128 keys, 16 KB) stored per causal problem: those that
+    hold a visible pair, counted by brute force over the tiles' pairs."""
+    nqt, nkt = -(-len_ // 64), -(-len_ // 128)
+    w = window if window is not None else len_
+    count = 0
+    for qt in range(nqt):
+        rows = range(qt * 64, min(len_, qt * 64 + 64))
+        per_row = 0
+        for kt in range(nkt):
+            k_lo, k_hi = kt * 128, min(len_, kt * 128 + 128) - 1
+            if any(k_lo <= r and r - k_hi < w for r in rows):
+                per_row += 1
+        count += per_row
+    return count
+
+
 def test_workspace_size_formula(lib):
     a256 = lambda x: math.ceil(x / 256) * 256
     B, L, n, Hq, Hkv, D = 2, 100, 3, 4, 2, 64
@@ -111,17 +128,35 @@ def test_workspace_size_formula(lib):
     stats = 2 * a256(rows * 4)  # delta and lse2, fp32 per query row
     # fp32: statistics only
     assert lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, 0, 1) == stats
-    # bf16 adds a transposed k per key/value problem, [D][len rounded up to 64] bf16
+    # bf16 adds the dS tiles of every problem: exactly the tiles holding a visible pair
+    # for causal layers (intra: one problem per stream)
     for mode, len_, streams in ((0, L, n), (1, n * L, 1)):
-        lp = math.ceil(len_ / 64) * 64
-        kt = a256(B * Hkv * streams * D * lp * 2)
-        assert lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 0) == stats + kt
-    for dtype in (0, 1):  # a local layer decomposes like the full cross-stream layer
+        ds = B * Hq * streams * _ds_tiles(len_) * 16384
+        assert lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 0) == stats + ds
+    for dtype in (0, 1):  # without a window a local layer gets the full causal size
         assert (lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, 2, dtype)
                 == lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, 1, dtype))
     assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 2, 64, 3, 0) == 0  # mode
     assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 3, 64, 0, 0) == 0  # Hq % Hkv
     assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 2, 48, 0, 0) == 0  # D
+
+
+@pytest.mark.parametrize("L,n,window", [(100, 3, 1), (100, 3, 64), (100, 3, 129), (100, 3, 299),
+                                        (100, 3, 300), (100, 3, 10 ** 6), (700, 4, 200),
+                                        (700, 4, 1000), (2048, 2, 4096)])
+def test_local_workspace_size(lib, L, n, window):
+    B, Hq, Hkv, D = 1, 2, 1, 32
+    full = lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, 1, 0)
+    got = lib.hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, window, 0)
+    # never more than the window-free size, and never less than the tiles holding a
+    # visible pair of this window
+    stats = lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, 1, 1)
+    assert stats + B * Hq * _ds_tiles(n * L, window) * 16384 <= got <= full
+    if window >= n * L:
+        assert got == full
+    assert lib.hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, 0, 0) == 0
+    assert (lib.hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, window, 1)
+            == stats)
 
 
 @pytest.mark.parametrize("kw,code", [
