@@ -56,6 +56,13 @@ def _load():
         f.restype = None
     lib.oracle_expand_embed.argtypes = [vp, vp, vp, i64, i64, i64, i64, i64, i64]
     lib.oracle_expand_embed.restype = i64
+    lib.oracle_expand_embed_bwd.argtypes = [vp, vp, i32, vp, i64, i64, i64, i64, i64]
+    lib.oracle_expand_embed_bwd.restype = None
+    lib.oracle_expand_embed_bwd_rows.argtypes = [vp, vp, i32, vp, i64, vp, i64, i64, i64, i64,
+                                                 i64]
+    lib.oracle_expand_embed_bwd_rows.restype = None
+    lib.oracle_cyclic_replicate.argtypes = [vp, vp, i64, i64, i64, i64, i64]
+    lib.oracle_cyclic_replicate.restype = None
     lib.oracle_sfa_mask.argtypes = [vp, i64, i64, i32, i64]
     lib.oracle_sfa_mask.restype = None
     _lib = lib
@@ -175,6 +182,47 @@ def expand_embed(ids, tables):
     bad = _load().oracle_expand_embed(_ptr(ids), _ptr(tables), _ptr(out), B, L, n, V, Dm,
                                       tables.dtype.itemsize)
     return out, int(bad)
+
+
+def expand_embed_bwd(ids, dout, V):
+    """Gradient of eq. (expansion) w.r.t. the tables: ids [B][L] int32, dout [B][n*L][Dm]
+    (fp64, fp32 or bf16 bits) -> dense fp64 [n][V][Dm]."""
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    dout = np.ascontiguousarray(dout)
+    B, L = ids.shape
+    N, Dm = dout.shape[1], dout.shape[2]
+    if dout.shape[0] != B or N % L:
+        raise ValueError("dout must be [B][n*L][Dm]")
+    n = N // L
+    out = np.empty((n, V, Dm))
+    _load().oracle_expand_embed_bwd(_ptr(ids), _ptr(dout), _dtype_code(dout), _ptr(out), B, L,
+                                    n, V, Dm)
+    return out
+
+
+def expand_embed_bwd_rows(ids, dout, V, req):
+    """The same gradient for the token ids listed in ``req`` only -> fp64 [len(req)][n][Dm]."""
+    ids = np.ascontiguousarray(ids, dtype=np.int32)
+    dout = np.ascontiguousarray(dout)
+    req = np.ascontiguousarray(req, dtype=np.int32).reshape(-1)
+    B, L = ids.shape
+    N, Dm = dout.shape[1], dout.shape[2]
+    n = N // L
+    out = np.empty((len(req), n, Dm))
+    _load().oracle_expand_embed_bwd_rows(_ptr(ids), _ptr(dout), _dtype_code(dout), _ptr(req),
+                                         len(req), _ptr(out), B, L, n, V, Dm)
+    return out
+
+
+def cyclic_replicate(tables, m):
+    """eq. (cyclic_init): tables [n][V][Dm] -> [m][V][Dm] with table s = tables[s mod n]."""
+    tables = np.ascontiguousarray(tables)
+    n, V, Dm = tables.shape
+    if m < n or m % n:
+        raise ValueError("m must be a positive multiple of n")
+    out = np.empty((m, V, Dm), dtype=tables.dtype)
+    _load().oracle_cyclic_replicate(_ptr(tables), _ptr(out), n, m, V, Dm, tables.dtype.itemsize)
+    return out
 
 
 def sfa_mask(L, n, mode, window=0):

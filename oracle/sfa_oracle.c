@@ -10,6 +10,10 @@
  * What it computes (paper: "Hidden Decoding at Scale", Sec. 2 "Method"):
  *   - multi-stream token expansion, eq. (expansion): expanded position of stream k
  *     of token i holds E_k(x_i); 0-based here: row p = t*n + s holds tables[s][ids[t]];
+ *     and its gradient with respect to the tables (the adjoint of that gather: a sum of
+ *     upstream rows per token id and stream);
+ *   - cyclic replication of the tables when the expansion factor grows,
+ *     eq. (cyclic_init): E_{n+k} <- E_k;
  *   - token/stream index maps, eq. (indices), 0-based: t(p) = p / n, s(p) = p % n;
  *   - intra-stream attention mask, eq. (mask_intra): key p' visible from query p
  *     iff s(p') == s(p) and p' <= p (equivalently t(p') <= t(p));
@@ -418,6 +422,67 @@ int64_t oracle_expand_embed(const int32_t *ids, const void *tables, void *out, i
                 memcpy(dst, src, (size_t)row_bytes);
             }
     return bad;
+}
+
+/*
+ * Gradient of eq. (expansion) with respect to the n tables.  The expansion is a
+ * gather, out[b][t*n + s] = tables[s][ids[b][t]], so for any upstream gradient dout
+ *   dtables[s][x][:] = sum over tokens (b, t) with ids[b][t] == x of dout[b][t*n + s][:],
+ * and tokens whose id lies outside [0, V) contribute nothing (their expanded rows are
+ * constant zeros).  Dense fp64 [n][V][Dm] output, overwritten; tokens are visited in
+ * (b, t) order.
+ */
+void oracle_expand_embed_bwd(const int32_t *ids, const void *dout, int dtype, double *dtables,
+                             int64_t B, int64_t L, int64_t n, int64_t V, int64_t Dm)
+{
+    memset(dtables, 0, (size_t)(n * V * Dm) * sizeof(double));
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t t = 0; t < L; ++t) {
+            const int64_t id = ids[b * L + t];
+            if (id < 0 || id >= V) continue;
+            for (int64_t s = 0; s < n; ++s) {
+                const int64_t row = b * n * L + t * n + s;
+                double *dst = dtables + (s * V + id) * Dm;
+                for (int64_t d = 0; d < Dm; ++d) dst[d] += load_elem(dout, dtype, row * Dm + d);
+            }
+        }
+}
+
+/*
+ * The same gradient for a list of token ids only: drows[r][s][:] = dtables[s][req[r]][:]
+ * above, each formed by scanning every token of the batch (for large vocabularies).
+ */
+void oracle_expand_embed_bwd_rows(const int32_t *ids, const void *dout, int dtype,
+                                  const int32_t *req, int64_t nreq, double *drows, int64_t B,
+                                  int64_t L, int64_t n, int64_t V, int64_t Dm)
+{
+    memset(drows, 0, (size_t)(nreq * n * Dm) * sizeof(double));
+    for (int64_t r = 0; r < nreq; ++r) {
+        const int64_t x = req[r];
+        if (x < 0 || x >= V) continue;
+        for (int64_t b = 0; b < B; ++b)
+            for (int64_t t = 0; t < L; ++t) {
+                if (ids[b * L + t] != x) continue;
+                for (int64_t s = 0; s < n; ++s) {
+                    const int64_t row = b * n * L + t * n + s;
+                    double *dst = drows + (r * n + s) * Dm;
+                    for (int64_t d = 0; d < Dm; ++d) dst[d] += load_elem(dout, dtype, row * Dm + d);
+                }
+            }
+    }
+}
+
+/*
+ * eq. (cyclic_init), 0-based: growing the expansion factor from n to m (a multiple of
+ * n), the m tables are dst[s] = src[s mod n]; for m = 2n this is E_{n+k} <- E_k.
+ * Element-size agnostic byte copy; src [n][V][Dm], dst [m][V][Dm].
+ */
+void oracle_cyclic_replicate(const void *src, void *dst, int64_t n, int64_t m, int64_t V,
+                             int64_t Dm, int64_t elem_bytes)
+{
+    const size_t table = (size_t)(V * Dm * elem_bytes);
+    for (int64_t s = 0; s < m; ++s)
+        memcpy((char *)dst + s * table, (const char *)src + (s % n) * table, table);
 }
 
 /* Mask as bytes [N][N] straight from the definition (for probes and pins). */

@@ -482,3 +482,120 @@ def test_local_row_sampled_entry_points_match_full(oracle_mod):
     for i, (b, h, j) in enumerate(krows):
         np.testing.assert_allclose(rdk[i], dk[b, j, h], atol=1e-14)
         np.testing.assert_allclose(rdv[i], dv[b, j, h], atol=1e-14)
+
+
+# ------------------------------------------------- expansion backward, cyclic init
+
+
+def _interleave_embedding(ids, tables):
+    """Library form of eq. (expansion): torch embedding lookups of the n tables,
+    stacked on a new stream axis and flattened token-major ([B][L][n] -> [B][n*L])."""
+    rows = torch.stack([F.embedding(ids, tables[s]) for s in range(tables.shape[0])], dim=2)
+    B, L, n, Dm = rows.shape
+    return rows.reshape(B, L * n, Dm)
+
+
+def test_expand_bwd_matches_hand_worked_golden(oracle_mod):
+    g = json.load(open(os.path.join(GOLDEN, "expand_bwd_n2.json")))
+    ids = np.array([g["ids"]], dtype=np.int32)
+    dout = np.array([g["dout"]], dtype=np.float64)
+    d = oracle_mod.expand_embed_bwd(ids, dout, g["V"])
+    np.testing.assert_array_equal(d[0], np.array(g["expected_dE1"], dtype=np.float64))
+    np.testing.assert_array_equal(d[1], np.array(g["expected_dE2"], dtype=np.float64))
+
+
+@pytest.mark.parametrize("B,L,n,V,Dm", [(1, 40, 2, 7, 5), (3, 17, 4, 50, 8), (2, 9, 1, 3, 4)])
+def test_expand_bwd_equals_library_autograd(oracle_mod, B, L, n, V, Dm):
+    """The gradient through torch's embedding lookups (autograd, fp64) of the interleaved
+    expansion equals the oracle's scatter-add, duplicates included."""
+    r = np.random.default_rng(B * 100 + L)
+    ids = r.integers(0, V, size=(B, L)).astype(np.int32)  # V small: many repeats
+    tables = torch.tensor(r.standard_normal((n, V, Dm)), requires_grad=True)
+    dout = r.standard_normal((B, n * L, Dm))
+    out = _interleave_embedding(torch.tensor(ids, dtype=torch.int64), tables)
+    out.backward(torch.tensor(dout))
+    np.testing.assert_allclose(oracle_mod.expand_embed_bwd(ids, dout, V), tables.grad.numpy(),
+                               rtol=1e-13, atol=1e-13)
+
+
+def test_expand_bwd_is_adjoint_of_forward(oracle_mod):
+    """<expand(E), G> == <E, expand_bwd(G)> for random E, G, with repeated and
+    out-of-range ids (the oracle's forward copies bytes, so fp64 tables go through it
+    exactly)."""
+    r = np.random.default_rng(7)
+    B, L, n, V, Dm = 2, 33, 3, 11, 6
+    ids = r.integers(-2, V + 2, size=(B, L)).astype(np.int32)
+    E = r.standard_normal((n, V, Dm))
+    G = r.standard_normal((B, n * L, Dm))
+    fwd, bad = oracle_mod.expand_embed(ids, E)
+    assert bad == int(np.sum((ids < 0) | (ids >= V)))
+    lhs = float(np.sum(fwd * G))
+    rhs = float(np.sum(E * oracle_mod.expand_embed_bwd(ids, G, V)))
+    assert abs(lhs - rhs) <= 1e-12 * np.sum(np.abs(fwd * G))
+
+
+def test_expand_bwd_distinct_ids_is_a_permutation(oracle_mod):
+    """All ids distinct: each upstream row lands, unchanged, in one table row."""
+    r = np.random.default_rng(8)
+    L, n, V, Dm = 20, 4, 64, 8
+    ids = r.permutation(V)[:L].astype(np.int32).reshape(1, L)
+    dout = synth.to_bf16_bits(r.standard_normal((1, n * L, Dm)))
+    d = oracle_mod.expand_embed_bwd(ids, dout, V)
+    rows = synth.bf16_bits_to_f32(dout).astype(np.float64)
+    for t in range(L):
+        for s in range(n):
+            np.testing.assert_array_equal(d[s, ids[0, t]], rows[0, t * n + s])
+    untouched = np.setdiff1d(np.arange(V), ids[0])
+    assert np.all(d[:, untouched] == 0)
+
+
+def test_expand_bwd_one_repeated_id_sums_each_stream(oracle_mod):
+    """Every token has the same id x: table s at x holds the sum of the stream-s rows."""
+    r = np.random.default_rng(9)
+    B, L, n, V, Dm = 2, 30, 3, 5, 4
+    ids = np.full((B, L), 3, dtype=np.int32)
+    dout = r.standard_normal((B, n * L, Dm))
+    d = oracle_mod.expand_embed_bwd(ids, dout, V)
+    for s in range(n):
+        np.testing.assert_allclose(d[s, 3], dout[:, s::n].sum(axis=(0, 1)), rtol=1e-13)
+    assert np.all(d[:, [0, 1, 2, 4]] == 0)
+
+
+def test_expand_bwd_rows_equal_dense(oracle_mod):
+    r = np.random.default_rng(10)
+    B, L, n, V, Dm = 2, 25, 2, 9, 3
+    ids = r.integers(-1, V + 1, size=(B, L)).astype(np.int32)
+    dout = r.standard_normal((B, n * L, Dm))
+    dense = oracle_mod.expand_embed_bwd(ids, dout, V)
+    req = np.array([0, 8, 4, -1, V, 4], dtype=np.int32)
+    rows = oracle_mod.expand_embed_bwd_rows(ids, dout, V, req)
+    for i, x in enumerate(req):
+        want = dense[:, x] if 0 <= x < V else np.zeros((n, Dm))
+        np.testing.assert_array_equal(rows[i], want)
+
+
+def test_cyclic_replicate_matches_paper_examples(oracle_mod):
+    g = json.load(open(os.path.join(GOLDEN, "expand_bwd_n2.json")))
+    V, Dm = 3, 2
+    for n, m, want in ((2, 4, g["cyclic_n2_to_4"]), (4, 8, g["cyclic_n4_to_8"])):
+        tables = np.stack([np.full((V, Dm), s + 1, dtype=np.uint16) for s in range(n)])
+        out = oracle_mod.cyclic_replicate(tables, m)
+        assert [int(out[s, 0, 0]) for s in range(m)] == want
+        np.testing.assert_array_equal(out[:n], tables)
+
+
+def test_cyclic_replicate_reproduces_the_smaller_model_rows(oracle_mod):
+    """After E_{n+k} <- E_k the expanded rows of stream s and s + n coincide, and the
+    first n streams of every token are the n-stream expansion (the expanded model
+    starts from the smaller one's inputs)."""
+    r = np.random.default_rng(11)
+    n, V, Dm, L = 2, 10, 4, 6
+    tables = synth.to_bf16_bits(r.standard_normal((n, V, Dm)))
+    ids = r.integers(0, V, size=(1, L)).astype(np.int32)
+    big = oracle_mod.cyclic_replicate(tables, 2 * n)
+    out2, _ = oracle_mod.expand_embed(ids, tables)
+    out4, _ = oracle_mod.expand_embed(ids, big)
+    for t in range(L):
+        for s in range(n):
+            np.testing.assert_array_equal(out4[0, t * 2 * n + s], out4[0, t * 2 * n + s + n])
+            np.testing.assert_array_equal(out4[0, t * 2 * n + s], out2[0, t * n + s])
