@@ -6,6 +6,7 @@ expanded rows, Hq=32, Hkv=8, D=128, bf16):
   * the stream expansion of 4096 token ids through n=4 tables of 151936 x 4096,
   * the forward of 36 attention layers (mixing layers at 8, 17, 26, 35, intra-stream
     layers elsewhere), then their backward in reverse order,
+  * the expansion's backward (sparse gradient of the n tables),
 each layer on its own seeded q/k/v/dO, all resident in HBM before timing starts.
 
 Prints one JSON line.  value = useful TFLOP/s of the whole step (useful flop counts
@@ -70,6 +71,8 @@ def per_kernel_flops(shape, mode, window):
 
 
 def kernel_family(name):
+    if name.startswith("embed_bwd"):
+        return "expand_bwd"
     for fam in ("fwd", "dkdv", "dq", "preprocess", "expand"):
         if fam in name:
             return fam
@@ -111,7 +114,8 @@ def main():
         with_embed = True
         wl_desc = (f"stack36: expand_embed (n=4 tables of {W.STACK_VOCAB}x{W.STACK_DMODEL}) + "
                    f"fwd of 36 layers (mix at {list(W.STACK_MIX_LAYERS)}, intra elsewhere) + "
-                   "bwd in reverse, each layer B=1 L=4096 n=4 Hq=32 Hkv=8 D=128")
+                   "bwd in reverse, each layer B=1 L=4096 n=4 Hq=32 Hkv=8 D=128, + "
+                   "expand_embed backward")
         std = W.QWEN8B.qkv_std
         spike = None
     else:
@@ -164,6 +168,14 @@ def main():
         tables = synth.device_normal((s.n, W.STACK_VOCAB, W.STACK_DMODEL), W.STACK_EMBED_STD,
                                      12, dev, torch.bfloat16)
         emb = torch.empty((1, s.N, W.STACK_DMODEL), dtype=torch.bfloat16, device=dev)
+        # the expansion's backward: upstream gradient of the expanded rows -> sparse
+        # table gradient (distinct ids, rows)
+        demb = synth.device_normal((1, s.N, W.STACK_DMODEL), 1.0, 13, dev, torch.bfloat16)
+        uniq = torch.empty(s.L, dtype=torch.int32, device=dev)
+        drows = torch.empty((s.n, s.L, W.STACK_DMODEL), dtype=torch.float32, device=dev)
+        nuniq = torch.empty(1, dtype=torch.int32, device=dev)
+        ews_bytes = hd.hd_expand_embed_bwd_workspace_bytes(1, s.L)
+        ews = torch.empty(ews_bytes, dtype=torch.uint8, device=dev)
     torch.cuda.synchronize()
     t_gen = time.time() - t_gen
 
@@ -187,6 +199,9 @@ def main():
                 hd.hd_sfa_bwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq, dk,
                               dv, s.B, s.L, s.n, s.Hq, s.Hkv, s.D, ly["mode"], scale, ws,
                               ws_bytes, stream=stream)
+        if with_embed:
+            hd.hd_expand_embed_bwd(ids, demb, 1, s.L, s.n, W.STACK_VOCAB, W.STACK_DMODEL, uniq,
+                                   drows, nuniq, ews, ews_bytes, stream=stream)
 
     for _ in range(args.warmup):
         step()
@@ -243,6 +258,10 @@ def main():
             ent["tflops"] = round(fam_flops[fam] / (ms / args.steps * 1e-3) / 1e12, 2)
         if fam == "expand":
             nbytes = W.embed_bytes(1, s.L, s.n, W.STACK_DMODEL)
+            ent["gbs"] = round(nbytes / (ms / args.steps * 1e-3) / 1e9, 1)
+            ent["bytes_per_launch"] = nbytes
+        if fam == "expand_bwd":
+            nbytes = W.embed_bwd_bytes(1, s.L, s.n, W.STACK_DMODEL, int(nuniq.cpu()[0]))
             ent["gbs"] = round(nbytes / (ms / args.steps * 1e-3) / 1e9, 1)
             ent["bytes_per_launch"] = nbytes
         breakdown[fam] = ent

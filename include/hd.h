@@ -75,6 +75,65 @@ hd_status_t hd_expand_embed(const int32_t *ids, const void *tables, void *out, i
                             int32_t *bad_id_count, hd_stream_t stream);
 
 /*
+ * hd_expand_embed_bwd -- gradient of eq. (expansion) with respect to the n tables.
+ * The expansion is a gather, so for an upstream gradient dout of its output
+ *   dtables[s][x][:] = sum over tokens (b, t) with ids[b][t] == x of dout[b][t*n + s][:]
+ * (tokens whose id lies outside [0, V) contribute nothing).  The result is returned
+ * sparse, for the distinct in-range ids of the batch only:
+ *
+ * ids        device int32 [B][L], the ids the forward expanded.
+ * dout       device [B][n*L][Dm] of `dtype` (bf16 or f32).
+ * uniq_ids   device int32 [B*L]: entries 0 .. *num_uniq-1 receive the distinct ids in
+ *            ascending order; later entries are not written.
+ * drows      device float [n][B*L][Dm]: drows[s][u][:] = dtables[s][uniq_ids[u]][:] for
+ *            u < *num_uniq, summed in fp32 over the id's tokens in ascending (b, t)
+ *            order (deterministic: no atomics); rows u >= *num_uniq are not written.
+ * num_uniq   device int32, receives the number of distinct in-range ids.
+ * workspace  device, 256-byte aligned, at least hd_expand_embed_bwd_workspace_bytes(B, L)
+ *            bytes; contents on entry ignored, on exit unspecified.
+ * Errors: INVALID_ARG for null pointers, sizes <= 0, V > INT32_MAX, B*L > 4194304,
+ *         misaligned pointers (dout, drows 16 bytes; ids, uniq_ids, num_uniq 4 bytes) or
+ *         a missing or short workspace.
+ */
+size_t hd_expand_embed_bwd_workspace_bytes(int B, int L);
+hd_status_t hd_expand_embed_bwd(const int32_t *ids, const void *dout, int B, int L, int n,
+                                int64_t V, int Dm, hd_dtype_t dtype, int32_t *uniq_ids,
+                                float *drows, int32_t *num_uniq, void *workspace,
+                                size_t workspace_bytes, hd_stream_t stream);
+
+/*
+ * hd_embed_grad_scatter_add -- adds the sparse table gradient of hd_expand_embed_bwd
+ * into a dense one:  dtables[s][uniq_ids[u]][:] += drows[s][u][:]  for u < *num_uniq.
+ * This entry point ACCUMULATES into dtables (the exception to the overwrite rule):
+ * gradients of several batches add up before an optimizer step.  The ids are distinct,
+ * so every destination row has one writer and the result is deterministic.
+ *
+ * uniq_ids, drows, num_uniq  as written by hd_expand_embed_bwd; max_rows is the row
+ *            capacity B*L that drows was laid out with ([n][max_rows][Dm]).
+ * dtables    device float [n][V][Dm].
+ * Errors: INVALID_ARG for null pointers, sizes <= 0, V > INT32_MAX or pointers that are
+ *         not 4-byte aligned.
+ */
+hd_status_t hd_embed_grad_scatter_add(const int32_t *uniq_ids, const float *drows,
+                                      const int32_t *num_uniq, int max_rows, int n, int64_t V,
+                                      int Dm, float *dtables, hd_stream_t stream);
+
+/*
+ * hd_cyclic_replicate -- Cyclic Replication Initialization, eq. (cyclic_init) (Sec.
+ * "Progressive Expansion"): growing the expansion factor from n to m, a multiple of n,
+ * the m tables become dst[s] = src[s mod n] (for m = 2n: E_{n+k} <- E_k; n = 2 -> 4
+ * gives (E1, E2, E1, E2)).
+ *
+ * src  device [n][V][Dm] of `dtype`;  dst  device [m][V][Dm] of `dtype`, overwritten.
+ * dst may be the same buffer as src (growth in place: src then has room for m tables
+ * and only tables n .. m-1 are written); any other overlap is rejected.
+ * Errors: INVALID_ARG for null or unaligned (16-byte) pointers, n <= 0, m not a
+ *         multiple of n or above 65535, V or Dm <= 0, or overlapping buffers.
+ */
+hd_status_t hd_cyclic_replicate(const void *src, void *dst, int n, int m, int64_t V, int Dm,
+                                hd_dtype_t dtype, hd_stream_t stream);
+
+/*
  * hd_sfa_fwd -- Stream-Factorized Attention forward over the expanded sequence.
  *   O_p = sum_{p' visible from p} softmax_p'(scale * q_p . k_p') v_p'
  *   lse_p = log sum_{p' visible} exp(scale * q_p . k_p')       (natural log)

@@ -18,7 +18,8 @@ HD_SFA_INTRA, HD_SFA_MIX, HD_SFA_LOCAL = 0, 1, 2
 HD_DTYPE_BF16, HD_DTYPE_F32 = 0, 1
 
 # every symbol include/hd.h declares
-EXPORTS = ("hd_expand_embed", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
+EXPORTS = ("hd_expand_embed", "hd_expand_embed_bwd_workspace_bytes", "hd_expand_embed_bwd",
+           "hd_embed_grad_scatter_add", "hd_cyclic_replicate", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
            "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
            "hd_timing_enable", "hd_timing_collect")
 
@@ -61,7 +62,13 @@ def lib() -> ctypes.CDLL:
     # the *_local variants take the window where the others take the mode
     L.hd_sfa_fwd_local.argtypes = L.hd_sfa_fwd.argtypes
     L.hd_sfa_bwd_local.argtypes = L.hd_sfa_bwd.argtypes
-    for f in (L.hd_expand_embed, L.hd_sfa_fwd, L.hd_sfa_fwd_local, L.hd_sfa_bwd,
+    L.hd_expand_embed_bwd_workspace_bytes.argtypes = [i32, i32]
+    L.hd_expand_embed_bwd_workspace_bytes.restype = sz
+    L.hd_expand_embed_bwd.argtypes = [vp, vp, i32, i32, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp]
+    L.hd_embed_grad_scatter_add.argtypes = [vp, vp, vp, i32, i32, i64, i32, vp, vp]
+    L.hd_cyclic_replicate.argtypes = [vp, vp, i32, i32, i64, i32, i32, vp]
+    for f in (L.hd_expand_embed, L.hd_expand_embed_bwd, L.hd_embed_grad_scatter_add,
+              L.hd_cyclic_replicate, L.hd_sfa_fwd, L.hd_sfa_fwd_local, L.hd_sfa_bwd,
               L.hd_sfa_bwd_local, L.hd_timing_enable):
         f.restype = i32
     L.hd_status_str.argtypes = [i32]
@@ -117,6 +124,29 @@ def hd_expand_embed(ids, tables, out, B, L, n, V, Dm, dtype=None, bad_id_count=N
     _check(lib().hd_expand_embed(_ptr(ids), _ptr(tables), _ptr(out), B, L, n, V, Dm,
                                  _dtype_code(tables, dtype), _ptr(bad_id_count),
                                  _stream(stream)))
+
+
+def hd_expand_embed_bwd_workspace_bytes(B, L) -> int:
+    return int(lib().hd_expand_embed_bwd_workspace_bytes(B, L))
+
+
+def hd_expand_embed_bwd(ids, dout, B, L, n, V, Dm, uniq_ids, drows, num_uniq, workspace,
+                        workspace_bytes, dtype=None, stream=None):
+    _check(lib().hd_expand_embed_bwd(_ptr(ids), _ptr(dout), B, L, n, V, Dm,
+                                     _dtype_code(dout, dtype), _ptr(uniq_ids), _ptr(drows),
+                                     _ptr(num_uniq), _ptr(workspace), workspace_bytes,
+                                     _stream(stream)))
+
+
+def hd_embed_grad_scatter_add(uniq_ids, drows, num_uniq, max_rows, n, V, Dm, dtables,
+                              stream=None):
+    _check(lib().hd_embed_grad_scatter_add(_ptr(uniq_ids), _ptr(drows), _ptr(num_uniq), max_rows,
+                                           n, V, Dm, _ptr(dtables), _stream(stream)))
+
+
+def hd_cyclic_replicate(src, dst, n, m, V, Dm, dtype=None, stream=None):
+    _check(lib().hd_cyclic_replicate(_ptr(src), _ptr(dst), n, m, V, Dm, _dtype_code(src, dtype),
+                                     _stream(stream)))
 
 
 def hd_sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, mode, scale, dtype=None, stream=None):
@@ -238,4 +268,35 @@ def expand_embed(ids, tables, *, bad_id_count=None, stream=None):
     n, V, Dm = tables.shape
     out = torch.empty((B, n * L, Dm), dtype=tables.dtype, device=tables.device)
     hd_expand_embed(ids, tables, out, B, L, n, V, Dm, bad_id_count=bad_id_count, stream=stream)
+    return out
+
+
+def expand_embed_backward(ids, dout, V, *, stream=None):
+    """Gradient of the expansion w.r.t. the tables, sparse: ids [B][L] int32, dout
+    [B][n*L][Dm] -> (uniq_ids [B*L] int32, drows [n][B*L][Dm] fp32, num_uniq [1] int32),
+    all device tensors; only the first num_uniq ids / rows are defined."""
+    import torch
+
+    B, L = ids.shape
+    N, Dm = dout.shape[1], dout.shape[2]
+    if N % L:
+        raise ValueError("dout must be [B][n*L][Dm]")
+    n = N // L
+    dev = dout.device
+    uniq = torch.empty(B * L, dtype=torch.int32, device=dev)
+    drows = torch.empty((n, B * L, Dm), dtype=torch.float32, device=dev)
+    num = torch.empty(1, dtype=torch.int32, device=dev)
+    need = hd_expand_embed_bwd_workspace_bytes(B, L)
+    ws = torch.empty(need, dtype=torch.uint8, device=dev)
+    hd_expand_embed_bwd(ids, dout, B, L, n, V, Dm, uniq, drows, num, ws, need, stream=stream)
+    return uniq, drows, num
+
+
+def cyclic_replicate(tables, m, *, stream=None):
+    """eq. (cyclic_init): tables [n][V][Dm] -> new [m][V][Dm] with table s = tables[s mod n]."""
+    import torch
+
+    n, V, Dm = tables.shape
+    out = torch.empty((m, V, Dm), dtype=tables.dtype, device=tables.device)
+    hd_cyclic_replicate(tables, out, n, m, V, Dm, stream=stream)
     return out

@@ -1,0 +1,513 @@
+// embed_bwd.hip -- gradient of the multi-stream token expansion with respect to the
+// n tables, and cyclic replication of the tables.
+//
+// The expansion of eq. (expansion) is a gather, out[b][t*n + s] = tables[s][ids[b][t]],
+// so its gradient is a scatter-add: table s at token id x receives the sum of the
+// upstream rows t*n + s of every token t with id x.  Done deterministically, without
+// atomics on the data:
+//   1. a stable LSD radix sort of the (id, token position) pairs by id, 8-bit digits
+//      (per-block digit histograms, one device-wide exclusive scan, then a scatter in
+//      which every block ranks its chunk stably with eight 1-bit splits in LDS); ids
+//      outside [0, V) get the key V and sort to the end;
+//   2. segment heads of the sorted ids give the distinct ids in ascending order and
+//      each id's run of token positions (ascending, as the sort is stable);
+//   3. one gather-reduce per (distinct id, stream): the upstream rows of the run are
+//      summed in fp32 in ascending token order (HBM-bound: every upstream row is read
+//      once, every gradient row written once).
+// The gradient comes out sparse, as (distinct ids, rows), so nothing scales with V;
+// hd_embed_grad_scatter_add adds such rows into a dense fp32 table gradient.
+//
+// Cyclic replication, eq. (cyclic_init): when the expansion factor grows from n to m
+// (a multiple of n), table s of the new set is table s mod n of the old one.
+#include <algorithm>
+
+#include "embed_internal.h"
+#include "hd_device.h"
+
+namespace hd {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kItems = 8;
+constexpr int kChunk = kThreads * kItems;  // keys per block in the scan and sort kernels
+constexpr int kWaves = kThreads / 64;
+
+// Exclusive scan of one int per thread across the workgroup; *total gets the sum.
+// `sh` is LDS scratch of kWaves + 1 ints.
+__device__ inline int block_exclusive_scan(int x, int *total, int *sh)
+{
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int v = x;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const int y = __shfl_up(v, o);
+        if (lane >= o) v += y;
+    }
+    if (lane == 63) sh[wave] = v;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int acc = 0;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) {
+            const int t = sh[w];
+            sh[w] = acc;
+            acc += t;
+        }
+        sh[kWaves] = acc;
+    }
+    __syncthreads();
+    const int r = sh[wave] + v - x;
+    *total = sh[kWaves];
+    __syncthreads();  // sh may be reused right away
+    return r;
+}
+
+// ---------------------------------------------------------------- device-wide scan
+// Exclusive scan of x[0..n) (n <= kChunk * kChunk) in three launches: per-block sums,
+// a one-block scan of the sums (the grand total goes to *total), per-block apply.
+
+__global__ __launch_bounds__(kThreads) void scan_reduce_kernel(const int *__restrict__ x, int n,
+                                                               int *__restrict__ sums)
+{
+    __shared__ int sh[kWaves + 1];
+    const int64_t base = (int64_t)blockIdx.x * kChunk + threadIdx.x * kItems;
+    int acc = 0;
+#pragma unroll
+    for (int j = 0; j < kItems; ++j)
+        if (base + j < n) acc += x[base + j];
+    int total;
+    block_exclusive_scan(acc, &total, sh);
+    if (threadIdx.x == 0) sums[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(kThreads) void scan_top_kernel(int *__restrict__ sums, int nb,
+                                                            int *__restrict__ total)
+{
+    __shared__ int sh[kWaves + 1];
+    const int base = threadIdx.x * kItems;
+    int v[kItems], acc = 0;
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        v[j] = base + j < nb ? sums[base + j] : 0;
+        acc += v[j];
+    }
+    int tot;
+    int run = block_exclusive_scan(acc, &tot, sh);
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        if (base + j < nb) sums[base + j] = run;
+        run += v[j];
+    }
+    if (threadIdx.x == 0 && total != nullptr) *total = tot;
+}
+
+__global__ __launch_bounds__(kThreads) void scan_apply_kernel(int *__restrict__ x, int n,
+                                                              const int *__restrict__ sums)
+{
+    __shared__ int sh[kWaves + 1];
+    const int64_t base = (int64_t)blockIdx.x * kChunk + threadIdx.x * kItems;
+    int v[kItems], acc = 0;
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        v[j] = base + j < n ? x[base + j] : 0;
+        acc += v[j];
+    }
+    int tot;
+    int run = block_exclusive_scan(acc, &tot, sh) + sums[blockIdx.x];
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        if (base + j < n) x[base + j] = run;
+        run += v[j];
+    }
+}
+
+hipError_t scan_exclusive(int *x, int n, int *sums, int *total, hipStream_t s)
+{
+    const int nb = (n + kChunk - 1) / kChunk;
+    scan_reduce_kernel<<<nb, kThreads, 0, s>>>(x, n, sums);
+    scan_top_kernel<<<1, kThreads, 0, s>>>(sums, nb, total);
+    scan_apply_kernel<<<nb, kThreads, 0, s>>>(x, n, sums);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- radix sort
+
+// sort key of token i: its id, or V for an id outside [0, V)
+__device__ inline uint32_t id_key(const int32_t *ids, int64_t i, int64_t V)
+{
+    const int32_t id = ids[i];
+    return id >= 0 && (int64_t)id < V ? (uint32_t)id : (uint32_t)V;
+}
+
+// digit histogram of each block's chunk, stored digit-major: hist[d * nblk + block]
+__global__ __launch_bounds__(kThreads) void radix_hist_kernel(const uint32_t *__restrict__ keys,
+                                                              const int32_t *__restrict__ ids,
+                                                              int M, int64_t V, int shift,
+                                                              int *__restrict__ hist)
+{
+    __shared__ int h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kChunk + threadIdx.x * kItems;
+#pragma unroll
+    for (int j = 0; j < kItems; ++j)
+        if (base + j < M) {
+            const uint32_t key = ids != nullptr ? id_key(ids, base + j, V) : keys[base + j];
+            atomicAdd(&h[(key >> shift) & 255], 1);
+        }
+    __syncthreads();
+    hist[threadIdx.x * gridDim.x + blockIdx.x] = h[threadIdx.x];
+}
+
+// Stable scatter of one 8-bit digit pass.  offs = exclusive scan of the histograms
+// (digit-major), so offs[d * nblk + block] is where this block's first key of digit d
+// goes.  Keys and values come from (ids, token index) on the first pass.
+__global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
+    const uint32_t *__restrict__ keys, const int32_t *__restrict__ vals,
+    const int32_t *__restrict__ ids, int M, int64_t V, int shift, const int *__restrict__ offs,
+    uint32_t *__restrict__ keys_out, int32_t *__restrict__ vals_out)
+{
+    __shared__ uint32_t sk[kChunk];
+    __shared__ int32_t sv[kChunk];
+    __shared__ int h[256];
+    __shared__ int sh[kWaves + 1];
+    const int64_t base = (int64_t)blockIdx.x * kChunk;
+    const int valid = (int)min((int64_t)kChunk, (int64_t)M - base);
+    uint32_t k[kItems];
+    int32_t v[kItems];
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        const int c = threadIdx.x * kItems + j;
+        if (c < valid) {
+            k[j] = ids != nullptr ? id_key(ids, base + c, V) : keys[base + c];
+            v[j] = ids != nullptr ? (int32_t)(base + c) : vals[base + c];
+        } else {
+            k[j] = 0xffffffffu;  // padding: digit 255, after every real key of the chunk
+            v[j] = 0;
+        }
+    }
+    // local stable sort of the chunk by the digit: one stable 1-bit split per bit
+    for (int bit = 0; bit < 8; ++bit) {
+        int zeros = 0;
+#pragma unroll
+        for (int j = 0; j < kItems; ++j) zeros += ((k[j] >> (shift + bit)) & 1) ? 0 : 1;
+        int ztot;
+        const int zb = block_exclusive_scan(zeros, &ztot, sh);  // zeros in earlier threads
+        int zc = 0;
+#pragma unroll
+        for (int j = 0; j < kItems; ++j) {
+            const int c = threadIdx.x * kItems + j;
+            const bool one = (k[j] >> (shift + bit)) & 1;
+            const int zbefore = zb + zc;  // zeros before element c
+            const int dst = one ? ztot + (c - zbefore) : zbefore;
+            zc += one ? 0 : 1;
+            sk[dst] = k[j];
+            sv[dst] = v[j];
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kItems; ++j) {
+            k[j] = sk[threadIdx.x * kItems + j];
+            v[j] = sv[threadIdx.x * kItems + j];
+        }
+        __syncthreads();
+    }
+    // start of each digit's run inside the sorted chunk (real keys only)
+    h[threadIdx.x] = 0;
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kItems; ++j)
+        if (threadIdx.x * kItems + j < valid) atomicAdd(&h[(k[j] >> shift) & 255], 1);
+    __syncthreads();
+    int tot;
+    const int start = block_exclusive_scan(h[threadIdx.x], &tot, sh);
+    h[threadIdx.x] = start;
+    __syncthreads();
+    // the chunk's real keys are its first `valid` sorted entries
+#pragma unroll
+    for (int j = 0; j < kItems; ++j) {
+        const int c = threadIdx.x * kItems + j;
+        if (c < valid) {
+            const int d = (k[j] >> shift) & 255;
+            const int64_t dst = (int64_t)offs[d * gridDim.x + blockIdx.x] + (c - h[d]);
+            keys_out[dst] = k[j];
+            vals_out[dst] = v[j];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- segments
+
+__global__ __launch_bounds__(kThreads) void seg_flags_kernel(const uint32_t *__restrict__ keys,
+                                                             int M, int *__restrict__ flags)
+{
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i < M) flags[i] = (i == 0 || keys[i] != keys[i - 1]) ? 1 : 0;
+}
+
+// segidx = exclusive scan of the head flags: a head's value is its segment's index
+__global__ __launch_bounds__(kThreads) void seg_write_kernel(const uint32_t *__restrict__ keys,
+                                                             const int *__restrict__ segidx,
+                                                             int M, int64_t V,
+                                                             int *__restrict__ seg_start,
+                                                             int32_t *__restrict__ uniq)
+{
+    const int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (i >= M || !(i == 0 || keys[i] != keys[i - 1])) return;
+    const int u = segidx[i];
+    seg_start[u] = (int)i;
+    if (keys[i] < (uint64_t)V) uniq[u] = (int32_t)keys[i];
+}
+
+// closes the last segment and counts the distinct in-range ids (the run of key V, if
+// any, is the last segment and is left out)
+__global__ void seg_finish_kernel(const uint32_t *__restrict__ keys, int M, int64_t V,
+                                  const int *__restrict__ nseg, int *__restrict__ seg_start,
+                                  int32_t *__restrict__ num_uniq)
+{
+    const int S = *nseg;
+    seg_start[S] = M;
+    *num_uniq = S - (keys[M - 1] == (uint64_t)V ? 1 : 0);
+}
+
+// ---------------------------------------------------------------- gather-reduce
+
+template <typename E>
+__device__ inline float elem(const E *p, int64_t i);
+template <>
+__device__ inline float elem<bf16>(const bf16 *p, int64_t i)
+{
+    return __uint_as_float((uint32_t)reinterpret_cast<const uint16_t *>(p)[i] << 16);
+}
+template <>
+__device__ inline float elem<float>(const float *p, int64_t i)
+{
+    return p[i];
+}
+
+// drows[s][u][:] = sum over the run of distinct id u of dout[pos*n + s][:] (fp32, in
+// ascending token order).  Work items (u, s) are strided over the grid; the item
+// count is read from the device.  VEC consecutive elements per thread.
+template <typename E, int VEC>
+__global__ __launch_bounds__(kThreads) void embed_grad_reduce_kernel(
+    const E *__restrict__ dout, const int32_t *__restrict__ pos, const int *__restrict__ seg_start,
+    const int32_t *__restrict__ num_uniq, int n, int Dm, int rows_cap, float *__restrict__ drows)
+{
+    const int64_t items = (int64_t)*num_uniq * n;
+    for (int64_t w = blockIdx.x; w < items; w += gridDim.x) {
+        const int u = (int)(w / n), s = (int)(w % n);
+        const int i0 = seg_start[u], i1 = seg_start[u + 1];
+        float *dst = drows + ((int64_t)s * rows_cap + u) * Dm;
+        for (int d0 = threadIdx.x * VEC; d0 < Dm; d0 += kThreads * VEC) {
+            float acc[VEC];
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+            for (int i = i0; i < i1; ++i) {
+                const int64_t row = (int64_t)pos[i] * n + s;
+                const E *src = dout + row * Dm + d0;
+                if constexpr (VEC == 8 && sizeof(E) == 2) {
+                    const u32x4 w4 = *reinterpret_cast<const u32x4 *>(src);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        acc[2 * e] += bf16_lo(w4[e]);
+                        acc[2 * e + 1] += bf16_hi(w4[e]);
+                    }
+                } else if constexpr (VEC == 8) {
+                    const f32x4 a = *reinterpret_cast<const f32x4 *>(src);
+                    const f32x4 b = *reinterpret_cast<const f32x4 *>(src + 4);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        acc[e] += a[e];
+                        acc[4 + e] += b[e];
+                    }
+                } else {
+#pragma unroll
+                    for (int e = 0; e < VEC; ++e) acc[e] += elem<E>(src, e);
+                }
+            }
+            if constexpr (VEC == 8) {
+                *reinterpret_cast<f32x4 *>(dst + d0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
+                *reinterpret_cast<f32x4 *>(dst + d0 + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
+            } else {
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) dst[d0 + e] = acc[e];
+            }
+        }
+    }
+}
+
+// dtables[s][uniq[u]][:] += drows[s][u][:] for u < *num_uniq (distinct ids: one writer
+// per destination row, no atomics)
+__global__ __launch_bounds__(kThreads) void embed_grad_scatter_add_kernel(
+    const int32_t *__restrict__ uniq, const float *__restrict__ drows,
+    const int32_t *__restrict__ num_uniq, int rows_cap, int n, int64_t V, int Dm,
+    float *__restrict__ dtables)
+{
+    const int64_t items = (int64_t)*num_uniq * n;
+    for (int64_t w = blockIdx.x; w < items; w += gridDim.x) {
+        const int u = (int)(w / n), s = (int)(w % n);
+        const int32_t x = uniq[u];
+        if (x < 0 || (int64_t)x >= V) continue;
+        const float *src = drows + ((int64_t)s * rows_cap + u) * Dm;
+        float *dst = dtables + ((int64_t)s * V + x) * Dm;
+        for (int d = threadIdx.x; d < Dm; d += kThreads) dst[d] += src[d];
+    }
+}
+
+// ---------------------------------------------------------------- cyclic replication
+
+// dst table s (s0 <= s < m) = src table s mod n; `words` W-sized words per table
+template <typename W>
+__global__ __launch_bounds__(kThreads) void cyclic_replicate_kernel(const W *__restrict__ src,
+                                                                    W *__restrict__ dst, int n,
+                                                                    int s0, int64_t words)
+{
+    const int s = s0 + blockIdx.y;
+    const W *a = src + (int64_t)(s % n) * words;
+    W *b = dst + (int64_t)s * words;
+    for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < words;
+         e += (int64_t)gridDim.x * kThreads)
+        b[e] = a[e];
+}
+
+}  // namespace
+
+EmbedBwdWorkspace embed_bwd_workspace(int M)
+{
+    EmbedBwdWorkspace w;
+    const size_t m4 = align256((size_t)M * 4);
+    const int nblk = (M + kChunk - 1) / kChunk;
+    w.keys_a = 0;
+    w.vals_a = w.keys_a + m4;
+    w.keys_b = w.vals_a + m4;
+    w.vals_b = w.keys_b + m4;
+    w.hist = w.vals_b + m4;
+    w.sums = w.hist + align256((size_t)256 * nblk * 4);
+    w.scalars = w.sums + align256((size_t)kChunk * 4);
+    w.segidx = w.scalars + 256;
+    w.seg_start = w.segidx + m4;
+    w.total = w.seg_start + align256(((size_t)M + 1) * 4);
+    return w;
+}
+
+hipError_t launch_embed_bwd(const int32_t *ids, const void *dout, int B, int L, int n, int64_t V,
+                            int Dm, int esize, int32_t *uniq, float *drows, int32_t *num_uniq,
+                            void *ws, hipStream_t s)
+{
+    const int M = B * L;
+    const EmbedBwdWorkspace w = embed_bwd_workspace(M);
+    char *base = static_cast<char *>(ws);
+    uint32_t *ka = reinterpret_cast<uint32_t *>(base + w.keys_a);
+    int32_t *va = reinterpret_cast<int32_t *>(base + w.vals_a);
+    uint32_t *kb = reinterpret_cast<uint32_t *>(base + w.keys_b);
+    int32_t *vb = reinterpret_cast<int32_t *>(base + w.vals_b);
+    int *hist = reinterpret_cast<int *>(base + w.hist);
+    int *sums = reinterpret_cast<int *>(base + w.sums);
+    int *nseg = reinterpret_cast<int *>(base + w.scalars);
+    int *segidx = reinterpret_cast<int *>(base + w.segidx);
+    int *seg_start = reinterpret_cast<int *>(base + w.seg_start);
+
+    const int nblk = (M + kChunk - 1) / kChunk;
+    int bits = 0;
+    while (bits < 32 && ((uint64_t)V >> bits) != 0) ++bits;  // the largest key is V
+    const int passes = bits == 0 ? 1 : (bits + 7) / 8;
+
+    timing_before("embed_bwd_sort", s);
+    hipError_t e = hipSuccess;
+    const uint32_t *kin = nullptr;
+    const int32_t *vin = nullptr;
+    for (int p = 0; p < passes && e == hipSuccess; ++p) {
+        uint32_t *kout = (p & 1) ? kb : ka;
+        int32_t *vout = (p & 1) ? vb : va;
+        const int32_t *from_ids = p == 0 ? ids : nullptr;
+        radix_hist_kernel<<<nblk, kThreads, 0, s>>>(kin, from_ids, M, V, 8 * p, hist);
+        e = scan_exclusive(hist, 256 * nblk, sums, nullptr, s);
+        radix_scatter_kernel<<<nblk, kThreads, 0, s>>>(kin, vin, from_ids, M, V, 8 * p, hist,
+                                                       kout, vout);
+        kin = kout;
+        vin = vout;
+        if (e == hipSuccess) e = hipGetLastError();
+    }
+    timing_after(s);
+    if (e != hipSuccess) return e;
+
+    timing_before("embed_bwd_segments", s);
+    const int nb1 = (M + kThreads - 1) / kThreads;
+    seg_flags_kernel<<<nb1, kThreads, 0, s>>>(kin, M, segidx);
+    e = scan_exclusive(segidx, M, sums, nseg, s);
+    seg_write_kernel<<<nb1, kThreads, 0, s>>>(kin, segidx, M, V, seg_start, uniq);
+    seg_finish_kernel<<<1, 1, 0, s>>>(kin, M, V, nseg, seg_start, num_uniq);
+    if (e == hipSuccess) e = hipGetLastError();
+    timing_after(s);
+    if (e != hipSuccess) return e;
+
+    // enough workgroups to keep every CU streaming; items beyond *num_uniq * n are
+    // strided over them
+    const int64_t max_items = (int64_t)M * n;
+    const int grid = (int)(max_items < 8192 ? max_items : 8192);
+    timing_before("embed_bwd_reduce", s);
+    const bool vec = Dm % 8 == 0;
+    if (esize == 2) {
+        const bf16 *d = static_cast<const bf16 *>(dout);
+        if (vec)
+            embed_grad_reduce_kernel<bf16, 8><<<grid, kThreads, 0, s>>>(d, vin, seg_start, num_uniq,
+                                                                        n, Dm, M, drows);
+        else
+            embed_grad_reduce_kernel<bf16, 1><<<grid, kThreads, 0, s>>>(d, vin, seg_start, num_uniq,
+                                                                        n, Dm, M, drows);
+    } else {
+        const float *d = static_cast<const float *>(dout);
+        if (vec)
+            embed_grad_reduce_kernel<float, 8><<<grid, kThreads, 0, s>>>(d, vin, seg_start,
+                                                                         num_uniq, n, Dm, M, drows);
+        else
+            embed_grad_reduce_kernel<float, 1><<<grid, kThreads, 0, s>>>(d, vin, seg_start,
+                                                                         num_uniq, n, Dm, M, drows);
+    }
+    e = hipGetLastError();
+    timing_after(s);
+    return e;
+}
+
+hipError_t launch_embed_grad_scatter_add(const int32_t *uniq, const float *drows,
+                                         const int32_t *num_uniq, int rows_cap, int n, int64_t V,
+                                         int Dm, float *dtables, hipStream_t s)
+{
+    const int64_t max_items = (int64_t)rows_cap * n;
+    const int grid = (int)(max_items < 8192 ? max_items : 8192);
+    timing_before("embed_grad_scatter_add", s);
+    embed_grad_scatter_add_kernel<<<grid, kThreads, 0, s>>>(uniq, drows, num_uniq, rows_cap, n, V,
+                                                            Dm, dtables);
+    hipError_t e = hipGetLastError();
+    timing_after(s);
+    return e;
+}
+
+hipError_t launch_cyclic_replicate(const void *src, void *dst, int n, int m, int64_t V, int Dm,
+                                   int esize, hipStream_t s)
+{
+    const int s0 = src == dst ? n : 0;  // in place: the first n tables are already there
+    if (s0 >= m) return hipSuccess;
+    const int64_t bytes = V * (int64_t)Dm * esize;
+    const dim3 block(kThreads);
+    timing_before("cyclic_replicate", s);
+    if (bytes % 16 == 0) {
+        const int64_t words = bytes / 16;
+        const dim3 grid((unsigned)std::min<int64_t>((words + kThreads - 1) / kThreads, 4096),
+                        (unsigned)(m - s0));
+        cyclic_replicate_kernel<u32x4><<<grid, block, 0, s>>>(
+            static_cast<const u32x4 *>(src), static_cast<u32x4 *>(dst), n, s0, words);
+    } else {
+        const int64_t words = bytes / 2;
+        const dim3 grid((unsigned)std::min<int64_t>((words + kThreads - 1) / kThreads, 4096),
+                        (unsigned)(m - s0));
+        cyclic_replicate_kernel<uint16_t><<<grid, block, 0, s>>>(
+            static_cast<const uint16_t *>(src), static_cast<uint16_t *>(dst), n, s0, words);
+    }
+    hipError_t e = hipGetLastError();
+    timing_after(s);
+    return e;
+}
+
+}  // namespace hd

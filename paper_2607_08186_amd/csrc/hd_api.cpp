@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "../../include/hd.h"
+#include "embed_internal.h"
 #include "hd_internal.h"
 
 namespace {
@@ -159,6 +160,85 @@ hd_status_t hd_expand_embed(const int32_t *ids, const void *tables, void *out, i
     return hip_status(hd::launch_expand_embed(ids, tables, out, B, L, n, V, Dm, esize,
                                               bad_id_count, (hipStream_t)stream),
                       "hd_expand_embed launch");
+}
+
+size_t hd_expand_embed_bwd_workspace_bytes(int B, int L)
+{
+    if (B <= 0 || L <= 0 || (int64_t)B * L > hd::kEmbedBwdMaxTokens) return 0;
+    return hd::embed_bwd_workspace(B * L).total;
+}
+
+hd_status_t hd_expand_embed_bwd(const int32_t *ids, const void *dout, int B, int L, int n,
+                                int64_t V, int Dm, hd_dtype_t dtype, int32_t *uniq_ids,
+                                float *drows, int32_t *num_uniq, void *workspace,
+                                size_t workspace_bytes, hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (!ids || !dout || !uniq_ids || !drows || !num_uniq)
+        return fail(HD_ERR_INVALID_ARG, "null ids, dout, uniq_ids, drows or num_uniq");
+    if (B <= 0 || L <= 0 || n <= 0 || Dm <= 0 || V <= 0)
+        return fail(HD_ERR_INVALID_ARG, "sizes must be positive (B=%d L=%d n=%d V=%lld Dm=%d)", B,
+                    L, n, (long long)V, Dm);
+    if (V > INT32_MAX) return fail(HD_ERR_INVALID_ARG, "V=%lld exceeds int32 ids", (long long)V);
+    if (dtype != HD_DTYPE_BF16 && dtype != HD_DTYPE_F32)
+        return fail(HD_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    if ((int64_t)B * L > hd::kEmbedBwdMaxTokens)
+        return fail(HD_ERR_INVALID_ARG, "B*L=%lld exceeds %d tokens", (long long)B * L,
+                    hd::kEmbedBwdMaxTokens);
+    if (!aligned16(dout) || !aligned16(drows) || (reinterpret_cast<uintptr_t>(ids) & 3) ||
+        (reinterpret_cast<uintptr_t>(uniq_ids) & 3) || (reinterpret_cast<uintptr_t>(num_uniq) & 3))
+        return fail(HD_ERR_INVALID_ARG,
+                    "dout/drows must be 16-byte aligned, ids/uniq_ids/num_uniq 4-byte aligned");
+    const size_t need = hd::embed_bwd_workspace(B * L).total;
+    if (!workspace) return fail(HD_ERR_INVALID_ARG, "null workspace (%zu bytes needed)", need);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+        return fail(HD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need)
+        return fail(HD_ERR_INVALID_ARG, "workspace of %zu bytes is short of %zu", workspace_bytes,
+                    need);
+    const int esize = dtype == HD_DTYPE_BF16 ? 2 : 4;
+    return hip_status(hd::launch_embed_bwd(ids, dout, B, L, n, V, Dm, esize, uniq_ids, drows,
+                                           num_uniq, workspace, (hipStream_t)stream),
+                      "hd_expand_embed_bwd launch");
+}
+
+hd_status_t hd_embed_grad_scatter_add(const int32_t *uniq_ids, const float *drows,
+                                      const int32_t *num_uniq, int max_rows, int n, int64_t V,
+                                      int Dm, float *dtables, hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (!uniq_ids || !drows || !num_uniq || !dtables)
+        return fail(HD_ERR_INVALID_ARG, "null uniq_ids, drows, num_uniq or dtables");
+    if (max_rows <= 0 || n <= 0 || Dm <= 0 || V <= 0 || V > INT32_MAX)
+        return fail(HD_ERR_INVALID_ARG, "bad sizes (max_rows=%d n=%d V=%lld Dm=%d)", max_rows, n,
+                    (long long)V, Dm);
+    if ((reinterpret_cast<uintptr_t>(drows) & 3) || (reinterpret_cast<uintptr_t>(dtables) & 3) ||
+        (reinterpret_cast<uintptr_t>(uniq_ids) & 3) || (reinterpret_cast<uintptr_t>(num_uniq) & 3))
+        return fail(HD_ERR_INVALID_ARG, "pointers must be 4-byte aligned");
+    return hip_status(hd::launch_embed_grad_scatter_add(uniq_ids, drows, num_uniq, max_rows, n, V,
+                                                        Dm, dtables, (hipStream_t)stream),
+                      "hd_embed_grad_scatter_add launch");
+}
+
+hd_status_t hd_cyclic_replicate(const void *src, void *dst, int n, int m, int64_t V, int Dm,
+                                hd_dtype_t dtype, hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (!src || !dst) return fail(HD_ERR_INVALID_ARG, "null src or dst");
+    if (n <= 0 || m < n || m % n != 0 || m > 65535)
+        return fail(HD_ERR_INVALID_ARG, "m=%d must be a multiple of n=%d (at most 65535)", m, n);
+    if (V <= 0 || Dm <= 0) return fail(HD_ERR_INVALID_ARG, "V and Dm must be positive");
+    if (dtype != HD_DTYPE_BF16 && dtype != HD_DTYPE_F32)
+        return fail(HD_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    if (!aligned16(src) || !aligned16(dst))
+        return fail(HD_ERR_INVALID_ARG, "src/dst must be 16-byte aligned");
+    const int esize = dtype == HD_DTYPE_BF16 ? 2 : 4;
+    const uintptr_t a = reinterpret_cast<uintptr_t>(src), b = reinterpret_cast<uintptr_t>(dst);
+    const uintptr_t table = (uintptr_t)V * Dm * esize;
+    if (src != dst && a < b + (uintptr_t)m * table && b < a + (uintptr_t)n * table)
+        return fail(HD_ERR_INVALID_ARG, "src and dst overlap without being the same buffer");
+    return hip_status(hd::launch_cyclic_replicate(src, dst, n, m, V, Dm, esize, (hipStream_t)stream),
+                      "hd_cyclic_replicate launch");
 }
 
 namespace {

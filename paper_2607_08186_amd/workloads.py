@@ -100,3 +100,10 @@ def stack_useful_flop(s: Shape = QWEN8B.shape) -> int:
 def embed_bytes(B: int, L: int, n: int, Dm: int, esize: int = 2) -> int:
     """Compulsory traffic of the expansion: read n*L rows, write n*L rows, read ids."""
     return 2 * B * n * L * Dm * esize + B * L * 4
+
+
+def embed_bwd_bytes(B: int, L: int, n: int, Dm: int, n_distinct: int, esize: int = 2) -> int:
+    """Compulsory traffic of the expansion's backward: read every upstream expanded row
+    and the ids once, write one fp32 gradient row per (distinct id, stream) and the
+    distinct ids (the sort of the B*L (id, token) pairs is not counted)."""
+    return B * n * L * Dm * esize + B * L * 4 + n * n_distinct * Dm * 4 + n_distinct * 4

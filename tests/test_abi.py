@@ -199,6 +199,62 @@ def test_expand_validation(lib, args, code):
     assert st == code
 
 
+@pytest.mark.parametrize("args,code", [
+    (dict(ids=None), INVALID), (dict(drows=None), INVALID), (dict(num=None), INVALID),
+    (dict(B=0), INVALID), (dict(n=0), INVALID), (dict(V=0), INVALID), (dict(V=1 << 40), INVALID),
+    (dict(Dm=0), INVALID), (dict(dtype=7), INVALID), (dict(L=4194305), INVALID),
+    (dict(dout=FAKE + 8), INVALID), (dict(drows=FAKE + 4), INVALID), (dict(uniq=FAKE + 2), INVALID),
+    (dict(ws=None), INVALID), (dict(ws=FAKE + 128), INVALID), (dict(ws_bytes=100), INVALID),
+])
+def test_expand_bwd_validation(lib, args, code):
+    a = dict(ids=FAKE, dout=FAKE, B=1, L=4, n=2, V=10, Dm=8, dtype=0, uniq=FAKE, drows=FAKE,
+             num=FAKE, ws=FAKE)
+    a.update(args)
+    need = lib.hd_expand_embed_bwd_workspace_bytes(1, 4)
+    st = lib.hd_expand_embed_bwd(a["ids"], a["dout"], a["B"], a["L"], a["n"], a["V"], a["Dm"],
+                                 a["dtype"], a["uniq"], a["drows"], a["num"], a["ws"],
+                                 a.get("ws_bytes", need), None)
+    assert st == code
+    assert lib.hd_last_error().decode() != ""
+
+
+def test_expand_bwd_workspace_size(lib):
+    """Sort buffers (4 x 4 bytes per token), histograms, scan sums, segment indices and
+    starts; 0 for sizes the entry point rejects."""
+    assert lib.hd_expand_embed_bwd_workspace_bytes(0, 5) == 0
+    assert lib.hd_expand_embed_bwd_workspace_bytes(1, 4194305) == 0
+    for B, L in [(1, 1), (1, 4096), (2, 2049), (1, 4194304)]:
+        M = B * L
+        got = lib.hd_expand_embed_bwd_workspace_bytes(B, L)
+        assert got >= 6 * 4 * M + 4 and got < 6 * 4 * M + 256 * 4 * (M // 2048 + 1) + 16384
+        assert got % 256 == 0
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(uniq=None), INVALID), (dict(dtables=None), INVALID), (dict(rows=0), INVALID),
+    (dict(n=0), INVALID), (dict(V=0), INVALID), (dict(Dm=-1), INVALID), (dict(drows=FAKE + 2), INVALID),
+])
+def test_grad_scatter_add_validation(lib, args, code):
+    a = dict(uniq=FAKE, drows=FAKE, num=FAKE, rows=4, n=2, V=10, Dm=8, dtables=FAKE)
+    a.update(args)
+    st = lib.hd_embed_grad_scatter_add(a["uniq"], a["drows"], a["num"], a["rows"], a["n"],
+                                       a["V"], a["Dm"], a["dtables"], None)
+    assert st == code
+
+
+@pytest.mark.parametrize("args,code", [
+    (dict(src=None), INVALID), (dict(n=0), INVALID), (dict(m=3), INVALID), (dict(m=1), INVALID),
+    (dict(V=0), INVALID), (dict(dtype=9), INVALID), (dict(dst=FAKE + 8), INVALID),
+    (dict(dst=FAKE + 8192), INVALID),  # one 8 KB table past src: overlaps without aliasing
+])
+def test_cyclic_replicate_validation(lib, args, code):
+    a = dict(src=FAKE, dst=FAKE + (1 << 30), n=2, m=4, V=64, Dm=64, dtype=0)
+    a.update(args)
+    st = lib.hd_cyclic_replicate(a["src"], a["dst"], a["n"], a["m"], a["V"], a["Dm"], a["dtype"],
+                                 None)
+    assert st == code
+
+
 def test_missing_library_raises(monkeypatch, tmp_path):
     """No silent fallback: a missing libhd.so is an ImportError on first use."""
     monkeypatch.setattr(binding, "_lib", None)
