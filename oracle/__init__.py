@@ -101,34 +101,50 @@ def _check_window(mode, window):
         raise ValueError("local mode needs a window of at least 1 expanded position")
 
 
-def _dims(q, k, B, L, n, mode, scale, nthreads, window=0):
+FINAL = 4  # or-ed into the mode: queries at the final stream of each token only
+
+
+def _dims(q, k, B, L, n, mode, scale, nthreads, window=0, final=False):
     N = n * L
-    if q.shape[:2] != (B, N) or k.shape[:2] != (B, N) or q.shape[3] != k.shape[3]:
-        raise ValueError("q must be [B][n*L][Hq][D] and k/v [B][n*L][Hkv][D]")
+    qrows = L if final else N
+    if q.shape[:2] != (B, qrows) or k.shape[:2] != (B, N) or q.shape[3] != k.shape[3]:
+        raise ValueError(f"q must be [B][{'L' if final else 'n*L'}][Hq][D] and k/v "
+                         "[B][n*L][Hkv][D]")
     Hq, D, Hkv = q.shape[2], q.shape[3], k.shape[2]
     if Hq % Hkv:
         raise ValueError("Hq must be a multiple of Hkv")
     _check_window(mode, window)
-    return (B, L, n, Hq, Hkv, D, int(mode), int(window), float(scale),
+    return (B, L, n, Hq, Hkv, D, int(mode) | (FINAL if final else 0), int(window), float(scale),
             int(nthreads or default_threads())), Hq, Hkv, D
 
 
-def sfa_fwd(q, k, v, *, L, n, mode, scale, nthreads=None, window=0):
-    """Full forward. Returns (o [B][N][Hq][D], lse [B][Hq][N]) in float64."""
+def _final_rows(rows, n, final):
+    """Query rows (b, hq, t) of a final-stream layer name expanded position t*n + n - 1."""
+    rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3).copy()
+    if final:
+        rows[:, 2] = rows[:, 2] * n + n - 1
+    return rows
+
+
+def sfa_fwd(q, k, v, *, L, n, mode, scale, nthreads=None, window=0, final=False):
+    """Full forward. Returns (o [B][N][Hq][D], lse [B][Hq][N]) in float64; with
+    final=True, q and o are [B][L][Hq][D] (final-stream queries) and lse [B][Hq][L]."""
     (q, k, v), code = _prep(q, k, v)
     B = q.shape[0]
-    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads, window)
-    o = np.zeros((B, n * L, Hq, D))
-    lse = np.zeros((B, Hq, n * L))
+    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads, window, final)
+    rows = L if final else n * L
+    o = np.zeros((B, rows, Hq, D))
+    lse = np.zeros((B, Hq, rows))
     _load().oracle_sfa_fwd(_ptr(q), _ptr(k), _ptr(v), code, _ptr(o), _ptr(lse), *dims)
     return o, lse
 
 
-def sfa_fwd_rows(q, k, v, rows, *, L, n, mode, scale, nthreads=None, window=0):
-    """Forward of listed rows; rows is int64 [R][3] of (b, hq, p)."""
+def sfa_fwd_rows(q, k, v, rows, *, L, n, mode, scale, nthreads=None, window=0, final=False):
+    """Forward of listed rows; rows is int64 [R][3] of (b, hq, p) (p = t, the token,
+    with final=True)."""
     (q, k, v), code = _prep(q, k, v)
-    rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
-    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads, window)
+    rows = _final_rows(rows, n, final)
+    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads, window, final)
     o = np.zeros((len(rows), D))
     lse = np.zeros(len(rows))
     _load().oracle_sfa_fwd_rows(_ptr(q), _ptr(k), _ptr(v), code, _ptr(rows), len(rows),
@@ -136,12 +152,13 @@ def sfa_fwd_rows(q, k, v, rows, *, L, n, mode, scale, nthreads=None, window=0):
     return o, lse
 
 
-def sfa_bwd(q, k, v, dout, *, L, n, mode, scale, nthreads=None, window=0):
-    """Full backward from (q, k, v, dO). Returns (dq, dk, dv) in float64."""
+def sfa_bwd(q, k, v, dout, *, L, n, mode, scale, nthreads=None, window=0, final=False):
+    """Full backward from (q, k, v, dO). Returns (dq, dk, dv) in float64 (dq, like q
+    and dO, [B][L][Hq][D] with final=True)."""
     (q, k, v, dout), code = _prep(q, k, v, dout)
     B = q.shape[0]
-    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads, window)
-    dq = np.zeros((B, n * L, Hq, D))
+    dims, Hq, Hkv, D = _dims(q, k, B, L, n, mode, scale, nthreads, window, final)
+    dq = np.zeros((B, L if final else n * L, Hq, D))
     dk = np.zeros((B, n * L, Hkv, D))
     dv = np.zeros((B, n * L, Hkv, D))
     _load().oracle_sfa_bwd(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), code, _ptr(dq), _ptr(dk),
@@ -149,22 +166,24 @@ def sfa_bwd(q, k, v, dout, *, L, n, mode, scale, nthreads=None, window=0):
     return dq, dk, dv
 
 
-def sfa_bwd_dq_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None, window=0):
-    """dQ of listed query rows (b, hq, p)."""
+def sfa_bwd_dq_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None, window=0,
+                    final=False):
+    """dQ of listed query rows (b, hq, p) ((b, hq, t) with final=True)."""
     (q, k, v, dout), code = _prep(q, k, v, dout)
-    rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
-    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads, window)
+    rows = _final_rows(rows, n, final)
+    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads, window, final)
     dq = np.zeros((len(rows), D))
     _load().oracle_sfa_bwd_dq_rows(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), code, _ptr(rows),
                                    len(rows), _ptr(dq), *dims)
     return dq
 
 
-def sfa_bwd_dkdv_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None, window=0):
+def sfa_bwd_dkdv_rows(q, k, v, dout, rows, *, L, n, mode, scale, nthreads=None, window=0,
+                      final=False):
     """dK, dV of listed key rows (b, hk, j), summed over the group's query heads."""
     (q, k, v, dout), code = _prep(q, k, v, dout)
     rows = np.ascontiguousarray(rows, dtype=np.int64).reshape(-1, 3)
-    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads, window)
+    dims, Hq, Hkv, D = _dims(q, k, q.shape[0], L, n, mode, scale, nthreads, window, final)
     dk = np.zeros((len(rows), D))
     dv = np.zeros((len(rows), D))
     _load().oracle_sfa_bwd_dkdv_rows(_ptr(q), _ptr(k), _ptr(v), _ptr(dout), code, _ptr(rows),

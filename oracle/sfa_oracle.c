@@ -14,6 +14,10 @@
  *     upstream rows per token id and stream);
  *   - cyclic replication of the tables when the expansion factor grows,
  *     eq. (cyclic_init): E_{n+k} <- E_k;
+ *   - layers that run only the final stream (Sec. "Training Cost", KV-mirror: only
+ *     the final stream of each token passes through the mirrored layers, whose keys
+ *     and values cover all n streams): the same masks evaluated for the query
+ *     positions t*n + n - 1 only;
  *   - token/stream index maps, eq. (indices), 0-based: t(p) = p / n, s(p) = p % n;
  *   - intra-stream attention mask, eq. (mask_intra): key p' visible from query p
  *     iff s(p') == s(p) and p' <= p (equivalently t(p') <= t(p));
@@ -38,6 +42,9 @@
  * Layouts (row-major, 0-based):
  *   q, o, dO, dq : [B][N][Hq][D]     k, v, dk, dv : [B][N][Hkv][D]
  *   lse          : [B][Hq][N] (natural log)        N = n * L
+ *   with ORC_FINAL or-ed into the mode (queries at the final stream only, keys and
+ *   values from all n streams): q, o, dO, dq [B][L][Hq][D] and lse [B][Hq][L]; the
+ *   row-selecting entry points still name query rows by expanded position.
  *   query head hq uses key/value head hq / (Hq / Hkv).
  *
  * Every function here is pinned by tests (closed forms, library reductions,
@@ -50,6 +57,11 @@
 #include <string.h>
 
 enum { ORC_INTRA = 0, ORC_MIX = 1, ORC_LOCAL = 2 };
+/* or-ed into a mode: only the final stream of each token carries a query row (the
+ * layers of Sec. "Training Cost" that run only the final stream, with keys and values
+ * from all n streams): q, o, dO and dq are [B][L][Hq][D], lse [B][Hq][L], and query row
+ * t sits at expanded position t*n + n - 1 */
+enum { ORC_FINAL = 4 };
 enum { ORC_F64 = 0, ORC_F32 = 1, ORC_BF16 = 2 };
 
 /* ---------------------------------------------------------------- inputs */
@@ -61,6 +73,7 @@ typedef struct {
     int mode;
     int64_t window; /* local cross-stream layers only */
     double scale;
+    int final_q; /* ORC_FINAL: queries at the final-stream positions only */
 } problem_t;
 
 static double load_elem(const void *base, int dtype, int64_t idx)
@@ -94,9 +107,25 @@ static int visible(int mode, int64_t n, int64_t window, int64_t pq, int64_t pk)
     return causal;
 }
 
+/* element (b, p, h, d) of q, o, dO or dq; p is an expanded position, which for
+ * final-stream queries is t*n + n - 1 and maps to row t of the [B][L] tensors */
 static int64_t q_index(const problem_t *P, int64_t b, int64_t p, int64_t h, int64_t d)
 {
+    if (P->final_q) return ((b * P->L + token_of(p, P->n)) * P->Hq + h) * P->D + d;
     return ((b * (P->n * P->L) + p) * P->Hq + h) * P->D + d;
+}
+
+/* does expanded position p carry a query row? */
+static int is_query(const problem_t *P, int64_t p)
+{
+    return !P->final_q || stream_of(p, P->n) == P->n - 1;
+}
+
+/* index of p's entry in lse [B][Hq][rows] */
+static int64_t lse_index(const problem_t *P, int64_t b, int64_t hq, int64_t p)
+{
+    if (P->final_q) return (b * P->Hq + hq) * P->L + token_of(p, P->n);
+    return (b * P->Hq + hq) * (P->n * P->L) + p;
 }
 
 static int64_t kv_index(const problem_t *P, int64_t b, int64_t p, int64_t h, int64_t d)
@@ -229,8 +258,9 @@ static void *fwd_job(void *arg)
     for (int64_t u = J->first; u < J->first + J->count; ++u) {
         int64_t b = u / P->Hq, hq = u % P->Hq;
         for (int64_t p = 0; p < N; ++p)
-            row_forward(P, b, hq, p, x, &o[q_index(P, b, p, hq, 0)],
-                        &lse[(b * P->Hq + hq) * N + p]);
+            if (is_query(P, p))
+                row_forward(P, b, hq, p, x, &o[q_index(P, b, p, hq, 0)],
+                            &lse[lse_index(P, b, hq, p)]);
     }
     free(x);
     return NULL;
@@ -240,7 +270,8 @@ static problem_t make_problem(const void *q, const void *k, const void *v, const
                               int dtype, int64_t B, int64_t L, int64_t n, int64_t Hq,
                               int64_t Hkv, int64_t D, int mode, int64_t window, double scale)
 {
-    problem_t P = {q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, window, scale};
+    problem_t P = {q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode & 3, window, scale,
+                   (mode & ORC_FINAL) != 0};
     return P;
 }
 
@@ -300,6 +331,7 @@ static void *bwd_job(void *arg)
         memset(dv_head, 0, (size_t)(N * D) * sizeof *dv_head);
         for (int64_t hq = hk * G; hq < (hk + 1) * G; ++hq)
             for (int64_t p = 0; p < N; ++p) {
+                if (!is_query(P, p)) continue;
                 double lse;
                 row_forward(P, b, hq, p, x, o, &lse);
                 row_backward(P, b, hq, p, x, o, &dq[q_index(P, b, p, hq, 0)], dk_head,
@@ -373,7 +405,7 @@ static void *dkdv_rows_job(void *arg)
         for (int64_t d = 0; d < D; ++d) dk[r * D + d] = dv[r * D + d] = 0.0;
         for (int64_t hq = hk * G; hq < (hk + 1) * G; ++hq)
             for (int64_t p = 0; p < N; ++p) {
-                if (!visible(P->mode, P->n, P->window, p, j)) continue;
+                if (!is_query(P, p) || !visible(P->mode, P->n, P->window, p, j)) continue;
                 double lse;
                 row_forward(P, b, hq, p, x, o, &lse);
                 row_backward(P, b, hq, p, x, o, NULL, &dk[r * D], &dv[r * D], &j, 1);

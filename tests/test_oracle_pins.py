@@ -599,3 +599,140 @@ def test_cyclic_replicate_reproduces_the_smaller_model_rows(oracle_mod):
         for s in range(n):
             np.testing.assert_array_equal(out4[0, t * 2 * n + s], out4[0, t * 2 * n + s + n])
             np.testing.assert_array_equal(out4[0, t * 2 * n + s], out2[0, t * n + s])
+
+
+# ------------------------------------------------- final-stream query layers
+
+
+def _embed_final(xf, n, fill):
+    """[B][L][H][D] final-stream rows placed at expanded positions t*n + n - 1 of a
+    [B][n*L][H][D] array whose other rows are `fill`."""
+    B, L, H, D = xf.shape
+    full = np.array(fill, dtype=np.float64, copy=True).reshape(B, n * L, H, D)
+    full[:, n - 1::n] = xf
+    return full
+
+
+FINAL_SHAPES = [(1, 7, 3, 2, 1, 4), (2, 5, 2, 4, 2, 8), (1, 6, 4, 3, 3, 5), (1, 9, 1, 2, 2, 6)]
+
+
+@pytest.mark.parametrize("mode,w", [(MIX, 0), (LOCAL, 5), (LOCAL, 1), (LOCAL, 100)])
+@pytest.mark.parametrize("shape", FINAL_SHAPES, ids=[str(s) for s in FINAL_SHAPES])
+def test_final_stream_layer_equals_library_rows(oracle_mod, shape, mode, w):
+    """Final-stream queries over all n streams' keys == library attention over the whole
+    expanded sequence (other query rows arbitrary, their upstream gradient zero), read at
+    the rows t*n + n - 1: outputs, lse, dq of those rows, and dk/dv of every key."""
+    B, L, n, Hq, Hkv, D = shape
+    N = n * L
+    r = np.random.default_rng(31 + L)
+    qf = r.standard_normal((B, L, Hq, D))
+    k = r.standard_normal((B, N, Hkv, D))
+    v = r.standard_normal((B, N, Hkv, D))
+    dof = r.standard_normal((B, L, Hq, D))
+    qfull = _embed_final(qf, n, r.standard_normal((B, N, Hq, D)))
+    dofull = _embed_final(dof, n, np.zeros((B, N, Hq, D)))
+    scale = 0.7
+    keep = _band(N, w) if mode == LOCAL else _band(N, N)
+    to, tl, tdq, tdk, tdv = _torch_masked(qfull, k, v, dofull, scale, keep)
+    kw = dict(L=L, n=n, mode=mode, scale=scale, window=w, final=True)
+    o, lse = oracle_mod.sfa_fwd(qf, k, v, **kw)
+    dq, dk, dv = oracle_mod.sfa_bwd(qf, k, v, dof, **kw)
+    np.testing.assert_allclose(o, to[:, n - 1::n], atol=1e-12)
+    np.testing.assert_allclose(lse, tl[:, :, n - 1::n], atol=1e-12)
+    np.testing.assert_allclose(dq, tdq[:, n - 1::n], atol=1e-12)
+    np.testing.assert_allclose(dk, tdk, atol=1e-12)
+    np.testing.assert_allclose(dv, tdv, atol=1e-12)
+
+
+def test_final_stream_with_one_stream_is_the_mixing_layer(oracle_mod):
+    q, k, v, do = _rand(33, 2, 11, 1, 4, 2, 8)
+    kw = dict(L=11, n=1, mode=MIX, scale=0.4)
+    for a, b in zip(oracle_mod.sfa_fwd(q, k, v, **kw) + oracle_mod.sfa_bwd(q, k, v, do, **kw),
+                    oracle_mod.sfa_fwd(q, k, v, final=True, **kw)
+                    + oracle_mod.sfa_bwd(q, k, v, do, final=True, **kw)):
+        np.testing.assert_array_equal(a, b)
+
+
+@pytest.mark.parametrize("mode,w", [(MIX, 0), (LOCAL, 6)])
+def test_final_stream_uniform_logits(oracle_mod, mode, w):
+    """q = 0: token t's final-stream query sees (t+1)n keys (min with w for LOCAL), so
+    lse = ln|vis| and O is the mean of the visible values."""
+    L, n, D = 9, 3, 4
+    N = n * L
+    r = np.random.default_rng(34)
+    qf = np.zeros((1, L, 1, D))
+    k = r.standard_normal((1, N, 1, D))
+    v = r.standard_normal((1, N, 1, D))
+    o, lse = oracle_mod.sfa_fwd(qf, k, v, L=L, n=n, mode=mode, scale=1.0, window=w, final=True)
+    for t in range(L):
+        p = t * n + n - 1
+        lo = max(0, p - w + 1) if mode == LOCAL else 0
+        assert abs(lse[0, 0, t] - math.log(p + 1 - lo)) < 1e-12
+        np.testing.assert_allclose(o[0, t, 0], v[0, lo:p + 1, 0].mean(axis=0), atol=1e-12)
+
+
+def test_final_stream_replicated_streams_reduce_to_token_causal(oracle_mod):
+    """Keys/values identical across the n streams of every token (eq. (cyclic_init) at
+    the input): the final stream of token t sees n copies of each token <= t, i.e.
+    causal attention over the L tokens with lse raised by ln n."""
+    B, L, n, Hq, Hkv, D = 1, 10, 4, 2, 1, 6
+    r = np.random.default_rng(35)
+    qf = r.standard_normal((B, L, Hq, D))
+    kt = r.standard_normal((B, L, Hkv, D))
+    vt = r.standard_normal((B, L, Hkv, D))
+    k, v = np.repeat(kt, n, axis=1), np.repeat(vt, n, axis=1)
+    o, lse = oracle_mod.sfa_fwd(qf, k, v, L=L, n=n, mode=MIX, scale=0.5, final=True)
+    to, tl, _, _, _ = _torch_causal(qf, kt, vt, np.zeros_like(qf), 0.5)
+    np.testing.assert_allclose(o, to, atol=1e-12)
+    np.testing.assert_allclose(lse, tl + math.log(n), atol=1e-12)
+
+
+@pytest.mark.parametrize("mode,w", [(MIX, 0), (LOCAL, 4)])
+def test_final_stream_finite_differences(oracle_mod, mode, w):
+    B, L, n, Hq, Hkv, D = 1, 4, 3, 2, 1, 4
+    r = np.random.default_rng(36)
+    qf = r.standard_normal((B, L, Hq, D))
+    k = r.standard_normal((B, n * L, Hkv, D))
+    v = r.standard_normal((B, n * L, Hkv, D))
+    dof = r.standard_normal((B, L, Hq, D))
+    kw = dict(L=L, n=n, mode=mode, scale=0.5, window=w, final=True)
+    grads = oracle_mod.sfa_bwd(qf, k, v, dof, **kw)
+
+    def f(qq, kk, vv):
+        return float((dof * oracle_mod.sfa_fwd(qq, kk, vv, nthreads=1, **kw)[0]).sum())
+
+    h = 1e-6
+    for idx, g in enumerate(grads):
+        x = [qf, k, v][idx]
+        gmax = max(np.abs(g).max(), 1.0)
+        for e in range(x.size):
+            args = [qf.copy(), k.copy(), v.copy()]
+            args[idx].flat[e] += h
+            fp = f(*args)
+            args[idx].flat[e] -= 2 * h
+            fd = (fp - f(*args)) / (2 * h)
+            assert abs(fd - g.flat[e]) <= 1e-6 * gmax, ("qkv"[idx], e)
+
+
+def test_final_stream_rows_equal_full(oracle_mod):
+    B, L, n, Hq, Hkv, D = 2, 6, 3, 4, 2, 5
+    r = np.random.default_rng(37)
+    qf = r.standard_normal((B, L, Hq, D))
+    k = r.standard_normal((B, n * L, Hkv, D))
+    v = r.standard_normal((B, n * L, Hkv, D))
+    dof = r.standard_normal((B, L, Hq, D))
+    kw = dict(L=L, n=n, mode=LOCAL, scale=0.6, window=7, final=True)
+    o, lse = oracle_mod.sfa_fwd(qf, k, v, **kw)
+    dq, dk, dv = oracle_mod.sfa_bwd(qf, k, v, dof, **kw)
+    rows = np.array([[0, 0, 0], [1, 3, 5], [0, 2, 3]])
+    ro, rl = oracle_mod.sfa_fwd_rows(qf, k, v, rows, **kw)
+    rdq = oracle_mod.sfa_bwd_dq_rows(qf, k, v, dof, rows, **kw)
+    for i, (b, h, t) in enumerate(rows):
+        np.testing.assert_allclose(ro[i], o[b, t, h], atol=1e-13)
+        assert abs(rl[i] - lse[b, h, t]) < 1e-13
+        np.testing.assert_allclose(rdq[i], dq[b, t, h], atol=1e-13)
+    krows = np.array([[0, 0, 0], [1, 1, 17], [0, 1, 10]])
+    rdk, rdv = oracle_mod.sfa_bwd_dkdv_rows(qf, k, v, dof, krows, **kw)
+    for i, (b, h, j) in enumerate(krows):
+        np.testing.assert_allclose(rdk[i], dk[b, j, h], atol=1e-13)
+        np.testing.assert_allclose(rdv[i], dv[b, j, h], atol=1e-13)
