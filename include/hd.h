@@ -218,6 +218,40 @@ hd_status_t hd_sfa_bwd_local(const void *q, const void *k, const void *v, const 
                              float scale, hd_dtype_t dtype, void *workspace,
                              size_t workspace_bytes, hd_stream_t stream);
 
+/*
+ * Final-stream layers (Sec. "Training Cost", KV-mirror): in the mirrored layers only the
+ * final stream of each token is run, while keys and values cover all n streams (they
+ * come from an earlier layer).  Query row t of these layers sits at expanded position
+ * t*n + n - 1 and sees, with window == 0, every key p' <= t*n + n - 1 (the full
+ * cross-stream mask of HD_SFA_MIX), or with window >= 1 the keys
+ * t*n + n - 1 - window < p' <= t*n + n - 1 (the local mask of HD_SFA_LOCAL).  An
+ * intra-stream mirrored layer needs no entry point of its own: it is plain causal
+ * attention over the final-stream rows.
+ *
+ * hd_sfa_fwd_final
+ *   q, o   device [B][L][Hq][D] bf16 (final-stream rows only).
+ *   k, v   device [B][n*L][Hkv][D] bf16, all expanded rows.
+ *   lse    device float [B][Hq][L], natural log.
+ * hd_sfa_bwd_final
+ *   dO, dq device [B][L][Hq][D];  dk, dv  device [B][n*L][Hkv][D] (summed over the query
+ *   heads of each group; keys that no final-stream query sees get zero);
+ *   workspace of at least hd_sfa_bwd_final_workspace_bytes(...) bytes (the two row
+ *   statistics per query row and the bf16 dS tiles: 16 KB per 64 query rows x 128 keys
+ *   of a key band, about 2*B*Hq*L*n*L bytes without a window).
+ * Other arguments, conventions and errors as hd_sfa_fwd / hd_sfa_bwd, plus INVALID_ARG
+ * for window < 0 and UNSUPPORTED for dtype HD_DTYPE_F32 or n > 63.
+ */
+hd_status_t hd_sfa_fwd_final(const void *q, const void *k, const void *v, void *o, float *lse,
+                             int B, int L, int n, int Hq, int Hkv, int D, int window,
+                             float scale, hd_dtype_t dtype, hd_stream_t stream);
+size_t hd_sfa_bwd_final_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D, int window,
+                                        hd_dtype_t dtype);
+hd_status_t hd_sfa_bwd_final(const void *q, const void *k, const void *v, const void *o,
+                             const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                             int B, int L, int n, int Hq, int Hkv, int D, int window,
+                             float scale, hd_dtype_t dtype, void *workspace,
+                             size_t workspace_bytes, hd_stream_t stream);
+
 /* Static name of a status code ("HD_OK", ...). */
 const char *hd_status_str(hd_status_t s);
 

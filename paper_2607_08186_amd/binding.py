@@ -19,7 +19,8 @@ HD_DTYPE_BF16, HD_DTYPE_F32 = 0, 1
 
 # every symbol include/hd.h declares
 EXPORTS = ("hd_expand_embed", "hd_expand_embed_bwd_workspace_bytes", "hd_expand_embed_bwd",
-           "hd_embed_grad_scatter_add", "hd_cyclic_replicate", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
+           "hd_embed_grad_scatter_add", "hd_cyclic_replicate", "hd_sfa_fwd_final",
+           "hd_sfa_bwd_final_workspace_bytes", "hd_sfa_bwd_final", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
            "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
            "hd_timing_enable", "hd_timing_collect")
 
@@ -62,13 +63,18 @@ def lib() -> ctypes.CDLL:
     # the *_local variants take the window where the others take the mode
     L.hd_sfa_fwd_local.argtypes = L.hd_sfa_fwd.argtypes
     L.hd_sfa_bwd_local.argtypes = L.hd_sfa_bwd.argtypes
+    L.hd_sfa_fwd_final.argtypes = L.hd_sfa_fwd.argtypes
+    L.hd_sfa_bwd_final.argtypes = L.hd_sfa_bwd.argtypes
+    L.hd_sfa_bwd_final_workspace_bytes.argtypes = [i32] * 8
+    L.hd_sfa_bwd_final_workspace_bytes.restype = sz
     L.hd_expand_embed_bwd_workspace_bytes.argtypes = [i32, i32]
     L.hd_expand_embed_bwd_workspace_bytes.restype = sz
     L.hd_expand_embed_bwd.argtypes = [vp, vp, i32, i32, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp]
     L.hd_embed_grad_scatter_add.argtypes = [vp, vp, vp, i32, i32, i64, i32, vp, vp]
     L.hd_cyclic_replicate.argtypes = [vp, vp, i32, i32, i64, i32, i32, vp]
     for f in (L.hd_expand_embed, L.hd_expand_embed_bwd, L.hd_embed_grad_scatter_add,
-              L.hd_cyclic_replicate, L.hd_sfa_fwd, L.hd_sfa_fwd_local, L.hd_sfa_bwd,
+              L.hd_cyclic_replicate, L.hd_sfa_fwd_final, L.hd_sfa_bwd_final, L.hd_sfa_fwd,
+              L.hd_sfa_fwd_local, L.hd_sfa_bwd,
               L.hd_sfa_bwd_local, L.hd_timing_enable):
         f.restype = i32
     L.hd_status_str.argtypes = [i32]
@@ -186,6 +192,25 @@ def hd_sfa_bwd_local(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, windo
                                   int(workspace_bytes), _stream(stream)))
 
 
+def hd_sfa_fwd_final(q, k, v, o, lse, B, L, n, Hq, Hkv, D, window, scale, dtype=None,
+                     stream=None):
+    _check(lib().hd_sfa_fwd_final(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), B, L, n, Hq,
+                                  Hkv, D, int(window), float(scale), _dtype_code(q, dtype),
+                                  _stream(stream)))
+
+
+def hd_sfa_bwd_final_workspace_bytes(B, L, n, Hq, Hkv, D, window, dtype) -> int:
+    return int(lib().hd_sfa_bwd_final_workspace_bytes(B, L, n, Hq, Hkv, D, int(window), int(dtype)))
+
+
+def hd_sfa_bwd_final(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, window, scale,
+                     workspace, workspace_bytes, dtype=None, stream=None):
+    _check(lib().hd_sfa_bwd_final(_ptr(q), _ptr(k), _ptr(v), _ptr(o), _ptr(lse), _ptr(dO),
+                                  _ptr(dq), _ptr(dk), _ptr(dv), B, L, n, Hq, Hkv, D, int(window),
+                                  float(scale), _dtype_code(q, dtype), _ptr(workspace),
+                                  workspace_bytes, _stream(stream)))
+
+
 def hd_timing_enable(enable: bool):
     _check(lib().hd_timing_enable(1 if enable else 0))
 
@@ -300,3 +325,36 @@ def cyclic_replicate(tables, m, *, stream=None):
     out = torch.empty((m, V, Dm), dtype=tables.dtype, device=tables.device)
     hd_cyclic_replicate(tables, out, n, m, V, Dm, stream=stream)
     return out
+
+
+def sfa_final_forward(q, k, v, *, n, window=0, scale=None, stream=None):
+    """Final-stream layer: q [B][L][Hq][D] (final-stream rows), k/v [B][n*L][Hkv][D] ->
+    (o [B][L][Hq][D], lse [B][Hq][L] fp32).  window 0: full cross-stream mask."""
+    import torch
+
+    B, L, Hq, D = q.shape
+    Hkv = k.shape[2]
+    if k.shape[1] != n * L:
+        raise ValueError("k/v must hold n*L expanded rows")
+    scale = scale if scale is not None else D ** -0.5
+    o = torch.empty_like(q)
+    lse = torch.empty((B, Hq, L), dtype=torch.float32, device=q.device)
+    hd_sfa_fwd_final(q, k, v, o, lse, B, L, n, Hq, Hkv, D, window, scale, stream=stream)
+    return o, lse
+
+
+def sfa_final_backward(q, k, v, o, lse, dO, *, n, window=0, scale=None, workspace=None,
+                       stream=None):
+    """-> (dq [B][L][Hq][D], dk, dv [B][n*L][Hkv][D])."""
+    import torch
+
+    B, L, Hq, D = q.shape
+    Hkv = k.shape[2]
+    scale = scale if scale is not None else D ** -0.5
+    need = hd_sfa_bwd_final_workspace_bytes(B, L, n, Hq, Hkv, D, window, _dtype_code(q, None))
+    if workspace is None:
+        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+    dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
+    hd_sfa_bwd_final(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, window, scale,
+                     workspace, workspace.numel(), stream=stream)
+    return dq, dk, dv

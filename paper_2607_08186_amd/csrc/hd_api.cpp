@@ -243,16 +243,35 @@ hd_status_t hd_cyclic_replicate(const void *src, void *dst, int n, int m, int64_
 
 namespace {
 
+// Final-stream layers (queries at the final stream of each token only): bf16 kernels,
+// and at most 63 streams (the forward's eight waves then all reach the last key tile
+// of their 256-row block).
+hd_status_t check_final(int n, hd_dtype_t dtype)
+{
+    if (dtype != HD_DTYPE_BF16)
+        return fail(HD_ERR_UNSUPPORTED, "final-stream layers are implemented for bf16 only");
+    if (n > 63) return fail(HD_ERR_UNSUPPORTED, "final-stream layers support n <= 63 (got %d)", n);
+    return HD_OK;
+}
+
+hd::SfaGeom geom(int B, int L, int n, int Hq, int Hkv, int D, int mode, float scale, int window,
+                 bool final_q)
+{
+    return final_q ? hd::make_geom_final(B, L, n, Hq, Hkv, D, mode, scale, window)
+                   : hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale, window);
+}
+
 hd_status_t sfa_fwd(const void *q, const void *k, const void *v, void *o, float *lse, int B, int L,
                     int n, int Hq, int Hkv, int D, int mode, int window, float scale,
-                    hd_dtype_t dtype, hd_stream_t stream)
+                    hd_dtype_t dtype, hd_stream_t stream, bool final_q = false)
 {
     if (!q || !k || !v || !o || !lse) return fail(HD_ERR_INVALID_ARG, "null tensor pointer");
     hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, scale, dtype);
     if (st != HD_OK) return st;
+    if (final_q && (st = check_final(n, dtype)) != HD_OK) return st;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse))
         return fail(HD_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
-    const hd::SfaGeom g = hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale, window);
+    const hd::SfaGeom g = geom(B, L, n, Hq, Hkv, D, mode, scale, window, final_q);
     hipError_t e;
     if (dtype == HD_DTYPE_BF16)
         e = hd::launch_fwd_bf16(q, k, v, o, lse, g, (hipStream_t)stream);
@@ -317,16 +336,18 @@ namespace {
 hd_status_t sfa_bwd(const void *q, const void *k, const void *v, const void *o, const float *lse,
                     const void *dO, void *dq, void *dk, void *dv, int B, int L, int n, int Hq,
                     int Hkv, int D, int mode, int window, float scale, hd_dtype_t dtype,
-                    void *workspace, size_t workspace_bytes, hd_stream_t stream)
+                    void *workspace, size_t workspace_bytes, hd_stream_t stream,
+                    bool final_q = false)
 {
     if (!q || !k || !v || !o || !lse || !dO || !dq || !dk || !dv)
         return fail(HD_ERR_INVALID_ARG, "null tensor pointer");
     hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, scale, dtype);
     if (st != HD_OK) return st;
+    if (final_q && (st = check_final(n, dtype)) != HD_OK) return st;
     if (!aligned16(q) || !aligned16(k) || !aligned16(v) || !aligned16(o) || !aligned16(lse) ||
         !aligned16(dO) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
         return fail(HD_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
-    const hd::SfaGeom g = hd::make_geom(B, L, n, Hq, Hkv, D, mode, scale, window);
+    const hd::SfaGeom g = geom(B, L, n, Hq, Hkv, D, mode, scale, window, final_q);
     const size_t need = hd::bwd_workspace_bytes(g, dtype == HD_DTYPE_BF16 ? 2 : 4);
     if (!workspace) return fail(HD_ERR_INVALID_ARG, "null workspace (%zu bytes needed)", need);
     if (reinterpret_cast<uintptr_t>(workspace) & 255)
@@ -372,6 +393,42 @@ hd_status_t hd_sfa_bwd_local(const void *q, const void *k, const void *v, const 
     if (window < 1) return fail(HD_ERR_INVALID_ARG, "window must be >= 1 (got %d)", window);
     return sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, HD_SFA_LOCAL, window,
                    scale, dtype, workspace, workspace_bytes, stream);
+}
+
+hd_status_t hd_sfa_fwd_final(const void *q, const void *k, const void *v, void *o, float *lse,
+                             int B, int L, int n, int Hq, int Hkv, int D, int window, float scale,
+                             hd_dtype_t dtype, hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (window < 0) return fail(HD_ERR_INVALID_ARG, "window must be >= 0 (got %d)", window);
+    return sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, window ? HD_SFA_LOCAL : HD_SFA_MIX,
+                   window, scale, dtype, stream, true);
+}
+
+size_t hd_sfa_bwd_final_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D, int window,
+                                        hd_dtype_t dtype)
+{
+    char saved[sizeof g_err];
+    memcpy(saved, g_err, sizeof g_err);
+    const int mode = window ? HD_SFA_LOCAL : HD_SFA_MIX;
+    hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, 1.0f, dtype);
+    if (st == HD_OK) st = check_final(n, dtype);
+    memcpy(g_err, saved, sizeof g_err);
+    if (st != HD_OK || window < 0) return 0;
+    return hd::bwd_workspace_bytes(hd::make_geom_final(B, L, n, Hq, Hkv, D, mode, 1.0f, window), 2);
+}
+
+hd_status_t hd_sfa_bwd_final(const void *q, const void *k, const void *v, const void *o,
+                             const float *lse, const void *dO, void *dq, void *dk, void *dv,
+                             int B, int L, int n, int Hq, int Hkv, int D, int window, float scale,
+                             hd_dtype_t dtype, void *workspace, size_t workspace_bytes,
+                             hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (window < 0) return fail(HD_ERR_INVALID_ARG, "window must be >= 0 (got %d)", window);
+    return sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D,
+                   window ? HD_SFA_LOCAL : HD_SFA_MIX, window, scale, dtype, workspace,
+                   workspace_bytes, stream, true);
 }
 
 hd_status_t hd_timing_enable(int enable)

@@ -16,12 +16,20 @@ struct SfaGeom {
     int B, L, n, Hq, Hkv, D, G;  // G = Hq / Hkv
     int N;                       // n * L
     int mode;                    // 0 intra, 1 mix (full cross-stream), 2 local cross-stream
-    int len;                     // rows per problem
+    int len;                     // key rows per problem
     int rowmul;                  // n (intra) or 1 (mix, local)
     int streams;                 // n (intra) or 1 (mix, local): problems per head
     int window;                  // local: row p sees keys p-window+1 .. p; else a huge value
     float scale;                 // softmax scale
     float scale_log2;            // scale * log2(e)
+    // Query side.  Query row i of a problem sits at key coordinate P(i) = i*qpmul + qpoff
+    // for the mask (key j visible iff j <= P(i) and P(i) - j < window).  Every layer
+    // but the final-stream one has one query row per key row: P(i) = i.
+    int qlen;                    // query rows per problem
+    int qN;                      // rows of q, o, dO, dq per batch ([B][qN][Hq][D]); lse [B][Hq][qN]
+    int qrowmul;                 // row stride of q, o, dO, dq in units of Hq*D
+    int qpmul, qpoff;
+    bool strided_waves;          // forward: wave w of a 256-row block takes rows w, w+8, ...
 };
 
 constexpr int kNoWindow = 1 << 30;
@@ -41,8 +49,33 @@ inline SfaGeom make_geom(int B, int L, int n, int Hq, int Hkv, int D, int mode, 
     g.window = mode == 2 ? window : kNoWindow;
     g.scale = scale;
     g.scale_log2 = scale * 1.4426950408889634f;
+    g.qlen = g.len;
+    g.qN = g.N;
+    g.qrowmul = g.rowmul;
+    g.qpmul = 1;
+    g.qpoff = 0;
+    g.strided_waves = false;
     return g;
 }
+
+// Final-stream layer (full cross-stream mode 1 or local mode 2): queries only at the
+// final stream of each token, q [B][L][Hq][D] with row t at expanded position
+// t*n + n - 1, keys and values over all N expanded rows.
+inline SfaGeom make_geom_final(int B, int L, int n, int Hq, int Hkv, int D, int mode, float scale,
+                               int window = 0)
+{
+    SfaGeom g = make_geom(B, L, n, Hq, Hkv, D, mode, scale, window);
+    g.qlen = L;
+    g.qN = L;
+    g.qrowmul = 1;
+    g.qpmul = n;
+    g.qpoff = n - 1;
+    g.strided_waves = true;
+    return g;
+}
+
+// key coordinate of query row i
+__host__ __device__ inline int qpos(const SfaGeom &g, int i) { return i * g.qpmul + g.qpoff; }
 
 // Launch wrappers record per-kernel timing events when timing is enabled.
 void timing_before(const char *name, hipStream_t s);
@@ -94,14 +127,21 @@ __host__ __device__ inline int64_t ds_tile_index(int band, int kt_lo, int qt, in
     return (int64_t)qt * band + (kt - kt_lo);
 }
 
-// Slots per query tile of a local layer, or 0 for triangular packing: used without a
-// window (or one >= len) and whenever the band would not be smaller, so the triangular
-// size bounds every window.
+// Slots per query tile, or 0 for triangular packing.  Layers with one query per key
+// (P(i) = i) pack triangularly without a window (or one >= len) and whenever a band
+// would not be smaller, so the triangular size bounds every window.  Final-stream
+// layers always use bands: query tile qt sees at most window + 63*qpmul consecutive
+// keys (all key tiles without a window).
 __host__ __device__ inline int ds_band(const SfaGeom &g)
 {
-    if (g.window >= g.len) return 0;
     const int nkt = (g.len + kDsKeys - 1) / kDsKeys;
-    const int nqt = (g.len + kDsRows - 1) / kDsRows;
+    const int nqt = (g.qlen + kDsRows - 1) / kDsRows;
+    if (g.qpmul != 1) {
+        const int64_t span = (int64_t)(g.window < g.len ? g.window : g.len) + 63 * g.qpmul;
+        const int64_t band = (span - 1 + kDsKeys - 1) / kDsKeys + 1;
+        return (int)(band < nkt ? band : nkt);
+    }
+    if (g.window >= g.len) return 0;
     int band = (g.window - 1 + kDsKeys - 1) / kDsKeys + 1;
     band = band < nkt ? band : nkt;
     return (int64_t)nqt * band < ds_tile_index(0, 0, nqt, 0) ? band : 0;
@@ -111,20 +151,20 @@ __host__ __device__ inline int ds_band(const SfaGeom &g)
 __host__ __device__ inline int ds_kt_lo(const SfaGeom &g, int qt)
 {
     if (g.window >= g.len) return 0;
-    const int first = qt * kDsRows - g.window + 1;
+    const int first = qpos(g, qt * kDsRows) - g.window + 1;
     return first > 0 ? first / kDsKeys : 0;
 }
 
 // dS tiles per causal problem
 inline int64_t ds_tiles_per_problem(const SfaGeom &g)
 {
-    const int nqt = (g.len + kDsRows - 1) / kDsRows;
+    const int nqt = (g.qlen + kDsRows - 1) / kDsRows;
     const int band = ds_band(g);
     return band == 0 ? ds_tile_index(0, 0, nqt, 0) : (int64_t)nqt * band;
 }
 
 // Backward workspace, each part 256-byte aligned:
-//   per-row statistics, fp32 [B][Hq][N] each: for fp32 those of
+//   per-row statistics, fp32 [B][Hq][qN] each: for fp32 those of
 //   launch_bwd_preprocess_f32, for bf16 -Delta and -lse/scale;
 //   bf16 path only: the dS tiles of every problem (b, hq[, s]), problem-major.
 struct BwdWorkspace {
@@ -137,7 +177,7 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 inline BwdWorkspace bwd_workspace(const SfaGeom &g, int esize)
 {
     BwdWorkspace w;
-    const size_t rows = (size_t)g.B * g.Hq * g.N;
+    const size_t rows = (size_t)g.B * g.Hq * g.qN;
     w.delta = 0;
     w.lse2 = align256(rows * 4);
     w.ds = w.lse2 + align256(rows * 4);

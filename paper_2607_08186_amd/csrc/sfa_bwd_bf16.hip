@@ -46,7 +46,7 @@ __global__ __launch_bounds__(256) void bwd_stats_bf16_kernel(const bf16 *__restr
                                                              float *__restrict__ nstat_l, SfaGeom g)
 {
     constexpr int LPR = D / 8;
-    const int64_t rows = (int64_t)g.B * g.N * g.Hq;
+    const int64_t rows = (int64_t)g.B * g.qN * g.Hq;
     const int64_t r = ((int64_t)blockIdx.x * 256 + threadIdx.x) / LPR;
     const int part = threadIdx.x % LPR;
     float acc = 0.f;
@@ -64,9 +64,9 @@ __global__ __launch_bounds__(256) void bwd_stats_bf16_kernel(const bf16 *__restr
     if (r < rows && part == 0) {
         const int hq = (int)(r % g.Hq);
         const int64_t bp = r / g.Hq;
-        const int p = (int)(bp % g.N);
-        const int b = (int)(bp / g.N);
-        const size_t li = ((size_t)b * g.Hq + hq) * g.N + p;
+        const int p = (int)(bp % g.qN);
+        const int b = (int)(bp / g.qN);
+        const size_t li = ((size_t)b * g.Hq + hq) * g.qN + p;
         nstat_d[li] = -acc;
         nstat_l[li] = -lse[li] / g.scale;
     }
@@ -95,8 +95,8 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const int hk = (prob / g.streams) % g.Hkv;
     const int b = prob / (g.streams * g.Hkv);
 
-    const size_t qslice = (size_t)g.N * g.Hq * D, kslice = (size_t)g.N * g.Hkv * D;
-    const size_t lslice = (size_t)g.Hq * g.N;
+    const size_t qslice = (size_t)g.qN * g.Hq * D, kslice = (size_t)g.N * g.Hkv * D;
+    const size_t lslice = (size_t)g.Hq * g.qN;
     const rsrc_t rq = make_rsrc(q + b * qslice, (uint32_t)(qslice * 2));
     const rsrc_t rdo = make_rsrc(dO + b * qslice, (uint32_t)(qslice * 2));
     const rsrc_t rk = make_rsrc(k + b * kslice, (uint32_t)(kslice * 2));
@@ -105,7 +105,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const rsrc_t rdv = make_rsrc(dv + b * kslice, (uint32_t)(kslice * 2));
     const rsrc_t rl2 = make_rsrc(lse2 + b * lslice, (uint32_t)(lslice * 4));
     const rsrc_t rdl = make_rsrc(delta + b * lslice, (uint32_t)(lslice * 4));
-    const uint32_t qstride = (uint32_t)g.rowmul * g.Hq * D * 2;
+    const uint32_t qstride = (uint32_t)g.qrowmul * g.Hq * D * 2;
     const uint32_t kstride = (uint32_t)g.rowmul * g.Hkv * D * 2;
     const uint32_t kbase = (uint32_t)(s * g.Hkv + hk) * D * 2;
 
@@ -123,12 +123,13 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     // to the one holding the first key.  Workgroups of one problem that run together
     // (decode_key_tile keeps a problem's key tiles on one XCD) then read the same Q/dO
     // tiles at about the same time, so most of those reads hit in L2.
-    const int qt_first = k0 / kRows;
+    // first query tile with a row that sees the first key (P(i) >= k0)
+    const int qt_first = max(0, (k0 - g.qpoff + g.qpmul - 1) / g.qpmul) / kRows;
     const int band = ds_band(g);
     // last query tile that sees a key of this workgroup: the end of the sequence, or for
-    // local layers the window's end past the last key
-    const int qt_end = (int)min((int64_t)(g.len + kRows - 1) / kRows,
-                                ((int64_t)k0 + kKeysPerWg - 2 + g.window) / kRows + 1);
+    // local layers the window's end past the last key (P(i) <= k0 + 126 + window)
+    const int qt_end = (int)min((int64_t)(g.qlen + kRows - 1) / kRows,
+                                ((int64_t)k0 + kKeysPerWg - 2 + g.window - g.qpoff) / g.qpmul / kRows + 1);
     const int nqt = qt_end - qt_first;
     const int iters = g.G * nqt;
 
@@ -156,12 +157,12 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
         const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
         const int row0 = qt * kRows;
         char *base = smem + st * STAGE;
-        T::load(base, rq, qbase, qstride, row0, g.len, wave, kDkdvWaves, lane);
-        T::load(base + T::BYTES, rdo, qbase, qstride, row0, g.len, wave, kDkdvWaves, lane);
+        T::load(base, rq, qbase, qstride, row0, g.qlen, wave, kDkdvWaves, lane);
+        T::load(base + T::BYTES, rdo, qbase, qstride, row0, g.qlen, wave, kDkdvWaves, lane);
         if (wave < 2) {  // per-row lse2 (wave 0) and delta (wave 1), 4 bytes per lane
             const int row = row0 + lane;
             const uint32_t off =
-                row < g.len ? (uint32_t)(((size_t)hq * g.N + (size_t)row * g.rowmul + s) * 4) : kOob;
+                row < g.qlen ? (uint32_t)(((size_t)hq * g.qN + (size_t)row * g.qrowmul + s) * 4) : kOob;
             dma_lds4(wave == 0 ? rl2 : rdl, base + 2 * T::BYTES + wave * kRows * 4, off);
         }
     };
@@ -188,7 +189,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                 const int r = rq * 4 + e;
                 float x = sacc[r];
                 if constexpr (kMask) {  // causal and, for local layers, windowed
-                    const int qd = qlo + 8 * rq + 4 * hi + e - key;  // query - key
+                    const int qd = qpos(g, qlo + 8 * rq + 4 * hi + e) - key;  // query - key
                     if (qd < 0 || qd >= g.window) x = -INFINITY;  // exp2 -> 0
                 }
                 p[e] = fast_exp2(x * c2);
@@ -216,7 +217,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
             kDsTileBytes);
         uint32_t dsw[8];
         // wave-uniform: some of my 32 queries see some of my keys
-        if (qlo + 31 >= kw0 && qlo - kw0 < 31 + g.window) {
+        if (qpos(g, qlo + 31) >= kw0 && qpos(g, qlo) - kw0 < 31 + g.window) {
             const char *qt = smem + st * STAGE;
             const char *dot = qt + T::BYTES;
             const float *sl = reinterpret_cast<const float *>(qt + 2 * T::BYTES) + qb * 32;
@@ -242,7 +243,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                               T::row_operand(vtl, krow, kk, hi), pacc);
             }
             uint32_t pw[8], dw[8];
-            if (qlo < kw0 + 31 || qlo + 31 - kw0 >= g.window)  // diagonal or window edge
+            if (qpos(g, qlo) < kw0 + 31 || qpos(g, qlo + 31) - kw0 >= g.window)  // diagonal or window edge
                 softmax(sacc, pacc, qlo, pw, dw, std::true_type{});
             else
                 softmax(sacc, pacc, qlo, pw, dw, std::false_type{});
@@ -341,7 +342,7 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     constexpr int kStage = T::BYTES + kDqWaves * kSlab;  // K rows | dS slabs
     __shared__ __attribute__((aligned(1024))) char smem[kStages][kStage];
 
-    const int ntiles = (g.len + kRowsPerWg - 1) / kRowsPerWg;
+    const int ntiles = (g.qlen + kRowsPerWg - 1) / kRowsPerWg;
     const int nprob = g.B * g.Hq * g.streams;
     int prob, tile;
     decode_tile(blockIdx.x, nprob, ntiles, prob, tile);
@@ -350,10 +351,10 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const int b = prob / (g.streams * g.Hq);
     const int hk = hq / g.G;
 
-    const size_t qslice = (size_t)g.N * g.Hq * D, kslice = (size_t)g.N * g.Hkv * D;
+    const size_t qslice = (size_t)g.qN * g.Hq * D, kslice = (size_t)g.N * g.Hkv * D;
     const rsrc_t rdq = make_rsrc(dq + b * qslice, (uint32_t)(qslice * 2));
     const rsrc_t rk = make_rsrc(k + b * kslice, (uint32_t)(kslice * 2));
-    const uint32_t qstride = (uint32_t)g.rowmul * g.Hq * D * 2;
+    const uint32_t qstride = (uint32_t)g.qrowmul * g.Hq * D * 2;
     const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
     const uint32_t kstride = (uint32_t)g.rowmul * g.Hkv * D * 2;
     const uint32_t kbase = (uint32_t)(s * g.Hkv + hk) * D * 2;
@@ -370,15 +371,17 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const int kt_lo = ds_kt_lo(g, qt);
     const bf16 *ds_prob = ds + (int64_t)prob * ds_tiles * (kDsTileBytes / 2);
 
-    const int kend = min(g.len, q0 + kRowsPerWg);
+    // keys of the block: up to the key coordinate of its last query row
+    const int kend = min(g.len, qpos(g, min(q0 + kRowsPerWg, g.qlen) - 1) + 1);
     const int nkt = (kend + kRows - 1) / kRows;
     // first key tile any row of the workgroup sees (0 unless the layer is local)
-    const int jf = max(0, q0 - g.window + 1) / kRows;
+    const int jf = max(0, qpos(g, q0) - g.window + 1) / kRows;
     // wave-uniform: 64-key tile j holds a key that a row of this wave sees (then the dS
     // tile that holds it exists)
     auto active = [&](int j) __attribute__((always_inline)) {
         const int kb0 = j * kRows;
-        return wrow_min < g.len && kb0 <= wrow_max && wrow_min - (kb0 + kRows - 1) < g.window;
+        return wrow_min < g.qlen && kb0 <= qpos(g, wrow_max) &&
+               qpos(g, wrow_min) - (kb0 + kRows - 1) < g.window;
     };
     const int kloads = loads_per_wave(T::INSTR, wave, kDqWaves);
     auto nloads = [&](int j) __attribute__((always_inline)) {
@@ -438,7 +441,7 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
         lds_barrier();
     }
 
-    if (row < g.len) {
+    if (row < g.qlen) {
         const uint32_t off = qbase + (uint32_t)row * qstride;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
@@ -459,7 +462,7 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o
                       hipStream_t s, const char *st_name, const char *dq_name,
                       const char *dkdv_name)
 {
-    const int64_t rows = (int64_t)g.B * g.N * g.Hq;
+    const int64_t rows = (int64_t)g.B * g.qN * g.Hq;
     timing_before(st_name, s);
     bwd_stats_bf16_kernel<D><<<(unsigned)((rows * (D / 8) + 255) / 256), 256, 0, s>>>(
         o, dO, lse, delta, lse2, g);
@@ -473,7 +476,7 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o
     e = hipGetLastError();
     timing_after(s);
     if (e != hipSuccess) return e;
-    const int nqt = (g.len + kRowsPerWg - 1) / kRowsPerWg;
+    const int nqt = (g.qlen + kRowsPerWg - 1) / kRowsPerWg;
     timing_before(dq_name, s);
     sfa_dq_bf16_kernel<D><<<nqt * g.B * g.Hq * g.streams, kDqWaves * 64, 0, s>>>(k, ds, dq, g,
                                                                                  ds_tiles);
@@ -497,14 +500,21 @@ hipError_t launch_bwd_bf16(const void *q, const void *k, const void *v, const vo
                *vv = static_cast<const bf16 *>(v), *dd = static_cast<const bf16 *>(dO),
                *oo = static_cast<const bf16 *>(o);
     bf16 *gq = static_cast<bf16 *>(dq), *gk = static_cast<bf16 *>(dk), *gv = static_cast<bf16 *>(dv);
+    const bool f = g.qpmul != 1;  // final-stream layer: tagged in the timing names
     if (g.D == 32)
         return bwd_bf16_d<32>(qq, kk, vv, oo, lse, dd, delta, lse2, ds, w.ds_tiles, gq, gk, gv, g,
-                              s, "sfa_bwd_stats_d32", "sfa_dq_bf16_d32", "sfa_dkdv_bf16_d32");
+                              s, f ? "sfa_bwd_final_stats_d32" : "sfa_bwd_stats_d32",
+                              f ? "sfa_dq_final_bf16_d32" : "sfa_dq_bf16_d32",
+                              f ? "sfa_dkdv_final_bf16_d32" : "sfa_dkdv_bf16_d32");
     if (g.D == 64)
         return bwd_bf16_d<64>(qq, kk, vv, oo, lse, dd, delta, lse2, ds, w.ds_tiles, gq, gk, gv, g,
-                              s, "sfa_bwd_stats_d64", "sfa_dq_bf16_d64", "sfa_dkdv_bf16_d64");
+                              s, f ? "sfa_bwd_final_stats_d64" : "sfa_bwd_stats_d64",
+                              f ? "sfa_dq_final_bf16_d64" : "sfa_dq_bf16_d64",
+                              f ? "sfa_dkdv_final_bf16_d64" : "sfa_dkdv_bf16_d64");
     return bwd_bf16_d<128>(qq, kk, vv, oo, lse, dd, delta, lse2, ds, w.ds_tiles, gq, gk, gv, g, s,
-                           "sfa_bwd_stats_d128", "sfa_dq_bf16_d128", "sfa_dkdv_bf16_d128");
+                           f ? "sfa_bwd_final_stats_d128" : "sfa_bwd_stats_d128",
+                           f ? "sfa_dq_final_bf16_d128" : "sfa_dq_bf16_d128",
+                           f ? "sfa_dkdv_final_bf16_d128" : "sfa_dkdv_bf16_d128");
 }
 
 }  // namespace hd

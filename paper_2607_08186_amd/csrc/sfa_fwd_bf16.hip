@@ -32,7 +32,9 @@ constexpr float kRescaleThreshold = 8.0f;  // log2 units
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
-template <int D>
+// FINAL: final-stream layer (query row i at key coordinate i*n + n - 1, strided wave
+// rows); otherwise query row i is key coordinate i and waves take consecutive rows.
+template <int D, bool FINAL>
 __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
     bf16 *__restrict__ o, float *__restrict__ lse, SfaGeom g)
@@ -45,7 +47,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     __shared__ __attribute__((aligned(1024))) char ks[2][T::BYTES];
     __shared__ __attribute__((aligned(1024))) char vs[2][T::BYTES];
 
-    const int ntiles = (g.len + kBM - 1) / kBM;
+    const int ntiles = (g.qlen + kBM - 1) / kBM;
     const int nprob = g.B * g.Hq * g.streams;
     int prob, tile;
     decode_tile(blockIdx.x, nprob, ntiles, prob, tile);
@@ -55,12 +57,12 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     const int hk = hq / g.G;
 
     // per-batch slices; all in-slice byte offsets fit in 31 bits
-    const size_t qslice = (size_t)g.N * g.Hq * D, kslice = (size_t)g.N * g.Hkv * D;
+    const size_t qslice = (size_t)g.qN * g.Hq * D, kslice = (size_t)g.N * g.Hkv * D;
     const rsrc_t rq = make_rsrc(q + b * qslice, (uint32_t)(qslice * 2));
     const rsrc_t rk = make_rsrc(k + b * kslice, (uint32_t)(kslice * 2));
     const rsrc_t rv = make_rsrc(v + b * kslice, (uint32_t)(kslice * 2));
     const rsrc_t ro = make_rsrc(o + b * qslice, (uint32_t)(qslice * 2));
-    const uint32_t qstride = (uint32_t)g.rowmul * g.Hq * D * 2;
+    const uint32_t qstride = (uint32_t)g.qrowmul * g.Hq * D * 2;
     const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
     const uint32_t kstride = (uint32_t)g.rowmul * g.Hkv * D * 2;
     const uint32_t kbase0 = (uint32_t)(s * g.Hkv + hk) * D * 2;
@@ -70,21 +72,28 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     const int group = wave >> 2;  // 0: A, 1: B (one wave of each per SIMD)
     const int l32 = lane & 31, hi = lane >> 5;
     const int q0 = tile * kBM;
-    const int row = q0 + wave * 32 + l32;
-    const int wrow_min = q0 + wave * 32, wrow_max = wrow_min + 31;
+    // This wave's 32 query rows: 32 consecutive rows, or, in final-stream layers (whose
+    // queries advance n key positions per row), rows wave, wave + 8, ... of the block,
+    // so that all eight waves reach (about) the same last key tile.
+    auto P = [&](int i) __attribute__((always_inline)) { return FINAL ? qpos(g, i) : i; };
+    const int row = FINAL ? q0 + wave + 8 * l32 : q0 + wave * 32 + l32;
+    const int wrow_min = FINAL ? q0 + wave : q0 + wave * 32;
+    const int wrow_max = FINAL ? wrow_min + 8 * 31 : wrow_min + 31;
 
-    const int kend = min(g.len, q0 + kBM);
+    // keys of the block: up to the key coordinate of its last query row
+    const int kend = min(g.len, P(min(q0 + kBM, g.qlen) - 1) + 1);
     const int nkt = (kend + kRows - 1) / kRows;
     // Tiles are numbered from jf, the first one holding a key that a row of this
     // workgroup sees (0 unless the layer is local); t below is relative to jf.
-    const int jf = max(0, q0 - g.window + 1) / kRows;
+    const int jf = max(0, P(q0) - g.window + 1) / kRows;
     const int ntl = nkt - jf;
-    const int jlast = min(nkt - 1, wrow_max / kRows) - jf;  // last tile with keys this wave sees
+    // last tile with keys this wave sees
+    const int jlast = min(nkt - 1, P(wrow_max) / kRows) - jf;
 
     // this lane's query row as the B operand of S^T = K Q^T
     bf16x8 qr[KS];
     {
-        const uint32_t off = row < g.len ? qbase + (uint32_t)row * qstride : kOob;
+        const uint32_t off = row < g.qlen ? qbase + (uint32_t)row * qstride : kOob;
 #pragma unroll
         for (int kk = 0; kk < KS; ++kk)
             qr[kk] = __builtin_bit_cast(bf16x8, ld16(rq, off + (kk * 16 + hi * 8) * 2));
@@ -122,7 +131,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     // keys at least a window before its last row
     auto needs_mask = [&](int t) __attribute__((always_inline)) {
         const int kb = (jf + t) * kRows;
-        return kb + kRows - 1 > wrow_min || kb <= wrow_max - g.window;
+        return kb + kRows - 1 > P(wrow_min) || kb <= P(wrow_max) - g.window;
     };
 
     // Matrix phase of tile t: the scores of tile t+1 (DO_S) and O^T += V^T P^T of
@@ -140,7 +149,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
                 // key = kb + c with c = mb*32 + 8*(r/4) + r%4 + 4*hi; masked if key > row
                 // or row - key >= window, compared against a per-lane limit so the
                 // per-element constants stay immediates
-                const int lim = row - 4 * hi - (jf + t + 1) * kRows;
+                const int lim = P(row) - 4 * hi - (jf + t + 1) * kRows;
                 const int lo = lim - g.window;
                 f32x16 bias[2];
 #pragma unroll
@@ -281,7 +290,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     while (nb < 2 * ntl + 2) bar();
 
     const float l = lsum0 + lsum1 + __shfl_xor(lsum0 + lsum1, 32);
-    if (row < g.len) {
+    if (row < g.qlen) {
         const float inv = 1.f / l;
         const uint32_t obase = qbase + (uint32_t)row * qstride;
 #pragma unroll
@@ -294,7 +303,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
                 st8(ro, obase + d0 * 2, w);
             }
         if (hi == 0) {
-            const size_t li = ((size_t)b * g.Hq + hq) * g.N + (size_t)row * g.rowmul + s;
+            const size_t li = ((size_t)b * g.Hq + hq) * g.qN + (size_t)row * g.qrowmul + s;
             lse[li] = (m2 + log2f(l)) * 0.6931471805599453f;
         }
     }
@@ -305,25 +314,25 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
 hipError_t launch_fwd_bf16(const void *q, const void *k, const void *v, void *o, float *lse,
                            const SfaGeom &g, hipStream_t s)
 {
-    const int ntiles = (g.len + kBM - 1) / kBM;
+    const int ntiles = (g.qlen + kBM - 1) / kBM;
     const int nprob = g.B * g.Hq * g.streams;
     const dim3 grid(ntiles * nprob), block(kWaves * 64);
     const bf16 *qq = static_cast<const bf16 *>(q), *kk = static_cast<const bf16 *>(k),
                *vv = static_cast<const bf16 *>(v);
     bf16 *oo = static_cast<bf16 *>(o);
+    auto launch = [&](auto dk, const char *name) {
+        constexpr int DD = decltype(dk)::value;
+        timing_before(name, s);
+        if (g.strided_waves)
+            sfa_fwd_bf16_kernel<DD, true><<<grid, block, 0, s>>>(qq, kk, vv, oo, lse, g);
+        else
+            sfa_fwd_bf16_kernel<DD, false><<<grid, block, 0, s>>>(qq, kk, vv, oo, lse, g);
+    };
+    const bool f = g.strided_waves;
     switch (g.D) {
-    case 32:
-        timing_before("sfa_fwd_bf16_d32", s);
-        sfa_fwd_bf16_kernel<32><<<grid, block, 0, s>>>(qq, kk, vv, oo, lse, g);
-        break;
-    case 64:
-        timing_before("sfa_fwd_bf16_d64", s);
-        sfa_fwd_bf16_kernel<64><<<grid, block, 0, s>>>(qq, kk, vv, oo, lse, g);
-        break;
-    default:
-        timing_before("sfa_fwd_bf16_d128", s);
-        sfa_fwd_bf16_kernel<128><<<grid, block, 0, s>>>(qq, kk, vv, oo, lse, g);
-        break;
+    case 32: launch(std::integral_constant<int, 32>{}, f ? "sfa_fwd_final_bf16_d32" : "sfa_fwd_bf16_d32"); break;
+    case 64: launch(std::integral_constant<int, 64>{}, f ? "sfa_fwd_final_bf16_d64" : "sfa_fwd_bf16_d64"); break;
+    default: launch(std::integral_constant<int, 128>{}, f ? "sfa_fwd_final_bf16_d128" : "sfa_fwd_bf16_d128"); break;
     }
     hipError_t e = hipGetLastError();
     timing_after(s);

@@ -255,6 +255,41 @@ def test_cyclic_replicate_validation(lib, args, code):
     assert st == code
 
 
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), INVALID), (dict(window=-1), INVALID), (dict(dtype=1), UNSUPPORTED),
+    (dict(n=64), UNSUPPORTED), (dict(D=48), UNSUPPORTED), (dict(Hkv=3), INVALID),
+])
+def test_final_validation(lib, kw, code):
+    a = dict(q=FAKE, B=1, L=8, n=2, Hq=4, Hkv=2, D=64, window=0, scale=0.125, dtype=0)
+    a.update(kw)
+    st = lib.hd_sfa_fwd_final(a["q"], FAKE, FAKE, FAKE, FAKE, a["B"], a["L"], a["n"], a["Hq"],
+                              a["Hkv"], a["D"], a["window"], a["scale"], a["dtype"], None)
+    assert st == code
+    need = lib.hd_sfa_bwd_final_workspace_bytes(a["B"], a["L"], a["n"], a["Hq"], a["Hkv"], a["D"],
+                                                a["window"], a["dtype"])
+    if a["q"] is not None:  # size and dtype errors make the workspace query return 0
+        assert (need == 0) == (code != 0)
+    st = lib.hd_sfa_bwd_final(a["q"], FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, a["B"],
+                              a["L"], a["n"], a["Hq"], a["Hkv"], a["D"], a["window"], a["scale"],
+                              a["dtype"], FAKE, max(need, 1 << 30), None)
+    assert st == code
+
+
+def test_final_workspace_sizes(lib):
+    """Row statistics per final-stream query row, plus bf16 dS tiles of 16 KB per 64
+    query rows x 128 keys: every key tile without a window, a band of
+    (w + 63 n - 1)/128 + 1 key tiles with one."""
+    B, L, n, Hq, Hkv, D = 1, 4096, 4, 32, 8, 128
+    stats = 2 * ((B * Hq * L * 4 + 255) // 256 * 256)
+    nqt, nkt = L // 64, n * L // 128
+    full = lib.hd_sfa_bwd_final_workspace_bytes(B, L, n, Hq, Hkv, D, 0, 0)
+    assert full == stats + B * Hq * nqt * nkt * 16384
+    w = 4096
+    band = (w + 63 * n - 1 + 127) // 128 + 1
+    local = lib.hd_sfa_bwd_final_workspace_bytes(B, L, n, Hq, Hkv, D, w, 0)
+    assert local == stats + B * Hq * nqt * band * 16384
+
+
 def test_missing_library_raises(monkeypatch, tmp_path):
     """No silent fallback: a missing libhd.so is an ImportError on first use."""
     monkeypatch.setattr(binding, "_lib", None)
