@@ -35,7 +35,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="stack36",
                     choices=["stack36"] + [f"{w}-{m}" for w in ("qwen8b", "frontier")
-                                           for m in ("intra", "mix", "local")]
+                                           for m in ("intra", "mix", "local", "final",
+                                                     "final-local")]
                     + [f"sweep-n{n}-{m}" for n in (1, 2, 4, 8) for m in ("intra", "mix", "local")])
     ap.add_argument("--window", type=int, default=None,
                     help="window of local layers in expanded positions "
@@ -59,11 +60,14 @@ def copy_calibration(nbytes):
     print(json.dumps({"copy_calibration_bytes": nbytes, "launches": 3}))
 
 
-def per_kernel_flops(shape, mode, window):
+def per_kernel_flops(shape, mode, window, final=False):
     """Algorithmic flop per kernel family for one layer (useful pairs only)."""
     from paper_2607_08186_amd import workloads as W
 
-    pairs = W.visible_pairs(shape, mode, window)
+    if final:
+        pairs = W.visible_pairs_final(shape, window if mode == W.LOCAL else 0)
+    else:
+        pairs = W.visible_pairs(shape, mode, window)
     D = shape.D
     # forward: S = QK^T and O = PV; dK/dV pass: S, dP, dV, dK; dQ pass: dQ only
     # (it recomputes S and dP, which the useful count does not credit twice)
@@ -118,8 +122,10 @@ def main():
                    "expand_embed backward")
         std = W.QWEN8B.qkv_std
         spike = None
+        final = False
     else:
-        parts = args.workload.split("-")
+        final = "final" in args.workload
+        parts = args.workload.replace("final-local", "local").replace("final", "mix").split("-")
         m = {"intra": W.INTRA, "mix": W.MIX, "local": W.LOCAL}[parts[-1]]
         if parts[0] == "qwen8b":
             wl = W.QWEN8B
@@ -129,6 +135,9 @@ def main():
             wl = {w.shape.n: w for w in W.SWEEP}[int(parts[1][1:])]
         shape, modes, with_embed = wl.shape, [m], False
         wl_desc = f"{wl.name} {W.MODE_NAMES[m]} fwd+bwd"
+        if final:
+            wl_desc = (f"{wl.name} final-stream {W.MODE_NAMES[m]} layer fwd+bwd (queries at "
+                       "the final stream of each token, keys over all n streams)")
         if m == W.LOCAL:
             wl_desc += f" (window {window} expanded positions)"
         std, spike = wl.qkv_std, wl.k_spike
@@ -141,10 +150,11 @@ def main():
     layers = []
     for li in range(nl):
         seed = synth.seed_for("bench", args.workload, li)
-        q = synth.device_normal((s.B, s.N, s.Hq, s.D), std, seed + 1, dev, torch.bfloat16)
+        qrows = s.L if final else s.N  # final-stream layers: one query row per token
+        q = synth.device_normal((s.B, qrows, s.Hq, s.D), std, seed + 1, dev, torch.bfloat16)
         k = synth.device_normal((s.B, s.N, s.Hkv, s.D), std, seed + 2, dev, torch.bfloat16)
         v = synth.device_normal((s.B, s.N, s.Hkv, s.D), std, seed + 3, dev, torch.bfloat16)
-        do = synth.device_normal((s.B, s.N, s.Hq, s.D), W.QWEN8B.dout_std, seed + 4, dev,
+        do = synth.device_normal((s.B, qrows, s.Hq, s.D), W.QWEN8B.dout_std, seed + 4, dev,
                                  torch.bfloat16)
         if spike is not None:  # scale a seeded 1% of K rows by 8 (exact in bf16)
             flat = k.view(-1, s.D)
@@ -154,13 +164,18 @@ def main():
                 :int(spike[0] * flat.shape[0])]
             flat[pick] *= spike[1]
         o = torch.empty_like(q)
-        lse = torch.empty((s.B, s.Hq, s.N), dtype=torch.float32, device=dev)
+        lse = torch.empty((s.B, s.Hq, qrows), dtype=torch.float32, device=dev)
         layers.append(dict(q=q, k=k, v=v, do=do, o=o, lse=lse, mode=modes[li]))
     dq = torch.empty_like(layers[0]["q"])
     dk = torch.empty_like(layers[0]["k"])
     dv = torch.empty_like(layers[0]["v"])
-    ws_bytes = max(hd.hd_sfa_bwd_workspace_bytes(s.B, s.L, s.n, s.Hq, s.Hkv, s.D, m,
-                                                 hd.HD_DTYPE_BF16) for m in set(modes))
+    if final:
+        ws_bytes = hd.hd_sfa_bwd_final_workspace_bytes(s.B, s.L, s.n, s.Hq, s.Hkv, s.D,
+                                                       window if W.LOCAL in modes else 0,
+                                                       hd.HD_DTYPE_BF16)
+    else:
+        ws_bytes = max(hd.hd_sfa_bwd_workspace_bytes(s.B, s.L, s.n, s.Hq, s.Hkv, s.D, m,
+                                                     hd.HD_DTYPE_BF16) for m in set(modes))
     ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
     if with_embed:
         ids = torch.randint(0, W.STACK_VOCAB, (1, s.L), dtype=torch.int32, device=dev,
@@ -184,14 +199,23 @@ def main():
             hd.hd_expand_embed(ids, tables, emb, 1, s.L, s.n, W.STACK_VOCAB, W.STACK_DMODEL,
                                stream=stream)
         for ly in layers:
-            if ly["mode"] == W.LOCAL:
+            if final:
+                hd.hd_sfa_fwd_final(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L, s.n,
+                                    s.Hq, s.Hkv, s.D, window if ly["mode"] == W.LOCAL else 0,
+                                    scale, stream=stream)
+            elif ly["mode"] == W.LOCAL:
                 hd.hd_sfa_fwd_local(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L,
                                     s.n, s.Hq, s.Hkv, s.D, window, scale, stream=stream)
             else:
                 hd.hd_sfa_fwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L, s.n,
                               s.Hq, s.Hkv, s.D, ly["mode"], scale, stream=stream)
         for ly in reversed(layers):
-            if ly["mode"] == W.LOCAL:
+            if final:
+                hd.hd_sfa_bwd_final(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq,
+                                    dk, dv, s.B, s.L, s.n, s.Hq, s.Hkv, s.D,
+                                    window if ly["mode"] == W.LOCAL else 0, scale, ws, ws_bytes,
+                                    stream=stream)
+            elif ly["mode"] == W.LOCAL:
                 hd.hd_sfa_bwd_local(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq,
                                     dk, dv, s.B, s.L, s.n, s.Hq, s.Hkv, s.D, window, scale, ws,
                                     ws_bytes, stream=stream)
@@ -219,14 +243,18 @@ def main():
     hd.hd_timing_enable(False)
     ktimes = hd.hd_timing_collect()
 
-    flop_step = sum(W.useful_flop(s, m, window=window) for m in modes)
+    if final:
+        flop_step = sum(14 * s.D * W.visible_pairs_final(s, window if m == W.LOCAL else 0)
+                        for m in modes)
+    else:
+        flop_step = sum(W.useful_flop(s, m, window=window) for m in modes)
     ms_per_step = elapsed * 1e3 / args.steps
     value = flop_step * args.steps / elapsed / 1e12
 
     # ------------------------------------------------------ per-kernel roofline
     fam_flops = {}
     for m in modes:
-        for fam, f in per_kernel_flops(s, m, window).items():
+        for fam, f in per_kernel_flops(s, m, window, final).items():
             fam_flops[fam] = fam_flops.get(fam, 0) + f
     per_kernel = []
     fam_ms = {}

@@ -251,3 +251,31 @@ def sfa_mask(L, n, mode, window=0):
     m = np.zeros((N, N), dtype=np.uint8)
     _load().oracle_sfa_mask(_ptr(m), L, n, int(mode), int(window))
     return m
+
+
+def sfa_decode(q, kcache, vcache, ctx, *, n, mode, scale, window=0, nthreads=None):
+    """Parallel-stream decode: the n streams of each sequence's new token attend to its
+    cached prefix.  q [B][n][Hq][D] (stream s of the new token of sequence b),
+    kcache/vcache [B][n*Lcap][Hkv][D] (expanded rows; the new token's own rows at
+    ctx[b]*n + s are already in the cache), ctx [B] tokens before the new one.
+    By definition this is the forward of the layer over the ctx[b] + 1 cached tokens,
+    read at the last token's n rows: returns o [B][n][Hq][D], lse [B][Hq][n] (fp64)."""
+    q = np.ascontiguousarray(q)
+    B, n_, Hq, D = q.shape
+    if n_ != n:
+        raise ValueError("q must be [B][n][Hq][D]")
+    o = np.zeros((B, n, Hq, D))
+    lse = np.zeros((B, Hq, n))
+    for b in range(B):
+        c = int(ctx[b])
+        L = c + 1
+        qf = np.zeros((1, n * L, Hq, D), dtype=q.dtype)
+        qf[0, c * n:(c + 1) * n] = q[b]
+        rows = np.array([(0, h, c * n + s) for s in range(n) for h in range(Hq)], np.int64)
+        ro, rl = sfa_fwd_rows(qf, np.ascontiguousarray(kcache[b:b + 1, :n * L]),
+                              np.ascontiguousarray(vcache[b:b + 1, :n * L]), rows, L=L, n=n,
+                              mode=mode, scale=scale, nthreads=nthreads, window=window)
+        for i, (_, h, p) in enumerate(rows):
+            o[b, p - c * n, h] = ro[i]
+            lse[b, h, p - c * n] = rl[i]
+    return o, lse

@@ -82,6 +82,16 @@ def visible_pairs(s: Shape, mode: int, window: int = LOCAL_WINDOW) -> int:
     return s.B * s.Hq * s.N * (s.N + 1) // 2
 
 
+def visible_pairs_final(s: Shape, window: int = 0) -> int:
+    """Visible pairs of a final-stream layer (queries at t*n + n - 1 only, keys over all
+    N rows): token t's query sees (t+1)*n keys, at most `window` of them when window > 0."""
+    full = s.n * s.L * (s.L + 1) // 2
+    if window <= 0:
+        return s.B * s.Hq * full
+    t0 = min(s.L, window // s.n)  # tokens whose whole prefix fits in the window
+    return s.B * s.Hq * (s.n * t0 * (t0 + 1) // 2 + (s.L - t0) * window)
+
+
 # useful flop per visible pair per head dim: fwd QK^T + PV; bwd recompute QK^T, dV, dP, dQ, dK
 FWD_FLOP_PER_PAIR_D = 4
 BWD_FLOP_PER_PAIR_D = 10

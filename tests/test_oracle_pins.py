@@ -736,3 +736,65 @@ def test_final_stream_rows_equal_full(oracle_mod):
     for i, (b, h, j) in enumerate(krows):
         np.testing.assert_allclose(rdk[i], dk[b, j, h], atol=1e-13)
         np.testing.assert_allclose(rdv[i], dv[b, j, h], atol=1e-13)
+
+
+# ------------------------------------------------------- parallel-stream decode
+
+
+@pytest.mark.parametrize("mode,w", [(MIX, 0), (INTRA, 0), (LOCAL, 6)])
+def test_decode_equals_library_last_rows(oracle_mod, mode, w):
+    """Decode of the new token's n streams == library attention over each sequence's
+    cached prefix (its own context length) read at the last n rows; intra-stream layers
+    compare with causal attention over the de-interleaved stream."""
+    B, Lcap, n, Hq, Hkv, D = 3, 9, 3, 4, 2, 5
+    r = np.random.default_rng(41 + mode)
+    ctx = np.array([0, 8, 4])
+    q = r.standard_normal((B, n, Hq, D))
+    kc = r.standard_normal((B, n * Lcap, Hkv, D))
+    vc = r.standard_normal((B, n * Lcap, Hkv, D))
+    o, lse = oracle_mod.sfa_decode(q, kc, vc, ctx, n=n, mode=mode, scale=0.6, window=w)
+    for b in range(B):
+        c = int(ctx[b])
+        S = n * (c + 1)
+        if mode == INTRA:
+            for s in range(n):
+                ks, vs = kc[b:b + 1, s:S:n], vc[b:b + 1, s:S:n]
+                qs = np.zeros((1, c + 1, Hq, D))
+                qs[0, c] = q[b, s]
+                to, tl, _, _, _ = _torch_causal(qs, ks, vs, np.zeros_like(qs), 0.6)
+                np.testing.assert_allclose(o[b, s], to[0, c], atol=1e-12)
+                np.testing.assert_allclose(lse[b, :, s], tl[0, :, c], atol=1e-12)
+            continue
+        qf = np.zeros((1, S, Hq, D))
+        qf[0, c * n:] = q[b]
+        keep = _band(S, w) if mode == LOCAL else _band(S, S)
+        to, tl, _, _, _ = _torch_masked(qf, kc[b:b + 1, :S], vc[b:b + 1, :S],
+                                        np.zeros_like(qf), 0.6, keep)
+        np.testing.assert_allclose(o[b], to[0, c * n:], atol=1e-12)
+        np.testing.assert_allclose(lse[b], tl[0, :, c * n:], atol=1e-12)
+
+
+def test_decode_ignores_cache_past_the_new_token_and_other_streams(oracle_mod):
+    """Rows past ctx*n + n - 1 are never read; intra-stream decode reads only its
+    stream's rows (poisoning the rest changes nothing)."""
+    B, Lcap, n, Hq, Hkv, D = 2, 7, 2, 2, 1, 4
+    r = np.random.default_rng(42)
+    ctx = np.array([3, 5])
+    q = r.standard_normal((B, n, Hq, D))
+    kc = r.standard_normal((B, n * Lcap, Hkv, D))
+    vc = r.standard_normal((B, n * Lcap, Hkv, D))
+    for mode in (MIX, INTRA):
+        o, lse = oracle_mod.sfa_decode(q, kc, vc, ctx, n=n, mode=mode, scale=0.5)
+        kp, vp = kc.copy(), vc.copy()
+        for b in range(B):
+            kp[b, (ctx[b] + 1) * n:] = 1e6
+            vp[b, (ctx[b] + 1) * n:] = np.nan
+        o2, lse2 = oracle_mod.sfa_decode(q, kp, vp, ctx, n=n, mode=mode, scale=0.5)
+        np.testing.assert_array_equal(o, o2)
+        np.testing.assert_array_equal(lse, lse2)
+    kp, vp = kc.copy(), vc.copy()
+    kp[:, 1::n], vp[:, 1::n] = 1e6, np.nan  # stream 1 poisoned: stream 0 unchanged
+    o, lse = oracle_mod.sfa_decode(q, kc, vc, ctx, n=n, mode=INTRA, scale=0.5)
+    o2, lse2 = oracle_mod.sfa_decode(q, kp, vp, ctx, n=n, mode=INTRA, scale=0.5)
+    np.testing.assert_array_equal(o[:, 0], o2[:, 0])
+    np.testing.assert_array_equal(lse[:, :, 0], lse2[:, :, 0])
