@@ -37,7 +37,8 @@ def parse():
                     choices=["stack36"] + [f"{w}-{m}" for w in ("qwen8b", "frontier")
                                            for m in ("intra", "mix", "local", "final",
                                                      "final-local")]
-                    + [f"sweep-n{n}-{m}" for n in (1, 2, 4, 8) for m in ("intra", "mix", "local")])
+                    + [f"sweep-n{n}-{m}" for n in (1, 2, 4, 8) for m in ("intra", "mix", "local")]
+                    + ["decode-stack36", "decode-intra", "decode-mix", "decode-local"])
     ap.add_argument("--window", type=int, default=None,
                     help="window of local layers in expanded positions "
                          "(default: the workloads' 4096)")
@@ -92,6 +93,9 @@ def main():
 
     if args.copy_calibration:
         copy_calibration(args.copy_calibration)
+        return
+    if args.workload.startswith("decode"):
+        run_decode(args)
         return
 
     import torch
@@ -309,6 +313,105 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(args.cpu_sample_tokens)
+    print(json.dumps(out), flush=True)
+
+
+DECODE_BATCH = 16  # sequences decoded together
+
+
+def run_decode(args):
+    """One parallel-stream decode step: for each layer, the n streams of every sequence's
+    new token against that layer's KV cache (all sequences at a full 4096-token context,
+    Qwen3-8B-like heads).  value = GB/s of cache rows read (each cached key/value row of a
+    layer is read once per step, whatever the layer type)."""
+    import torch
+
+    import paper_2607_08186_amd as hd
+    from paper_2607_08186_amd import synth
+    from paper_2607_08186_amd import workloads as W
+
+    if not os.path.exists(hd.binding.LIB_PATH):
+        from paper_2607_08186_amd import build as hip_build
+
+        hip_build.build()
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    s = W.QWEN8B.shape
+    B, Lcap, n = DECODE_BATCH, s.L, s.n
+    window = args.window if args.window is not None else W.LOCAL_WINDOW
+    kind = args.workload.split("-")[1]
+    modes = (W.stack_modes() if kind == "stack36" else
+             [{"intra": W.INTRA, "mix": W.MIX, "local": W.LOCAL}[kind]])
+    ctx_len = Lcap - 1
+    ctx = torch.full((B,), ctx_len, dtype=torch.int32, device=dev)
+    t_gen = time.time()
+    layers = []
+    for li, m in enumerate(modes):
+        seed = synth.seed_for("decode-bench", li)
+        layers.append(dict(
+            mode=m,
+            q=synth.device_normal((B, n, s.Hq, s.D), W.QWEN8B.qkv_std, seed + 1, dev, torch.bfloat16),
+            k=synth.device_normal((B, n * Lcap, s.Hkv, s.D), W.QWEN8B.qkv_std, seed + 2, dev,
+                                  torch.bfloat16),
+            v=synth.device_normal((B, n * Lcap, s.Hkv, s.D), W.QWEN8B.qkv_std, seed + 3, dev,
+                                  torch.bfloat16),
+            o=torch.empty((B, n, s.Hq, s.D), dtype=torch.bfloat16, device=dev),
+            lse=torch.empty((B, s.Hq, n), dtype=torch.float32, device=dev)))
+    ws_bytes = max(hd.hd_sfa_decode_workspace_bytes(B, Lcap, n, s.Hq, s.Hkv, s.D, m, window,
+                                                    ctx_len) for m in set(modes))
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+    torch.cuda.synchronize()
+    t_gen = time.time() - t_gen
+
+    def step():
+        for ly in layers:
+            hd.hd_sfa_decode(ly["q"], ly["k"], ly["v"], ctx, ctx_len, ly["o"], ly["lse"], B, Lcap,
+                             n, s.Hq, s.Hkv, s.D, ly["mode"], window, s.scale, ws, ws_bytes,
+                             stream=stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    hd.hd_timing_enable(True)
+    hd.hd_timing_collect()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    hd.hd_timing_enable(False)
+    ktimes = hd.hd_timing_collect()
+
+    def cache_bytes(m):
+        rows = (ctx_len + 1) * n
+        if m == W.LOCAL:
+            rows = min(rows, window + n - 1)  # the last window positions of the n queries
+        return B * rows * s.Hkv * s.D * 2 * 2
+    bytes_step = sum(cache_bytes(m) for m in modes)
+    ms_step = elapsed * 1e3 / args.steps
+    value = bytes_step * args.steps / elapsed / 1e9
+    per_kernel = [{"kernel": name, "launches": nl, "avg_ms": round(ms / nl, 5),
+                   "share": round(ms / (elapsed * 1e3), 4)} for name, nl, ms in ktimes]
+    dom = max(ktimes, key=lambda r: r[2])
+    avg_ms = dom[2] / dom[1]
+    per_launch = bytes_step * args.steps / dom[1] if "partial" in dom[0] or "decode_bf16" in dom[0] else None
+    roofline = {"kernel": dom[0], "bound": "hbm", "unit": "GB/s", "peak": W.MI355X_HBM_PEAK_GBS,
+                "achieved": round(per_launch / (avg_ms * 1e-3) / 1e9, 1) if per_launch else None,
+                "frac": round(per_launch / (avg_ms * 1e-3) / 1e9 / W.MI355X_HBM_PEAK_GBS, 4)
+                if per_launch else None,
+                "traffic": None, "bytes_per_launch": per_launch, "avg_launch_ms": round(avg_ms, 5)}
+    out = {
+        "metric": "SFA parallel-stream decode KV-cache read GB/s", "value": round(value, 1),
+        "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic (seeded device normal draws)",
+        "config": {"workload": f"{args.workload}: {DECODE_BATCH} sequences x {ctx_len + 1} "
+                               f"tokens in cache, n={n} Hq={s.Hq} Hkv={s.Hkv} D={s.D}, "
+                               f"{len(modes)} layer(s)",
+                   "layers": len(modes), **({"window": window} if W.LOCAL in modes else {})},
+        "roofline": roofline, "per_kernel": per_kernel, "input_gen_s": round(t_gen, 2),
+    }
     print(json.dumps(out), flush=True)
 
 

@@ -252,6 +252,38 @@ hd_status_t hd_sfa_bwd_final(const void *q, const void *k, const void *v, const 
                              float scale, hd_dtype_t dtype, void *workspace,
                              size_t workspace_bytes, hd_stream_t stream);
 
+/*
+ * hd_sfa_decode -- parallel-stream decode (Sec. "Serving Cost": at a decode step the n
+ * streams of a sequence's new token are processed together).  For every sequence b with
+ * ctx_tokens[b] = c tokens before the new one, query row s (stream s of the new token,
+ * expanded position c*n + s) attends under `mode`'s mask to the sequence's cached rows:
+ *   HD_SFA_INTRA: rows t*n + s for t <= c (its own stream: 1/n of the cache);
+ *   HD_SFA_MIX  : rows p' <= c*n + s;
+ *   HD_SFA_LOCAL: rows c*n + s - window < p' <= c*n + s.
+ * The new token's own keys and values must already be in the cache (rows c*n .. c*n+n-1);
+ * rows past c*n + n - 1 are never read.  Forward only.
+ *
+ * q               device bf16 [B][n][Hq][D], the new token's n query rows per sequence.
+ * k_cache,v_cache device bf16 [B][n*Lcap][Hkv][D], expanded rows p = t*n + s (grouped
+ *                 heads as in hd_sfa_fwd).
+ * ctx_tokens      device int32 [B], each in [0, max_ctx_tokens].
+ * max_ctx_tokens  host bound on ctx_tokens (sizes the launch and the workspace), < Lcap.
+ * o               device bf16 [B][n][Hq][D];  lse  device float [B][Hq][n] (natural log).
+ * window          the local window (HD_SFA_LOCAL, >= 1); ignored by the other modes.
+ * workspace       device, 256-byte aligned, hd_sfa_decode_workspace_bytes(...) bytes:
+ *                 fp32 partial results per 256 cached rows.
+ * Errors: INVALID_ARG for null or misaligned pointers, sizes <= 0, Hq % Hkv != 0, a bad
+ *         mode, window or scale, max_ctx_tokens outside [0, Lcap), oversize tensors or a
+ *         short workspace; UNSUPPORTED for fp32 or D not in {32, 64, 128}.
+ */
+size_t hd_sfa_decode_workspace_bytes(int B, int Lcap, int n, int Hq, int Hkv, int D,
+                                     hd_sfa_mode_t mode, int window, int max_ctx_tokens);
+hd_status_t hd_sfa_decode(const void *q, const void *k_cache, const void *v_cache,
+                          const int32_t *ctx_tokens, int max_ctx_tokens, void *o, float *lse,
+                          int B, int Lcap, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode,
+                          int window, float scale, hd_dtype_t dtype, void *workspace,
+                          size_t workspace_bytes, hd_stream_t stream);
+
 /* Static name of a status code ("HD_OK", ...). */
 const char *hd_status_str(hd_status_t s);
 

@@ -20,7 +20,8 @@ HD_DTYPE_BF16, HD_DTYPE_F32 = 0, 1
 # every symbol include/hd.h declares
 EXPORTS = ("hd_expand_embed", "hd_expand_embed_bwd_workspace_bytes", "hd_expand_embed_bwd",
            "hd_embed_grad_scatter_add", "hd_cyclic_replicate", "hd_sfa_fwd_final",
-           "hd_sfa_bwd_final_workspace_bytes", "hd_sfa_bwd_final", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
+           "hd_sfa_bwd_final_workspace_bytes", "hd_sfa_bwd_final", "hd_sfa_decode_workspace_bytes",
+           "hd_sfa_decode", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
            "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
            "hd_timing_enable", "hd_timing_collect")
 
@@ -67,13 +68,17 @@ def lib() -> ctypes.CDLL:
     L.hd_sfa_bwd_final.argtypes = L.hd_sfa_bwd.argtypes
     L.hd_sfa_bwd_final_workspace_bytes.argtypes = [i32] * 8
     L.hd_sfa_bwd_final_workspace_bytes.restype = sz
+    L.hd_sfa_decode_workspace_bytes.argtypes = [i32] * 9
+    L.hd_sfa_decode_workspace_bytes.restype = sz
+    L.hd_sfa_decode.argtypes = [vp, vp, vp, vp, i32, vp, vp] + [i32] * 8 + [f32, i32, vp, sz, vp]
     L.hd_expand_embed_bwd_workspace_bytes.argtypes = [i32, i32]
     L.hd_expand_embed_bwd_workspace_bytes.restype = sz
     L.hd_expand_embed_bwd.argtypes = [vp, vp, i32, i32, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp]
     L.hd_embed_grad_scatter_add.argtypes = [vp, vp, vp, i32, i32, i64, i32, vp, vp]
     L.hd_cyclic_replicate.argtypes = [vp, vp, i32, i32, i64, i32, i32, vp]
     for f in (L.hd_expand_embed, L.hd_expand_embed_bwd, L.hd_embed_grad_scatter_add,
-              L.hd_cyclic_replicate, L.hd_sfa_fwd_final, L.hd_sfa_bwd_final, L.hd_sfa_fwd,
+              L.hd_cyclic_replicate, L.hd_sfa_fwd_final, L.hd_sfa_bwd_final, L.hd_sfa_decode,
+              L.hd_sfa_fwd,
               L.hd_sfa_fwd_local, L.hd_sfa_bwd,
               L.hd_sfa_bwd_local, L.hd_timing_enable):
         f.restype = i32
@@ -209,6 +214,19 @@ def hd_sfa_bwd_final(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, windo
                                   _ptr(dq), _ptr(dk), _ptr(dv), B, L, n, Hq, Hkv, D, int(window),
                                   float(scale), _dtype_code(q, dtype), _ptr(workspace),
                                   workspace_bytes, _stream(stream)))
+
+
+def hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, mode, window, max_ctx_tokens) -> int:
+    return int(lib().hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, int(mode), int(window),
+                                                   int(max_ctx_tokens)))
+
+
+def hd_sfa_decode(q, k_cache, v_cache, ctx_tokens, max_ctx_tokens, o, lse, B, Lcap, n, Hq, Hkv, D,
+                  mode, window, scale, workspace, workspace_bytes, dtype=None, stream=None):
+    _check(lib().hd_sfa_decode(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(ctx_tokens),
+                               int(max_ctx_tokens), _ptr(o), _ptr(lse), B, Lcap, n, Hq, Hkv, D,
+                               int(mode), int(window), float(scale), _dtype_code(q, dtype),
+                               _ptr(workspace), workspace_bytes, _stream(stream)))
 
 
 def hd_timing_enable(enable: bool):
@@ -358,3 +376,24 @@ def sfa_final_backward(q, k, v, o, lse, dO, *, n, window=0, scale=None, workspac
     hd_sfa_bwd_final(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, window, scale,
                      workspace, workspace.numel(), stream=stream)
     return dq, dk, dv
+
+
+def sfa_decode(q, k_cache, v_cache, ctx_tokens, *, max_ctx, mode, window=0, scale=None,
+               workspace=None, stream=None):
+    """Parallel-stream decode: q [B][n][Hq][D] (the new token's n streams), caches
+    [B][n*Lcap][Hkv][D], ctx_tokens [B] int32 (device) -> (o [B][n][Hq][D],
+    lse [B][Hq][n] fp32)."""
+    import torch
+
+    B, n, Hq, D = q.shape
+    Lcap = k_cache.shape[1] // n
+    Hkv = k_cache.shape[2]
+    scale = scale if scale is not None else D ** -0.5
+    need = hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, mode, window, max_ctx)
+    if workspace is None:
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)
+    o = torch.empty_like(q)
+    lse = torch.empty((B, Hq, n), dtype=torch.float32, device=q.device)
+    hd_sfa_decode(q, k_cache, v_cache, ctx_tokens, max_ctx, o, lse, B, Lcap, n, Hq, Hkv, D, mode,
+                  window, scale, workspace, workspace.numel(), stream=stream)
+    return o, lse

@@ -12,8 +12,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libhd.so")
 
 SOURCES = ["hd_api.cpp", "expand_embed.hip", "embed_bwd.hip", "sfa_fwd_bf16.hip", "sfa_bwd_bf16.hip",
-           "sfa_f32.hip"]
-HEADERS = ["hd_internal.h", "hd_device.h", "sfa_lds.h", "embed_internal.h"]
+           "sfa_f32.hip", "sfa_decode_bf16.hip"]
+HEADERS = ["hd_internal.h", "hd_device.h", "sfa_lds.h", "embed_internal.h", "decode_internal.h"]
 
 ARCH = "gfx950"
 # Packed fp32 VALU ops are kept off: plain fp32 code only.

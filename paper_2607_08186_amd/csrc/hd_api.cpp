@@ -14,6 +14,7 @@
 #include <vector>
 
 #include "../../include/hd.h"
+#include "decode_internal.h"
 #include "embed_internal.h"
 #include "hd_internal.h"
 
@@ -429,6 +430,79 @@ hd_status_t hd_sfa_bwd_final(const void *q, const void *k, const void *v, const 
     return sfa_bwd(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D,
                    window ? HD_SFA_LOCAL : HD_SFA_MIX, window, scale, dtype, workspace,
                    workspace_bytes, stream, true);
+}
+
+namespace {
+
+hd_status_t check_decode(int B, int Lcap, int n, int Hq, int Hkv, int D, int mode, int window,
+                         int max_ctx, hd_dtype_t dtype)
+{
+    if (B <= 0 || Lcap <= 0 || n <= 0 || Hq <= 0 || Hkv <= 0 || D <= 0)
+        return fail(HD_ERR_INVALID_ARG, "sizes must be positive (B=%d Lcap=%d n=%d Hq=%d Hkv=%d D=%d)",
+                    B, Lcap, n, Hq, Hkv, D);
+    if (Hq % Hkv != 0) return fail(HD_ERR_INVALID_ARG, "Hq=%d is not a multiple of Hkv=%d", Hq, Hkv);
+    if (mode != HD_SFA_INTRA && mode != HD_SFA_MIX && mode != HD_SFA_LOCAL)
+        return fail(HD_ERR_INVALID_ARG, "unknown mode %d", mode);
+    if (mode == HD_SFA_LOCAL && window < 1)
+        return fail(HD_ERR_INVALID_ARG, "local layers need window >= 1 (got %d)", window);
+    if (max_ctx < 0 || max_ctx >= Lcap)
+        return fail(HD_ERR_INVALID_ARG, "max_ctx_tokens=%d must lie in [0, Lcap-1=%d]", max_ctx,
+                    Lcap - 1);
+    if (dtype != HD_DTYPE_BF16 && dtype != HD_DTYPE_F32)
+        return fail(HD_ERR_INVALID_ARG, "unknown dtype %d", (int)dtype);
+    if (dtype != HD_DTYPE_BF16) return fail(HD_ERR_UNSUPPORTED, "decode is implemented for bf16 only");
+    if (D != 32 && D != 64 && D != 128)
+        return fail(HD_ERR_UNSUPPORTED, "head dim D=%d not supported (32, 64 or 128)", D);
+    if ((int64_t)n * Lcap * Hkv * D * 2 >= kSliceLimit || (int64_t)B * n * Hq * D * 2 >= kSliceLimit)
+        return fail(HD_ERR_INVALID_ARG, "a sequence's cache or the query tensor exceeds 2^31 bytes");
+    const hd::DecGeom g = hd::make_dec_geom(B, Lcap, n, Hq, Hkv, D, mode, window, 1.f, max_ctx);
+    if (g.problems > 65535) return fail(HD_ERR_INVALID_ARG, "too many decode problems (%d)", g.problems);
+    return HD_OK;
+}
+
+}  // namespace
+
+size_t hd_sfa_decode_workspace_bytes(int B, int Lcap, int n, int Hq, int Hkv, int D,
+                                     hd_sfa_mode_t mode, int window, int max_ctx_tokens)
+{
+    char saved[sizeof g_err];
+    memcpy(saved, g_err, sizeof g_err);
+    hd_status_t st = check_decode(B, Lcap, n, Hq, Hkv, D, mode, window, max_ctx_tokens,
+                                  HD_DTYPE_BF16);
+    memcpy(g_err, saved, sizeof g_err);
+    if (st != HD_OK) return 0;
+    return hd::decode_workspace_bytes(
+        hd::make_dec_geom(B, Lcap, n, Hq, Hkv, D, mode, window, 1.f, max_ctx_tokens));
+}
+
+hd_status_t hd_sfa_decode(const void *q, const void *k_cache, const void *v_cache,
+                          const int32_t *ctx_tokens, int max_ctx_tokens, void *o, float *lse,
+                          int B, int Lcap, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode,
+                          int window, float scale, hd_dtype_t dtype, void *workspace,
+                          size_t workspace_bytes, hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (!q || !k_cache || !v_cache || !ctx_tokens || !o || !lse)
+        return fail(HD_ERR_INVALID_ARG, "null pointer");
+    hd_status_t st = check_decode(B, Lcap, n, Hq, Hkv, D, mode, window, max_ctx_tokens, dtype);
+    if (st != HD_OK) return st;
+    if (!std::isfinite(scale) || !(scale > 0.f))
+        return fail(HD_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", (double)scale);
+    if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o) ||
+        !aligned16(lse) || (reinterpret_cast<uintptr_t>(ctx_tokens) & 3))
+        return fail(HD_ERR_INVALID_ARG, "tensors must be 16-byte aligned, ctx_tokens 4-byte aligned");
+    const hd::DecGeom g = hd::make_dec_geom(B, Lcap, n, Hq, Hkv, D, mode, window, scale,
+                                            max_ctx_tokens);
+    const size_t need = hd::decode_workspace_bytes(g);
+    if (!workspace) return fail(HD_ERR_INVALID_ARG, "null workspace (%zu bytes needed)", need);
+    if (reinterpret_cast<uintptr_t>(workspace) & 255)
+        return fail(HD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
+    if (workspace_bytes < need)
+        return fail(HD_ERR_INVALID_ARG, "workspace of %zu bytes is short of %zu", workspace_bytes,
+                    need);
+    return hip_status(hd::launch_decode_bf16(q, k_cache, v_cache, ctx_tokens, o, lse, g, workspace,
+                                             (hipStream_t)stream),
+                      "hd_sfa_decode launch");
 }
 
 hd_status_t hd_timing_enable(int enable)

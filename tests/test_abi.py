@@ -290,6 +290,41 @@ def test_final_workspace_sizes(lib):
     assert local == stats + B * Hq * nqt * band * 16384
 
 
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), INVALID), (dict(ctx=None), INVALID), (dict(B=0), INVALID),
+    (dict(Hkv=3), INVALID), (dict(mode=7), INVALID), (dict(mode=2, window=0), INVALID),
+    (dict(max_ctx=16), INVALID), (dict(max_ctx=-1), INVALID), (dict(scale=0.0), INVALID),
+    (dict(dtype=1), UNSUPPORTED), (dict(D=96), UNSUPPORTED), (dict(o=FAKE + 8), INVALID),
+    (dict(ctx=FAKE + 2), INVALID), (dict(ws=None), INVALID), (dict(ws=FAKE + 64), INVALID),
+    (dict(ws_bytes=10), INVALID),
+])
+def test_decode_validation(lib, kw, code):
+    a = dict(q=FAKE, ctx=FAKE, o=FAKE, B=2, Lcap=16, n=4, Hq=8, Hkv=2, D=64, mode=1, window=0,
+             max_ctx=10, scale=0.125, dtype=0, ws=FAKE)
+    a.update(kw)
+    need = lib.hd_sfa_decode_workspace_bytes(2, 16, 4, 8, 2, 64, 1, 0, 10)
+    st = lib.hd_sfa_decode(a["q"], FAKE, FAKE, a["ctx"], a["max_ctx"], a["o"], FAKE, a["B"],
+                           a["Lcap"], a["n"], a["Hq"], a["Hkv"], a["D"], a["mode"], a["window"],
+                           a["scale"], a["dtype"], a["ws"], a.get("ws_bytes", need), None)
+    assert st == code
+    assert lib.hd_last_error().decode() != ""
+
+
+def test_decode_workspace_size(lib):
+    """fp32 partials (max, sum and D sums for 32 query slots) per 256 cached rows of every
+    problem: (b, kv head, head chunk[, stream])."""
+    B, Lcap, n, Hq, Hkv, D = 2, 5000, 4, 32, 8, 128
+    per_chunk = 32 * (D + 2) * 4
+    rows = 4096 * n  # max_ctx + 1 = 4096 tokens
+    mix = lib.hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, 1, 0, 4095)
+    assert mix == B * Hkv * 1 * (rows // 256) * per_chunk  # G*n = 16 slots: one head chunk
+    intra = lib.hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, 0, 0, 4095)
+    assert intra == B * Hkv * n * (4096 // 256) * per_chunk
+    wide = lib.hd_sfa_decode_workspace_bytes(1, 100, 8, 64, 4, 64, 1, 0, 99)  # G*n = 128 slots
+    assert wide == 1 * 4 * 4 * ((100 * 8 + 255) // 256) * 32 * 66 * 4
+    assert lib.hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, 1, 0, Lcap) == 0
+
+
 def test_missing_library_raises(monkeypatch, tmp_path):
     """No silent fallback: a missing libhd.so is an ImportError on first use."""
     monkeypatch.setattr(binding, "_lib", None)
