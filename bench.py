@@ -400,7 +400,8 @@ def run_decode(args):
                 "achieved": round(per_launch / (avg_ms * 1e-3) / 1e9, 1) if per_launch else None,
                 "frac": round(per_launch / (avg_ms * 1e-3) / 1e9 / W.MI355X_HBM_PEAK_GBS, 4)
                 if per_launch else None,
-                "traffic": None, "bytes_per_launch": per_launch, "avg_launch_ms": round(avg_ms, 5)}
+                "traffic": measured_traffic(dom[0], args.workload), "bytes_per_launch": per_launch,
+                "avg_launch_ms": round(avg_ms, 5)}
     out = {
         "metric": "SFA parallel-stream decode KV-cache read GB/s", "value": round(value, 1),
         "unit": "GB/s", "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -417,6 +418,8 @@ def run_decode(args):
 
 # sources each kernel family is built from (a change voids stored counter readings)
 KERNEL_SOURCES = {
+    "sfa_decode_bf16": ["sfa_decode_bf16.hip", "decode_internal.h", "sfa_lds.h", "hd_device.h",
+                        "hd_internal.h"],
     "sfa_dkdv_bf16": ["sfa_bwd_bf16.hip", "sfa_lds.h", "hd_device.h", "hd_internal.h"],
     "sfa_dq_bf16": ["sfa_bwd_bf16.hip", "sfa_lds.h", "hd_device.h", "hd_internal.h"],
     "sfa_fwd_bf16": ["sfa_fwd_bf16.hip", "sfa_lds.h", "hd_device.h", "hd_internal.h"],

@@ -253,8 +253,8 @@ hd_status_t hd_sfa_bwd_final(const void *q, const void *k, const void *v, const 
                              size_t workspace_bytes, hd_stream_t stream);
 
 /*
- * hd_sfa_decode -- parallel-stream decode (Sec. "Serving Cost": at a decode step the n
- * streams of a sequence's new token are processed together).  For every sequence b with
+ * hd_sfa_decode -- parallel-stream decode (Sec. "Inference Cost": at a decode step the
+ * n streams of a sequence's new token are processed together in one pass).  For every sequence b with
  * ctx_tokens[b] = c tokens before the new one, query row s (stream s of the new token,
  * expanded position c*n + s) attends under `mode`'s mask to the sequence's cached rows:
  *   HD_SFA_INTRA: rows t*n + s for t <= c (its own stream: 1/n of the cache);

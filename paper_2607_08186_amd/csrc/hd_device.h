@@ -77,11 +77,6 @@ __device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-// Swap bits 2 and 3 of a key index inside a 16-key group.  An MFMA result register
-// block of lane half h holds keys {0..3, 8..11} + 4h of each 16-key group, so storing
-// key k at position swap23(k) lets those 8 keys be read back as one 16-byte run.
-__device__ inline int swap23(int k) { return (k & ~12) | ((k & 4) << 1) | ((k & 8) >> 1); }
-
 // Workgroup id -> (problem, row tile).  Tiles with the longest causal extent go first.
 // Consecutive workgroup ids are spread round-robin over the 8 XCDs, so when the
 // problem count allows it each XCD gets a contiguous band of problems (the query heads

@@ -225,42 +225,6 @@ struct Tile {
     }
 };
 
-// Transposed tile: 64 positions x D dims stored as D LDS rows of 64 positions (128
-// bytes), loaded from a pre-transposed copy in HBM whose positions already sit in
-// swap23 order inside each 16-position group (so the 8 positions an MFMA lane half
-// needs are one 16-byte chunk).  Chunk c of LDS row d sits at c ^ ((d >> 1) & 7):
-// 16 lanes reading 16 consecutive rows at one chunk hit 16 distinct bank groups.
-template <int D>
-struct TileT {
-    static constexpr int BYTES = D * kRows * 2;
-    static constexpr int INSTR = D * (kRows / 8) / 64;
-
-    __device__ static inline int swz(int d) { return (d >> 1) & 7; }
-
-    // rows d of the transposed copy live at byte base + d*stride (stride = padded
-    // length * 2); positions row0 .. row0+63 start at byte row0*2 of each row
-    __device__ static inline void load(char *lds_tile, rsrc_t rs, uint32_t base, uint32_t stride,
-                                       int row0, int wave, int nwaves, int lane)
-    {
-#pragma unroll
-        for (int t = wave; t < INSTR; t += nwaves) {
-            const int slot = t * 64 + lane;
-            const int d = slot >> 3;
-            const int c = (slot & 7) ^ swz(d);
-            const uint32_t off = base + (uint32_t)d * stride + (uint32_t)row0 * 2 + c * 16;
-            dma_lds16(rs, lds_tile + t * 1024, off);
-        }
-    }
-
-    // MFMA operand with k-slots along the positions: dim (LDS row) d, positions of
-    // 16-group kk held by lane half `half` (one 16-byte chunk in swap23 order)
-    __device__ static inline bf16x8 operand(const char *lds_tile, int d, int kk, int half)
-    {
-        const int c = (kk * 2 + half) ^ swz(d);
-        return *reinterpret_cast<const bf16x8 *>(lds_tile + d * (kRows * 2) + c * 16);
-    }
-};
-
 // Scheduling hint for the basic block it ends: P LDS reads up front, then N
 // repetitions of (M MFMAs, R LDS reads, V other vector ALU instructions), so that each
 // MFMA's operands were requested about P reads earlier.
