@@ -84,6 +84,39 @@ def kernel_family(name):
     return name
 
 
+def time_steps(hd, torch, step, steps):
+    """Run one untimed step with every library launch bracketed by HIP events (the
+    per-kernel breakdown), then `steps` timed steps in which only the launches of the
+    dominant kernel of that breakdown carry events (recorded on their launch stream),
+    so the timed region holds no other event.  -> (elapsed s of the timed steps,
+    breakdown [(name, launches, total ms)] of the one step, (name, launches, total ms)
+    of the dominant kernel over the timed steps)."""
+    torch.cuda.synchronize()
+    hd.hd_timing_filter(None)
+    hd.hd_timing_enable(True)
+    hd.hd_timing_collect()  # drop anything recorded before
+    step()
+    torch.cuda.synchronize()
+    hd.hd_timing_enable(False)
+    breakdown = hd.hd_timing_collect()
+    dom_name = max(breakdown, key=lambda r: r[2])[0]
+    hd.hd_timing_filter(dom_name)
+    hd.hd_timing_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step()
+        print(f"[bench] step {i + 1}/{steps} enqueued", file=sys.stderr, flush=True)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    hd.hd_timing_enable(False)
+    hd.hd_timing_filter(None)
+    dom = [r for r in hd.hd_timing_collect() if r[0] == dom_name]
+    if len(dom) != 1:
+        raise RuntimeError(f"no timing events for {dom_name} over the timed steps")
+    return elapsed, breakdown, dom[0]
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -233,19 +266,7 @@ def main():
 
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-
-    hd.hd_timing_enable(True)
-    hd.hd_timing_collect()  # drop anything recorded before
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step()
-        print(f"[bench] step {i + 1}/{args.steps} enqueued", file=sys.stderr, flush=True)
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    hd.hd_timing_enable(False)
-    ktimes = hd.hd_timing_collect()
+    elapsed, ktimes, dom = time_steps(hd, torch, step, args.steps)
 
     if final:
         flop_step = sum(14 * s.D * W.visible_pairs_final(s, window if m == W.LOCAL else 0)
@@ -260,15 +281,16 @@ def main():
     for m in modes:
         for fam, f in per_kernel_flops(s, m, window, final).items():
             fam_flops[fam] = fam_flops.get(fam, 0) + f
+    # breakdown: the one fully bracketed step; share = that kernel's time in it over the
+    # timed steps' ms per step
     per_kernel = []
     fam_ms = {}
     for name, launches, total_ms in ktimes:
         fam = kernel_family(name)
         fam_ms[fam] = fam_ms.get(fam, 0.0) + total_ms
-        per_kernel.append({"kernel": name, "launches": launches,
+        per_kernel.append({"kernel": name, "launches_per_step": launches,
                            "avg_ms": round(total_ms / launches, 5),
-                           "share": round(total_ms / (elapsed * 1e3), 4)})
-    dom = max(ktimes, key=lambda r: r[2])
+                           "share": round(total_ms / ms_per_step, 4)})
     dom_fam = kernel_family(dom[0])
     dom_launches = dom[1]
     avg_ms = dom[2] / dom_launches
@@ -285,16 +307,16 @@ def main():
                     "unit": "GB/s", "frac": None, "traffic": None}
     breakdown = {}
     for fam, ms in fam_ms.items():
-        ent = {"ms_per_step": round(ms / args.steps, 4)}
+        ent = {"ms_per_step": round(ms, 4)}
         if fam in fam_flops:
-            ent["tflops"] = round(fam_flops[fam] / (ms / args.steps * 1e-3) / 1e12, 2)
+            ent["tflops"] = round(fam_flops[fam] / (ms * 1e-3) / 1e12, 2)
         if fam == "expand":
             nbytes = W.embed_bytes(1, s.L, s.n, W.STACK_DMODEL)
-            ent["gbs"] = round(nbytes / (ms / args.steps * 1e-3) / 1e9, 1)
+            ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
             ent["bytes_per_launch"] = nbytes
         if fam == "expand_bwd":
             nbytes = W.embed_bwd_bytes(1, s.L, s.n, W.STACK_DMODEL, int(nuniq.cpu()[0]))
-            ent["gbs"] = round(nbytes / (ms / args.steps * 1e-3) / 1e9, 1)
+            ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
             ent["bytes_per_launch"] = nbytes
         breakdown[fam] = ent
 
@@ -372,16 +394,7 @@ def run_decode(args):
 
     for _ in range(args.warmup):
         step()
-    torch.cuda.synchronize()
-    hd.hd_timing_enable(True)
-    hd.hd_timing_collect()
-    t0 = time.perf_counter()
-    for i in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    hd.hd_timing_enable(False)
-    ktimes = hd.hd_timing_collect()
+    elapsed, ktimes, dom = time_steps(hd, torch, step, args.steps)
 
     def cache_bytes(m):
         rows = (ctx_len + 1) * n
@@ -391,9 +404,8 @@ def run_decode(args):
     bytes_step = sum(cache_bytes(m) for m in modes)
     ms_step = elapsed * 1e3 / args.steps
     value = bytes_step * args.steps / elapsed / 1e9
-    per_kernel = [{"kernel": name, "launches": nl, "avg_ms": round(ms / nl, 5),
-                   "share": round(ms / (elapsed * 1e3), 4)} for name, nl, ms in ktimes]
-    dom = max(ktimes, key=lambda r: r[2])
+    per_kernel = [{"kernel": name, "launches_per_step": nl, "avg_ms": round(ms / nl, 5),
+                   "share": round(ms / ms_step, 4)} for name, nl, ms in ktimes]
     avg_ms = dom[2] / dom[1]
     per_launch = bytes_step * args.steps / dom[1] if "partial" in dom[0] or "decode_bf16" in dom[0] else None
     roofline = {"kernel": dom[0], "bound": "hbm", "unit": "GB/s", "peak": W.MI355X_HBM_PEAK_GBS,

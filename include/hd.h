@@ -294,6 +294,9 @@ const char *hd_last_error(void);
  * Per-kernel timing (diagnostics, not needed for normal use).  While enabled, every
  * kernel the library launches is bracketed by a pair of HIP events recorded on the
  * launch stream (event objects are created on first use and reused).
+ * hd_timing_filter restricts this to kernels whose timing name starts with `prefix`
+ * (NULL or "" restores all; the string is copied), so that a measurement can bracket
+ * one kernel without adding events around the others.
  * hd_timing_collect waits for the recorded events, writes up to `max` entries of
  * accumulated (kernel name, launch count, total milliseconds) and clears the record.
  * Returns the number of entries written, or -1 on a HIP error.
@@ -305,6 +308,7 @@ typedef struct {
 } hd_kernel_time_t;
 
 hd_status_t hd_timing_enable(int enable);
+hd_status_t hd_timing_filter(const char *prefix);
 int hd_timing_collect(hd_kernel_time_t *out, int max);
 
 #ifdef __cplusplus

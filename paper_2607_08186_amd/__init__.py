@@ -12,7 +12,7 @@ from .binding import (HD_DTYPE_BF16, HD_DTYPE_F32, HD_SFA_INTRA, HD_SFA_LOCAL, H
                       hd_sfa_bwd_local_workspace_bytes, hd_sfa_bwd_workspace_bytes, hd_sfa_fwd, hd_sfa_fwd_local,
                       hd_sfa_bwd_final, hd_sfa_bwd_final_workspace_bytes, hd_sfa_decode,
                       hd_sfa_decode_workspace_bytes, hd_sfa_fwd_final, sfa_decode,
-                      hd_timing_collect, hd_timing_enable, sfa_backward, sfa_final_backward,
+                      hd_timing_collect, hd_timing_enable, hd_timing_filter, sfa_backward, sfa_final_backward,
                       sfa_final_forward, sfa_forward)
 
 __all__ = ["HD_DTYPE_BF16", "HD_DTYPE_F32", "HD_SFA_INTRA", "HD_SFA_LOCAL", "HD_SFA_MIX",
@@ -21,7 +21,7 @@ __all__ = ["HD_DTYPE_BF16", "HD_DTYPE_F32", "HD_SFA_INTRA", "HD_SFA_LOCAL", "HD_
            "hd_expand_embed_bwd", "hd_expand_embed_bwd_workspace_bytes", "hd_sfa_bwd",
            "hd_sfa_bwd_local",
            "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd_workspace_bytes", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_timing_collect",
-           "hd_timing_enable", "hd_sfa_bwd_final", "hd_sfa_bwd_final_workspace_bytes",
+           "hd_timing_enable", "hd_timing_filter", "hd_sfa_bwd_final", "hd_sfa_bwd_final_workspace_bytes",
            "hd_sfa_fwd_final", "hd_sfa_decode", "hd_sfa_decode_workspace_bytes", "sfa_decode",
            "sfa_backward", "sfa_final_backward", "sfa_final_forward",
            "sfa_forward"]

@@ -23,7 +23,7 @@ EXPORTS = ("hd_expand_embed", "hd_expand_embed_bwd_workspace_bytes", "hd_expand_
            "hd_sfa_bwd_final_workspace_bytes", "hd_sfa_bwd_final", "hd_sfa_decode_workspace_bytes",
            "hd_sfa_decode", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
            "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
-           "hd_timing_enable", "hd_timing_collect")
+           "hd_timing_enable", "hd_timing_filter", "hd_timing_collect")
 
 
 class HDError(RuntimeError):
@@ -80,13 +80,14 @@ def lib() -> ctypes.CDLL:
               L.hd_cyclic_replicate, L.hd_sfa_fwd_final, L.hd_sfa_bwd_final, L.hd_sfa_decode,
               L.hd_sfa_fwd,
               L.hd_sfa_fwd_local, L.hd_sfa_bwd,
-              L.hd_sfa_bwd_local, L.hd_timing_enable):
+              L.hd_sfa_bwd_local, L.hd_timing_enable, L.hd_timing_filter):
         f.restype = i32
     L.hd_status_str.argtypes = [i32]
     L.hd_status_str.restype = ctypes.c_char_p
     L.hd_last_error.argtypes = []
     L.hd_last_error.restype = ctypes.c_char_p
     L.hd_timing_enable.argtypes = [i32]
+    L.hd_timing_filter.argtypes = [ctypes.c_char_p]
     L.hd_timing_collect.argtypes = [ctypes.POINTER(KernelTime), i32]
     L.hd_timing_collect.restype = i32
     _lib = L
@@ -231,6 +232,11 @@ def hd_sfa_decode(q, k_cache, v_cache, ctx_tokens, max_ctx_tokens, o, lse, B, Lc
 
 def hd_timing_enable(enable: bool):
     _check(lib().hd_timing_enable(1 if enable else 0))
+
+
+def hd_timing_filter(prefix: str | None = None):
+    """Time only kernels whose timing name starts with `prefix` (None or "": all)."""
+    _check(lib().hd_timing_filter(prefix.encode() if prefix else None))
 
 
 def hd_timing_collect(max_entries: int = 64):

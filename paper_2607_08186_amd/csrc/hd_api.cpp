@@ -82,6 +82,7 @@ struct TimingRecord {
 
 std::mutex g_tmu;
 bool g_timing = false;
+std::string g_tfilter;  // time only kernels whose name starts with this (empty: all)
 std::vector<hipEvent_t> g_pool;
 std::vector<TimingRecord> g_records;
 thread_local int g_open = -1;
@@ -106,7 +107,7 @@ void timing_before(const char *name, hipStream_t s)
 {
     std::lock_guard<std::mutex> lk(g_tmu);
     g_open = -1;
-    if (!g_timing) return;
+    if (!g_timing || strncmp(name, g_tfilter.c_str(), g_tfilter.size()) != 0) return;
     TimingRecord r{name, take_event(), take_event()};
     if (!r.start || !r.stop) return;
     (void)hipEventRecord(r.start, s);
@@ -509,6 +510,13 @@ hd_status_t hd_timing_enable(int enable)
 {
     std::lock_guard<std::mutex> lk(g_tmu);
     g_timing = enable != 0;
+    return HD_OK;
+}
+
+hd_status_t hd_timing_filter(const char *prefix)
+{
+    std::lock_guard<std::mutex> lk(g_tmu);
+    g_tfilter = prefix ? prefix : "";
     return HD_OK;
 }
 

@@ -119,10 +119,11 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const int kw0 = k0 + kw * 32;
     const int key = kw0 + l32;
 
-    // Sweep: for each query head of the group, the query tiles from the last one down
-    // to the one holding the first key.  Workgroups of one problem that run together
-    // (decode_key_tile keeps a problem's key tiles on one XCD) then read the same Q/dO
-    // tiles at about the same time, so most of those reads hit in L2.
+    // Sweep: the query tiles from the last one down to the one holding the first key,
+    // and for each tile every query head of the group in turn.  Workgroups of one
+    // problem that run together (decode_key_tile keeps a problem's key tiles on one
+    // XCD) then read the same Q/dO tiles at about the same time, and the group's heads
+    // follow each other, so most of those reads hit in L2.
     // first query tile with a row that sees the first key (P(i) >= k0)
     const int qt_first = max(0, (k0 - g.qpoff + g.qpmul - 1) / g.qpmul) / kRows;
     const int band = ds_band(g);
@@ -202,14 +203,15 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
         }
     };
     // Sweep position (query head gi, query tile qt) of the current step; the next step
-    // takes the tile below, or the last tile of the next head.
+    // takes the next head of the group, or after the last one the first head of the
+    // tile below.
     int cur_gi = 0, cur_qt = qt_end - 1;
     const bf16 *ds_head = ds_problem(0);
     auto step = [&](int it, auto stage) __attribute__((always_inline)) {
         constexpr int st = decltype(stage)::value;
-        const bool wrap = cur_qt == qt_first;
-        const int nxt_gi = wrap ? cur_gi + 1 : cur_gi;
-        const int nxt_qt = wrap ? qt_end - 1 : cur_qt - 1;
+        const bool wrap = cur_gi + 1 == g.G;
+        const int nxt_gi = wrap ? 0 : cur_gi + 1;
+        const int nxt_qt = wrap ? cur_qt - 1 : cur_qt;
         if (it + 1 < iters) issue(nxt_gi, nxt_qt, st ^ 1);
         const int qlo = cur_qt * kRows + qb * 32;
         const rsrc_t rds = make_rsrc(
@@ -287,7 +289,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
         lds_barrier();
         cur_gi = nxt_gi;
         cur_qt = nxt_qt;
-        if (wrap) ds_head = ds_problem(nxt_gi);
+        ds_head = ds_problem(nxt_gi);
     };
     for (int it = 0; it < iters; it += 2) {
         step(it, std::integral_constant<int, 0>{});

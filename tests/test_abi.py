@@ -335,3 +335,11 @@ def test_missing_library_raises(monkeypatch, tmp_path):
 
 def test_timing_collect_empty(lib):
     assert binding.hd_timing_collect() == []
+
+
+def test_timing_filter_set_and_reset(lib):
+    assert lib.hd_timing_filter(b"sfa_dkdv") == 0
+    assert lib.hd_timing_filter(None) == 0
+    binding.hd_timing_filter("sfa_fwd")
+    binding.hd_timing_filter(None)
+    assert binding.hd_timing_collect() == []
