@@ -244,6 +244,9 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                 pacc = mfma32(T::row_operand(dot, qb * 32 + l32, kk, hi),
                               T::row_operand(vtl, krow, kk, hi), pacc);
             }
+            // statistics and the first operands up front, then each MFMA's operands
+            // about three MFMAs ahead
+            sched_pattern<12, 2 * KS, 1, 2, 0>();
             uint32_t pw[8], dw[8];
             if (qpos(g, qlo) < kw0 + 31 || qpos(g, qlo + 31) - kw0 >= g.window)  // diagonal or window edge
                 softmax(sacc, pacc, qlo, pw, dw, std::true_type{});
@@ -262,6 +265,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                     adk[db] = mfma32(T::tr_operand(qt, db * 32, kk, lane), dsb, adk[db]);
                 }
             }
+            sched_pattern<8, 4 * DB, 1, 2, 0>();
             // dw[2 rq .. 2 rq + 1]: queries 8 rq + 4 hi .. +3 of my key.  Swap the upper
             // octets of half 0 with the lower octets of half 1, so that half 0 holds
             // queries 0..15 and half 1 queries 16..31: 32 contiguous bytes per lane.
