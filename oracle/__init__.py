@@ -54,6 +54,10 @@ def _load():
     for f in (lib.oracle_sfa_fwd, lib.oracle_sfa_fwd_rows, lib.oracle_sfa_bwd,
               lib.oracle_sfa_bwd_dq_rows, lib.oracle_sfa_bwd_dkdv_rows):
         f.restype = None
+    lib.oracle_final_gather.argtypes = [vp, vp, i64, i64, i64, i64, i64]
+    lib.oracle_final_gather.restype = None
+    lib.oracle_final_gather_bwd.argtypes = [vp, vp, i64, i64, i64, i64, i64]
+    lib.oracle_final_gather_bwd.restype = None
     lib.oracle_expand_embed.argtypes = [vp, vp, vp, i64, i64, i64, i64, i64, i64]
     lib.oracle_expand_embed.restype = i64
     lib.oracle_expand_embed_bwd.argtypes = [vp, vp, i32, vp, i64, i64, i64, i64, i64]
@@ -242,6 +246,27 @@ def cyclic_replicate(tables, m):
     out = np.empty((m, V, Dm), dtype=tables.dtype)
     _load().oracle_cyclic_replicate(_ptr(tables), _ptr(out), n, m, V, Dm, tables.dtype.itemsize)
     return out
+
+
+def final_gather(h, n):
+    """eq. (hd_loss) input: h [B][n*L][Dm] (any dtype) -> [B][L][Dm], row i = h[i*n + n-1]."""
+    h = np.ascontiguousarray(h)
+    B, N, Dm = h.shape
+    if N % n:
+        raise ValueError("h must be [B][n*L][Dm]")
+    L = N // n
+    out = np.empty((B, L, Dm), dtype=h.dtype)
+    _load().oracle_final_gather(_ptr(h), _ptr(out), B, L, n, Dm, h.dtype.itemsize)
+    return out
+
+
+def final_gather_bwd(dout, n):
+    """Adjoint of final_gather: dout [B][L][Dm] -> dh [B][n*L][Dm], zero off the final rows."""
+    dout = np.ascontiguousarray(dout)
+    B, L, Dm = dout.shape
+    dh = np.empty((B, n * L, Dm), dtype=dout.dtype)
+    _load().oracle_final_gather_bwd(_ptr(dout), _ptr(dh), B, L, n, Dm, dout.dtype.itemsize)
+    return dh
 
 
 def sfa_mask(L, n, mode, window=0):

@@ -524,3 +524,30 @@ void oracle_sfa_mask(unsigned char *mask, int64_t L, int64_t n, int mode, int64_
     for (int64_t p = 0; p < N; ++p)
         for (int64_t j = 0; j < N; ++j) mask[p * N + j] = (unsigned char)visible(mode, n, window, p, j);
 }
+
+/* Final-stream gather, eq. (hd_loss): the loss reads the hidden state of token i only at
+ * the final stream of its block, expanded position i*n + n - 1 (0-based), so
+ * out[b][i][:] = h[b][i*n + n - 1][:] for h [B][n*L][Dm] and out [B][L][Dm].  Elements
+ * are copied as opaque elem_bytes-byte values. */
+void oracle_final_gather(const void *h, void *out, int64_t B, int64_t L, int64_t n,
+                         int64_t Dm, int64_t elem_bytes)
+{
+    const size_t row = (size_t)(Dm * elem_bytes);
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t i = 0; i < L; ++i)
+            memcpy((char *)out + (size_t)(b * L + i) * row,
+                   (const char *)h + (size_t)(b * n * L + i * n + n - 1) * row, row);
+}
+
+/* Its adjoint: the gradient w.r.t. h is dout at the final-stream positions and zero at
+ * the other n - 1 positions of every token (those receive no direct loss). */
+void oracle_final_gather_bwd(const void *dout, void *dh, int64_t B, int64_t L, int64_t n,
+                             int64_t Dm, int64_t elem_bytes)
+{
+    const size_t row = (size_t)(Dm * elem_bytes);
+    memset(dh, 0, (size_t)(B * n * L) * row);
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t i = 0; i < L; ++i)
+            memcpy((char *)dh + (size_t)(b * n * L + i * n + n - 1) * row,
+                   (const char *)dout + (size_t)(b * L + i) * row, row);
+}

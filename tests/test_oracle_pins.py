@@ -798,3 +798,40 @@ def test_decode_ignores_cache_past_the_new_token_and_other_streams(oracle_mod):
     o2, lse2 = oracle_mod.sfa_decode(q, kp, vp, ctx, n=n, mode=INTRA, scale=0.5)
     np.testing.assert_array_equal(o[:, 0], o2[:, 0])
     np.testing.assert_array_equal(lse[:, :, 0], lse2[:, :, 0])
+
+
+def test_final_gather_reads_the_supervised_stream(oracle_mod):
+    """eq. (hd_loss) supervises the final stream E_n(x_i) of each token: gathered from the
+    layer-0 expanded sequence it is the paper's n=2 example's E2 rows, and in general the
+    final table's rows of the ids (numpy indexing)."""
+    g = json.load(open(os.path.join(GOLDEN, "expand_n2.json")))
+    tables = np.array([g["tables_E1"], g["tables_E2"]], dtype=np.uint16)
+    ids = np.array([g["ids"]], dtype=np.int32)
+    out, _ = oracle_mod.expand_embed(ids, tables)
+    fin = oracle_mod.final_gather(out, 2)
+    np.testing.assert_array_equal(fin[0], np.array(g["expected_rows"], dtype=np.uint16)[1::2])
+    r = np.random.default_rng(21)
+    for n in (1, 3, 5):
+        B, L, V, Dm = 2, 13, 9, 4
+        ids = r.integers(0, V, size=(B, L)).astype(np.int32)
+        tab = r.standard_normal((n, V, Dm))
+        out, _ = oracle_mod.expand_embed(ids, tab)
+        np.testing.assert_array_equal(oracle_mod.final_gather(out, n), tab[n - 1][ids])
+        if n == 1:  # one stream: the gather is the identity
+            np.testing.assert_array_equal(oracle_mod.final_gather(out, 1), out)
+
+
+def test_final_gather_bwd_equals_library_autograd_and_is_adjoint(oracle_mod):
+    """The gradient of torch's index_select of rows i*n + n-1 (autograd, fp64) equals the
+    oracle's backward, which is zero at the other n-1 rows of each token, and
+    <gather(h), y> == <h, gather_bwd(y)>."""
+    r = np.random.default_rng(22)
+    for B, L, n, Dm in ((1, 7, 4, 3), (3, 10, 2, 5), (2, 6, 1, 4)):
+        h = torch.tensor(r.standard_normal((B, n * L, Dm)), requires_grad=True)
+        y = r.standard_normal((B, L, Dm))
+        torch.index_select(h, 1, torch.arange(L) * n + n - 1).backward(torch.tensor(y))
+        dh = oracle_mod.final_gather_bwd(y, n)
+        np.testing.assert_array_equal(dh, h.grad.numpy())
+        hv = h.detach().numpy()
+        lhs = float(np.sum(oracle_mod.final_gather(hv, n) * y))
+        assert abs(lhs - float(np.sum(hv * dh))) <= 1e-12 * np.sum(np.abs(hv[:, n - 1::n] * y))
