@@ -5,14 +5,18 @@ One step = one pass of the whole hot path over one batch of synthetic input, the
 expanded rows, Hq=32, Hkv=8, D=128, bf16):
   * the stream expansion of 4096 token ids through n=4 tables of 151936 x 4096,
   * the forward of 36 attention layers (mixing layers at 8, 17, 26, 35, intra-stream
-    layers elsewhere), then their backward in reverse order,
+    layers elsewhere),
+  * the final-stream gather of the 4096 x 4096 hidden states that the loss reads,
+    eq. (hd_loss), and its adjoint,
+  * the backward of the 36 layers in reverse order,
   * the expansion's backward (sparse gradient of the n tables),
 each layer on its own seeded q/k/v/dO, all resident in HBM before timing starts.
 
 Prints one JSON line.  value = useful TFLOP/s of the whole step (useful flop counts
 only visible query/key pairs: 4*D per pair forward, 10*D backward).  The roofline
-entry is for the kernel with the largest share of the step, timed with HIP events
-recorded by the library around every launch, on the launch stream.
+entry is for the kernel with the largest share of the step (from one untimed step with
+HIP events around every launch), timed with HIP events that the library records on the
+launch stream around that kernel's launches in the timed steps.
 """
 from __future__ import annotations
 
@@ -155,6 +159,7 @@ def main():
         with_embed = True
         wl_desc = (f"stack36: expand_embed (n=4 tables of {W.STACK_VOCAB}x{W.STACK_DMODEL}) + "
                    f"fwd of 36 layers (mix at {list(W.STACK_MIX_LAYERS)}, intra elsewhere) + "
+                   "final-stream gather of the hidden states and its adjoint + "
                    "bwd in reverse, each layer B=1 L=4096 n=4 Hq=32 Hkv=8 D=128, + "
                    "expand_embed backward")
         std = W.QWEN8B.qkv_std
@@ -228,6 +233,12 @@ def main():
         nuniq = torch.empty(1, dtype=torch.int32, device=dev)
         ews_bytes = hd.hd_expand_embed_bwd_workspace_bytes(1, s.L)
         ews = torch.empty(ews_bytes, dtype=torch.uint8, device=dev)
+        # the loss input: final-stream rows of the top hidden states (the expansion's
+        # output stands in for them: same [1][N][Dm] layout), and the adjoint of an
+        # upstream gradient of those rows
+        hfin = torch.empty((1, s.L, W.STACK_DMODEL), dtype=torch.bfloat16, device=dev)
+        dfin = synth.device_normal((1, s.L, W.STACK_DMODEL), 1.0, 14, dev, torch.bfloat16)
+        dh = torch.empty((1, s.N, W.STACK_DMODEL), dtype=torch.bfloat16, device=dev)
     torch.cuda.synchronize()
     t_gen = time.time() - t_gen
 
@@ -246,6 +257,9 @@ def main():
             else:
                 hd.hd_sfa_fwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L, s.n,
                               s.Hq, s.Hkv, s.D, ly["mode"], scale, stream=stream)
+        if with_embed:
+            hd.hd_final_stream_gather(emb, hfin, 1, s.L, s.n, W.STACK_DMODEL, stream=stream)
+            hd.hd_final_stream_gather_bwd(dfin, dh, 1, s.L, s.n, W.STACK_DMODEL, stream=stream)
         for ly in reversed(layers):
             if final:
                 hd.hd_sfa_bwd_final(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq,
@@ -312,6 +326,10 @@ def main():
             ent["tflops"] = round(fam_flops[fam] / (ms * 1e-3) / 1e12, 2)
         if fam == "expand":
             nbytes = W.embed_bytes(1, s.L, s.n, W.STACK_DMODEL)
+            ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
+            ent["bytes_per_launch"] = nbytes
+        if fam in ("final_gather", "final_gather_bwd"):
+            nbytes = W.final_gather_bytes(1, s.L, s.n, W.STACK_DMODEL, fam == "final_gather_bwd")
             ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
             ent["bytes_per_launch"] = nbytes
         if fam == "expand_bwd":

@@ -134,6 +134,34 @@ hd_status_t hd_cyclic_replicate(const void *src, void *dst, int n, int m, int64_
                                 hd_dtype_t dtype, hd_stream_t stream);
 
 /*
+ * hd_final_stream_gather -- the input of the training loss, eq. (hd_loss) (Sec. "Training
+ * objective"): only the final stream of each token is supervised, so the loss reads token
+ * i's hidden state at expanded position i*n + n - 1 (the paper's t = i n, 1-based):
+ *   out[b][i][:] = h[b][i*n + n - 1][:]
+ *
+ * h    device [B][n*L][Dm] of `dtype` (bf16 or f32), the last layer's hidden states.
+ * out  device [B][L][Dm] of `dtype`, overwritten; must not overlap h.
+ * Errors: INVALID_ARG for null or unaligned (16-byte) pointers, B, L, n, Dm <= 0,
+ *         B*n*L > INT32_MAX, an output of 2^31 copy words or more (16-byte words when
+ *         Dm*esize is a multiple of 16, else 4- or 2-byte words), or overlapping buffers.
+ */
+hd_status_t hd_final_stream_gather(const void *h, void *out, int B, int L, int n, int Dm,
+                                   hd_dtype_t dtype, hd_stream_t stream);
+
+/*
+ * hd_final_stream_gather_bwd -- its adjoint: the gradient with respect to h of a loss on
+ * the gathered rows,
+ *   dh[b][i*n + n - 1][:] = dout[b][i][:],   dh[b][i*n + s][:] = 0 for s < n - 1
+ * (the first n - 1 streams of a token receive no direct loss).
+ *
+ * dout device [B][L][Dm] of `dtype`;  dh  device [B][n*L][Dm] of `dtype`, overwritten in
+ *      full; must not overlap dout.
+ * Errors: as hd_final_stream_gather (the size limit applies to dh).
+ */
+hd_status_t hd_final_stream_gather_bwd(const void *dout, void *dh, int B, int L, int n, int Dm,
+                                       hd_dtype_t dtype, hd_stream_t stream);
+
+/*
  * hd_sfa_fwd -- Stream-Factorized Attention forward over the expanded sequence.
  *   O_p = sum_{p' visible from p} softmax_p'(scale * q_p . k_p') v_p'
  *   lse_p = log sum_{p' visible} exp(scale * q_p . k_p')       (natural log)

@@ -21,7 +21,7 @@ HD_DTYPE_BF16, HD_DTYPE_F32 = 0, 1
 EXPORTS = ("hd_expand_embed", "hd_expand_embed_bwd_workspace_bytes", "hd_expand_embed_bwd",
            "hd_embed_grad_scatter_add", "hd_cyclic_replicate", "hd_sfa_fwd_final",
            "hd_sfa_bwd_final_workspace_bytes", "hd_sfa_bwd_final", "hd_sfa_decode_workspace_bytes",
-           "hd_sfa_decode", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
+           "hd_sfa_decode", "hd_final_stream_gather", "hd_final_stream_gather_bwd", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
            "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
            "hd_timing_enable", "hd_timing_filter", "hd_timing_collect")
 
@@ -76,8 +76,11 @@ def lib() -> ctypes.CDLL:
     L.hd_expand_embed_bwd.argtypes = [vp, vp, i32, i32, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp]
     L.hd_embed_grad_scatter_add.argtypes = [vp, vp, vp, i32, i32, i64, i32, vp, vp]
     L.hd_cyclic_replicate.argtypes = [vp, vp, i32, i32, i64, i32, i32, vp]
+    L.hd_final_stream_gather.argtypes = [vp, vp] + [i32] * 5 + [vp]
+    L.hd_final_stream_gather_bwd.argtypes = [vp, vp] + [i32] * 5 + [vp]
     for f in (L.hd_expand_embed, L.hd_expand_embed_bwd, L.hd_embed_grad_scatter_add,
-              L.hd_cyclic_replicate, L.hd_sfa_fwd_final, L.hd_sfa_bwd_final, L.hd_sfa_decode,
+              L.hd_cyclic_replicate, L.hd_final_stream_gather, L.hd_final_stream_gather_bwd,
+              L.hd_sfa_fwd_final, L.hd_sfa_bwd_final, L.hd_sfa_decode,
               L.hd_sfa_fwd,
               L.hd_sfa_fwd_local, L.hd_sfa_bwd,
               L.hd_sfa_bwd_local, L.hd_timing_enable, L.hd_timing_filter):
@@ -159,6 +162,16 @@ def hd_embed_grad_scatter_add(uniq_ids, drows, num_uniq, max_rows, n, V, Dm, dta
 def hd_cyclic_replicate(src, dst, n, m, V, Dm, dtype=None, stream=None):
     _check(lib().hd_cyclic_replicate(_ptr(src), _ptr(dst), n, m, V, Dm, _dtype_code(src, dtype),
                                      _stream(stream)))
+
+
+def hd_final_stream_gather(h, out, B, L, n, Dm, dtype=None, stream=None):
+    _check(lib().hd_final_stream_gather(_ptr(h), _ptr(out), B, L, n, Dm, _dtype_code(h, dtype),
+                                        _stream(stream)))
+
+
+def hd_final_stream_gather_bwd(dout, dh, B, L, n, Dm, dtype=None, stream=None):
+    _check(lib().hd_final_stream_gather_bwd(_ptr(dout), _ptr(dh), B, L, n, Dm,
+                                            _dtype_code(dout, dtype), _stream(stream)))
 
 
 def hd_sfa_fwd(q, k, v, o, lse, B, L, n, Hq, Hkv, D, mode, scale, dtype=None, stream=None):
@@ -349,6 +362,28 @@ def cyclic_replicate(tables, m, *, stream=None):
     out = torch.empty((m, V, Dm), dtype=tables.dtype, device=tables.device)
     hd_cyclic_replicate(tables, out, n, m, V, Dm, stream=stream)
     return out
+
+
+def final_stream_gather(h, n, *, stream=None):
+    """eq. (hd_loss) input: h [B][n*L][Dm] -> new [B][L][Dm], row i = h[i*n + n - 1]."""
+    import torch
+
+    B, N, Dm = h.shape
+    if N % n:
+        raise ValueError("h must hold n*L expanded rows")
+    out = torch.empty((B, N // n, Dm), dtype=h.dtype, device=h.device)
+    hd_final_stream_gather(h, out, B, N // n, n, Dm, stream=stream)
+    return out
+
+
+def final_stream_gather_backward(dout, n, *, stream=None):
+    """Adjoint: dout [B][L][Dm] -> new dh [B][n*L][Dm], zero off the final-stream rows."""
+    import torch
+
+    B, L, Dm = dout.shape
+    dh = torch.empty((B, n * L, Dm), dtype=dout.dtype, device=dout.device)
+    hd_final_stream_gather_bwd(dout, dh, B, L, n, Dm, stream=stream)
+    return dh
 
 
 def sfa_final_forward(q, k, v, *, n, window=0, scale=None, stream=None):

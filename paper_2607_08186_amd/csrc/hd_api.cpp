@@ -245,6 +245,48 @@ hd_status_t hd_cyclic_replicate(const void *src, void *dst, int n, int m, int64_
 
 namespace {
 
+hd_status_t final_gather(const void *src, void *dst, int B, int L, int n, int Dm,
+                         hd_dtype_t dtype, bool backward, hd_stream_t stream, const char *what)
+{
+    g_err[0] = 0;
+    if (!src || !dst) return fail(HD_ERR_INVALID_ARG, "%s: null pointer", what);
+    if (B <= 0 || L <= 0 || n <= 0 || Dm <= 0)
+        return fail(HD_ERR_INVALID_ARG, "%s: sizes must be positive (B=%d L=%d n=%d Dm=%d)", what,
+                    B, L, n, Dm);
+    if (dtype != HD_DTYPE_BF16 && dtype != HD_DTYPE_F32)
+        return fail(HD_ERR_INVALID_ARG, "%s: unknown dtype %d", what, (int)dtype);
+    if (!aligned16(src) || !aligned16(dst))
+        return fail(HD_ERR_INVALID_ARG, "%s: pointers must be 16-byte aligned", what);
+    const int esize = dtype == HD_DTYPE_BF16 ? 2 : 4;
+    const int64_t row = (int64_t)Dm * esize;
+    const int64_t word = row % 16 == 0 ? 16 : row % 4 == 0 ? 4 : 2;
+    const int64_t big = (int64_t)B * n * L * row, small = (int64_t)B * L * row;  // h, out bytes
+    if ((int64_t)B * n * L > INT32_MAX || (backward ? big : small) / word >= ((int64_t)1 << 31))
+        return fail(HD_ERR_INVALID_ARG, "%s: too large (B=%d L=%d n=%d Dm=%d)", what, B, L, n, Dm);
+    const uintptr_t a = reinterpret_cast<uintptr_t>(src), b = reinterpret_cast<uintptr_t>(dst);
+    const uintptr_t alen = (uintptr_t)(backward ? small : big), blen = (uintptr_t)(backward ? big : small);
+    if (a < b + blen && b < a + alen) return fail(HD_ERR_INVALID_ARG, "%s: buffers overlap", what);
+    return hip_status(hd::launch_final_gather(src, dst, B, L, n, Dm, esize, backward,
+                                              (hipStream_t)stream),
+                      what);
+}
+
+}  // namespace
+
+hd_status_t hd_final_stream_gather(const void *h, void *out, int B, int L, int n, int Dm,
+                                   hd_dtype_t dtype, hd_stream_t stream)
+{
+    return final_gather(h, out, B, L, n, Dm, dtype, false, stream, "hd_final_stream_gather");
+}
+
+hd_status_t hd_final_stream_gather_bwd(const void *dout, void *dh, int B, int L, int n, int Dm,
+                                       hd_dtype_t dtype, hd_stream_t stream)
+{
+    return final_gather(dout, dh, B, L, n, Dm, dtype, true, stream, "hd_final_stream_gather_bwd");
+}
+
+namespace {
+
 // Final-stream layers (queries at the final stream of each token only): bf16 kernels,
 // and at most 63 streams (the forward's eight waves then all reach the last key tile
 // of their 256-row block).

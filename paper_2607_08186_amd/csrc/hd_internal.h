@@ -84,6 +84,9 @@ void timing_after(hipStream_t s);
 hipError_t launch_expand_embed(const int32_t *ids, const void *tables, void *out, int B, int L,
                                int n, int64_t V, int Dm, int esize, int32_t *bad,
                                hipStream_t s);
+// final-stream gather (backward: its adjoint, dh written in full)
+hipError_t launch_final_gather(const void *h, void *out, int B, int L, int n, int Dm, int esize,
+                               bool backward, hipStream_t s);
 
 hipError_t launch_fwd_bf16(const void *q, const void *k, const void *v, void *o, float *lse,
                            const SfaGeom &g, hipStream_t s);

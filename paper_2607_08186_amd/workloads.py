@@ -112,6 +112,13 @@ def embed_bytes(B: int, L: int, n: int, Dm: int, esize: int = 2) -> int:
     return 2 * B * n * L * Dm * esize + B * L * 4
 
 
+def final_gather_bytes(B: int, L: int, n: int, Dm: int, backward: bool, esize: int = 2) -> int:
+    """Compulsory traffic of the final-stream gather (read and write L rows) or of its
+    adjoint (read L rows, write all n*L rows)."""
+    row = B * Dm * esize
+    return (L + n * L) * row if backward else 2 * L * row
+
+
 def embed_bwd_bytes(B: int, L: int, n: int, Dm: int, n_distinct: int, esize: int = 2) -> int:
     """Compulsory traffic of the expansion's backward: read every upstream expanded row
     and the ids once, write one fp32 gradient row per (distinct id, stream) and the

@@ -343,3 +343,27 @@ def test_timing_filter_set_and_reset(lib):
     binding.hd_timing_filter("sfa_fwd")
     binding.hd_timing_filter(None)
     assert binding.hd_timing_collect() == []
+
+
+# h at FAKE is [B][n*L][Dm] = 2*3*5*8 bf16 = 480 bytes; out [B][L][Dm] = 160 bytes
+@pytest.mark.parametrize("args,code", [
+    (dict(src=None), INVALID), (dict(dst=None), INVALID), (dict(B=0), INVALID),
+    (dict(L=-1), INVALID), (dict(n=0), INVALID), (dict(Dm=0), INVALID), (dict(dtype=7), INVALID),
+    (dict(src=FAKE + 4), INVALID), (dict(dst=FAKE + (1 << 20) + 8), INVALID),
+    (dict(dst=FAKE + 464), INVALID),      # overlaps the end of the larger buffer
+    (dict(dst=FAKE - 144), INVALID),      # the smaller buffer ends inside the larger one
+    (dict(B=1 << 16, L=1 << 16), INVALID),  # B*n*L beyond int32
+])
+@pytest.mark.parametrize("backward", [False, True])
+def test_final_stream_gather_validation(lib, args, code, backward):
+    a = dict(src=FAKE, dst=FAKE + (1 << 20), B=2, L=5, n=3, Dm=8, dtype=0)
+    a.update(args)
+    if backward:  # src is dout (small), dst is dh (large): mirror the overlap cases
+        if "dst" in args and args["dst"] is not None and args["dst"] != FAKE + (1 << 20) + 8:
+            a["src"], a["dst"] = a["dst"], FAKE
+        st = lib.hd_final_stream_gather_bwd(a["src"], a["dst"], a["B"], a["L"], a["n"], a["Dm"],
+                                            a["dtype"], None)
+    else:
+        st = lib.hd_final_stream_gather(a["src"], a["dst"], a["B"], a["L"], a["n"], a["Dm"],
+                                        a["dtype"], None)
+    assert st == code
