@@ -123,3 +123,30 @@ def test_decode_fullsize_batch(mode):
     ro, rl = oracle.sfa_decode(ins["q"][pick], ins["k"][pick], ins["v"][pick], ctx[pick],
                                n=s.n, mode=mode, scale=s.scale)
     G.assert_close_fwd(o[pick], lse[pick], ro, rl, "bf16", "decode fullsize")
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("mode", [MIX, INTRA], ids=["mix", "intra"])
+def test_decode_at_the_cache_slice_limit(mode):
+    """Each sequence's cache as large as the boundary accepts: Lcap=262143 tokens of n=4
+    streams at Hkv=8, D=128 is 2147475456 bytes per sequence for K (and for V), the
+    largest below the 2^31 bytes that the kernels' 32-bit buffer offsets address; two sequences,
+    so the second one's slice starts past 2 GiB.  Contexts at the capacity and mid-way,
+    checked against the oracle.  The caches come from torch's seeded device generator
+    (a host draw of 2 x 10^9 normals takes minutes); the oracle reads host copies."""
+    B, Lcap, n, Hq, Hkv, D = 2, 262143, 4, 32, 8, 128
+    assert n * Lcap * Hkv * D * 2 < 2 ** 31 <= n * (Lcap + 1) * Hkv * D * 2
+    seed = synth.seed_for("decode_slice_limit", mode)
+    print(f"decode slice limit mode={mode} Lcap={Lcap} seed={seed}", flush=True)
+    dev = G.dev()
+    q = synth.device_normal((B, n, Hq, D), 2 ** -0.5, seed, dev, torch.bfloat16)
+    k = synth.device_normal((B, n * Lcap, Hkv, D), 2 ** -0.5, seed + 1, dev, torch.bfloat16)
+    v = synth.device_normal((B, n * Lcap, Hkv, D), 2 ** -0.5, seed + 2, dev, torch.bfloat16)
+    ctx = np.array([Lcap - 1, 100003], dtype=np.int32)
+    o, lse = hd.sfa_decode(q, k, v, torch.from_numpy(ctx).to(dev), max_ctx=Lcap - 1, mode=mode,
+                           window=0)
+    torch.cuda.synchronize()
+    print("decode slice limit: oracle", flush=True)
+    ro, rl = oracle.sfa_decode(G.bits(q), G.bits(k), G.bits(v), ctx, n=n, mode=mode,
+                               scale=D ** -0.5)
+    G.assert_close_fwd(G.to_host64(o), G.to_host64(lse), ro, rl, "bf16", "decode slice limit")

@@ -79,3 +79,53 @@ def test_fullsize_sampled(wl, mode):
         scale_k = np.abs(dk[:, sl]).sum(axis=1)
         assert np.all(np.abs(got_k) <= 1e-2 * scale_k + 1e-3), "sum_j dK_j != 0"
     assert np.all(np.isfinite(lse)) and np.all(np.isfinite(o))
+
+
+_SLICE_LIMIT = {}
+
+
+def _slice_limit_inputs(N, Hq, Hkv, D):
+    """Seeded inputs of the slice-limit shape, drawn once for both modes: N(0, 1/2) from
+    torch's seeded device generator (a host draw of 10^9 normals takes minutes), rounded
+    to bf16; the oracle reads host copies of the same tensors."""
+    if not _SLICE_LIMIT:
+        import torch
+
+        seed = synth.seed_for("slice_limit")
+        t = {name: synth.device_normal((1, N, h, D), 2 ** -0.5, seed + i, G.dev(), torch.bfloat16)
+             for i, (name, h) in enumerate((("q", Hq), ("k", Hkv), ("v", Hkv)))}
+        _SLICE_LIMIT.update(seed=seed, dev=t, **{name: G.bits(x) for name, x in t.items()})
+    return _SLICE_LIMIT
+
+
+@pytest.mark.parametrize("mode", [INTRA, MIX], ids=["intra", "mix"])
+def test_forward_at_the_slice_limit(mode):
+    """q and o as large as the boundary accepts: B=1, L=32752, n=4 (N=131008), Hq=64,
+    Hkv=8, D=128 puts 2146435072 bytes of q in the batch slice, just under the 2^31 bytes
+    that the kernels' 32-bit buffer offsets address.  Sampled rows, among them the last
+    rows of the sequence in the last head, against the oracle.  (The backward's dS
+    workspace grows as N^2 and does not fit at this length.)"""
+    B, L, n, Hq, Hkv, D = 1, 32752, 4, 64, 8, 128
+    N = n * L
+    assert N * Hq * D * 2 < 2 ** 31 <= (N + 64) * Hq * D * 2
+    print(f"slice limit mode={mode} N={N} Hq={Hq}: drawing inputs", flush=True)
+    ins = _slice_limit_inputs(N, Hq, Hkv, D)
+    seed, q, k, v = ins["seed"], ins["q"], ins["k"], ins["v"]
+    print(f"slice limit mode={mode} seed={seed}: forward", flush=True)
+    import paper_2607_08186_amd as hd
+    import torch
+
+    o, lse = hd.sfa_forward(*(ins["dev"][x] for x in "qkv"), n=n, mode=mode, scale=D ** -0.5)
+    torch.cuda.synchronize()
+    rng = np.random.default_rng((seed + mode) & 0xFFFFFFFF)
+    rows = {(0, Hq - 1, N - 1), (0, 0, N - 1), (0, Hq - 1, N - 2), (0, 31, N - 5), (0, 0, 0)}
+    while len(rows) < 24:
+        rows.add((0, int(rng.integers(Hq)), int(rng.integers(N - 2048, N))))
+    while len(rows) < 40:
+        rows.add((0, int(rng.integers(Hq)), int(rng.integers(N))))
+    rows = np.array(sorted(rows), dtype=np.int64)
+    ro, rl = oracle.sfa_fwd_rows(q, k, v, rows, L=L, n=n, mode=mode, scale=D ** -0.5)
+    b, h, p = (torch.as_tensor(x, device=o.device) for x in rows.T)
+    oh = G.to_host64(o[b, p, h])
+    lh = G.to_host64(lse[b, h, p])
+    G.assert_close_fwd(oh, lh, ro, rl, "bf16", "slice limit")
