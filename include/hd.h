@@ -12,12 +12,15 @@
  *     dense and row-major in the layouts stated per function.
  *   - The library never allocates, frees or synchronises device memory.  Work is
  *     enqueued on `stream` (0 = the null stream) and the call returns after enqueue.
- *     Outputs are overwritten, never accumulated into.
+ *     Outputs are overwritten, never accumulated into (hd_embed_grad_scatter_add, whose
+ *     purpose is to add into a dense gradient, is the one exception).
  *   - Arguments are validated on the host before anything is enqueued.  On a
  *     non-HD_OK return nothing has been enqueued, except for HD_ERR_HIP, which
  *     reports a launch failure; hd_last_error() then holds a readable detail.
- *   - Per-batch slices of every tensor must stay below 2^31 bytes (32-bit offsets
- *     inside the kernels); larger inputs are rejected with HD_ERR_INVALID_ARG.
+ *   - Per-batch slices of the attention tensors (q, k, v, o, dO, dq, dk, dv and the
+ *     decode caches) must stay below 2^31 bytes (32-bit offsets inside the kernels);
+ *     larger inputs are rejected with HD_ERR_INVALID_ARG.  The expansion, its
+ *     gradient and the final-stream gather state their own limits.
  *   - Calls are thread-safe with respect to each other; calls that write the same
  *     output buffers on overlapping streams race, as with any kernel.
  */
