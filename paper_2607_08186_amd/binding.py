@@ -102,6 +102,8 @@ def _ptr(x):
         return None
     if isinstance(x, int):
         return x
+    if not x.is_cuda:
+        raise ValueError("tensors passed to libhd must live on the GPU (device pointers)")
     if not x.is_contiguous():
         raise ValueError("tensors passed to libhd must be contiguous")
     return x.data_ptr()

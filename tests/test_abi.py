@@ -367,3 +367,17 @@ def test_final_stream_gather_validation(lib, args, code, backward):
         st = lib.hd_final_stream_gather(a["src"], a["dst"], a["B"], a["L"], a["n"], a["Dm"],
                                         a["dtype"], None)
     assert st == code
+
+
+def test_binding_rejects_host_and_strided_tensors(lib):
+    """Host tensors would hand the kernels host addresses, strided views a layout they do
+    not read: both are refused in the binding before any call."""
+    import torch
+
+    q = torch.zeros((1, 8, 2, 32), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU"):
+        binding.hd_sfa_fwd(q, q, q, q, q, 1, 4, 2, 2, 2, 32, 0, 0.125)
+    with pytest.raises(ValueError, match="GPU"):
+        binding.final_stream_gather(torch.zeros((1, 8, 16)), 2)
+    with pytest.raises(ValueError, match="GPU"):
+        binding.expand_embed(torch.zeros((1, 4), dtype=torch.int32), torch.zeros((2, 5, 8)))
