@@ -3,7 +3,9 @@ batch, length, stream count, grouped-query ratio, head dim, layer type (intra-st
 full and local cross-stream, final-stream full and local) and window, each forward and
 backward against the fp64 oracle at the bf16 tolerances (max |O - O_ref| and
 max |lse - lse_ref| <= 2e-2; max |g - g_ref| / max |g_ref| <= 5e-2 for dQ, dK, dV).
-The list is drawn once from a fixed seed, so every run checks the same cases."""
+Decode steps are drawn the same way (batch, cache capacity, ragged per-sequence contexts,
+mask, window, heads).  The lists are drawn once from fixed seeds, so every run checks the
+same cases."""
 import math
 
 import numpy as np
@@ -69,3 +71,42 @@ def test_random_shape_parity(case):
     G.assert_close_fwd(G.to_host64(o), G.to_host64(lse), ro, rl, "bf16", str(case))
     for name, got, ref in (("dq", dq, rdq), ("dk", dk, rdk), ("dv", dv, rdv)):
         G.assert_close_grad(G.to_host64(got), ref, "bf16", name, str(case))
+
+
+def _draw_decode(count=16, seed=20261203):
+    r = np.random.default_rng(seed)
+    cases = []
+    for _ in range(count):
+        mode = int(r.integers(3))
+        n = int(r.integers(1, 9))
+        B = int(r.integers(1, 5))
+        Lcap = int(r.integers(1, 1500))
+        Hkv = int(r.integers(1, 3))
+        Hq = Hkv * int(r.choice([1, 2, 4, 8]))
+        D = int(r.choice([32, 64, 128]))
+        window = int(r.integers(1, 2 * n * Lcap + 2)) if mode == LOCAL else 0
+        ctx = [int(c) for c in r.integers(0, Lcap, size=B)]
+        cases.append((mode, B, Lcap, n, Hq, Hkv, D, window, ctx))
+    return cases
+
+
+DECODE_CASES = _draw_decode()
+
+
+@pytest.mark.parametrize("case", DECODE_CASES,
+                         ids=[f"m{c[0]}-B{c[1]}-Lcap{c[2]}-n{c[3]}-Hq{c[4]}-Hkv{c[5]}-D{c[6]}-w{c[7]}"
+                              for c in DECODE_CASES])
+def test_random_decode_parity(case):
+    mode, B, Lcap, n, Hq, Hkv, D, window, ctx = case
+    seed = synth.seed_for("random_decode", str(case))
+    print(f"random decode {case} seed={seed}", flush=True)
+    to = synth.to_bf16_bits
+    q = to(synth.normal(seed, (B, n, Hq, D), 2 ** -0.5))
+    k = to(synth.normal(seed + 1, (B, n * Lcap, Hkv, D), 2 ** -0.5))
+    v = to(synth.normal(seed + 2, (B, n * Lcap, Hkv, D), 2 ** -0.5))
+    tctx = torch.from_numpy(np.asarray(ctx, dtype=np.int32)).to(G.dev())
+    o, lse = hd.sfa_decode(G.to_dev(q), G.to_dev(k), G.to_dev(v), tctx, max_ctx=max(ctx),
+                           mode=mode, window=window)
+    torch.cuda.synchronize()
+    ro, rl = oracle.sfa_decode(q, k, v, ctx, n=n, mode=mode, scale=D ** -0.5, window=window)
+    G.assert_close_fwd(G.to_host64(o), G.to_host64(lse), ro, rl, "bf16", str(case))
