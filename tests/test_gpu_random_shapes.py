@@ -4,7 +4,7 @@ full and local cross-stream, final-stream full and local) and window, each forwa
 backward against the fp64 oracle at the bf16 tolerances (max |O - O_ref| and
 max |lse - lse_ref| <= 2e-2; max |g - g_ref| / max |g_ref| <= 5e-2 for dQ, dK, dV).
 Decode steps are drawn the same way (batch, cache capacity, ragged per-sequence contexts,
-mask, window, heads).  The lists are drawn once from fixed seeds, so every run checks the
+mask, window, heads), and fp32-path shapes (max error <= 1e-4 on every output).  The lists are drawn once from fixed seeds, so every run checks the
 same cases."""
 import math
 
@@ -110,3 +110,41 @@ def test_random_decode_parity(case):
     torch.cuda.synchronize()
     ro, rl = oracle.sfa_decode(q, k, v, ctx, n=n, mode=mode, scale=D ** -0.5, window=window)
     G.assert_close_fwd(G.to_host64(o), G.to_host64(lse), ro, rl, "bf16", str(case))
+
+
+def _draw_f32(count=8, seed=20261204):
+    r = np.random.default_rng(seed)
+    cases = []
+    for _ in range(count):
+        mode = int(r.integers(3))
+        n = int(r.integers(1, 6))
+        L = int(r.integers(1, 300 // n + 1))
+        B = int(r.integers(1, 3))
+        Hkv = int(r.integers(1, 3))
+        Hq = Hkv * int(r.choice([1, 2, 4]))
+        D = int(r.choice([32, 64, 128]))
+        window = int(r.integers(1, 2 * n * L + 2)) if mode == LOCAL else 0
+        cases.append((mode, B, L, n, Hq, Hkv, D, window))
+    return cases
+
+
+F32_CASES = _draw_f32()
+
+
+@pytest.mark.parametrize("case", F32_CASES,
+                         ids=[f"m{c[0]}-B{c[1]}-L{c[2]}-n{c[3]}-Hq{c[4]}-Hkv{c[5]}-D{c[6]}-w{c[7]}"
+                              for c in F32_CASES])
+def test_random_f32_parity(case):
+    """The fp32 path at its 1e-4 bar (same forms as the bf16 one)."""
+    mode, B, L, n, Hq, Hkv, D, window = case
+    seed = synth.seed_for("random_f32", str(case))
+    print(f"random f32 {case} seed={seed}", flush=True)
+    scale = 1.0 / math.sqrt(D)
+    ins = synth.sfa_inputs(B, L, n, Hq, Hkv, D, seed=seed, dtype="f32")
+    got = G.run_sfa(ins, n, mode, scale, window=window if mode == LOCAL else None)
+    kw = dict(L=L, n=n, mode=mode, scale=scale, window=window)
+    ro, rl = oracle.sfa_fwd(ins["q"], ins["k"], ins["v"], **kw)
+    rdq, rdk, rdv = oracle.sfa_bwd(ins["q"], ins["k"], ins["v"], ins["dout"], **kw)
+    G.assert_close_fwd(G.to_host64(got["o"]), G.to_host64(got["lse"]), ro, rl, "f32", str(case))
+    for name, ref in (("dq", rdq), ("dk", rdk), ("dv", rdv)):
+        G.assert_close_grad(G.to_host64(got[name]), ref, "f32", name, str(case))
