@@ -18,8 +18,10 @@ import subprocess
 import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-_SRC = os.path.join(_HERE, "sfa_oracle.c")
-_LIB = os.path.join(_HERE, "liboracle.so")
+# HD_ORACLE_SRC / HD_ORACLE_LIB point the module at another build of the oracle (the
+# mutation tests use them to check that the pins catch planted mistakes)
+_SRC = os.environ.get("HD_ORACLE_SRC") or os.path.join(_HERE, "sfa_oracle.c")
+_LIB = os.environ.get("HD_ORACLE_LIB") or os.path.join(_HERE, "liboracle.so")
 
 INTRA, MIX, LOCAL = 0, 1, 2
 _F64, _F32, _BF16 = 0, 1, 2
