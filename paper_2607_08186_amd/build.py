@@ -17,7 +17,7 @@ HEADERS = ["hd_internal.h", "hd_device.h", "sfa_lds.h", "embed_internal.h", "dec
 
 ARCH = "gfx950"
 # Packed fp32 VALU ops are kept off: plain fp32 code only.
-FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall",
+FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-Wall", "-Wextra",
          "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
 
 

@@ -218,7 +218,7 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     __syncthreads();
 #pragma unroll
     for (int j = 0; j < kItems; ++j)
-        if (threadIdx.x * kItems + j < valid) atomicAdd(&h[(k[j] >> shift) & 255], 1);
+        if ((int)threadIdx.x * kItems + j < valid) atomicAdd(&h[(k[j] >> shift) & 255], 1);
     __syncthreads();
     int tot;
     const int start = block_exclusive_scan(h[threadIdx.x], &tot, sh);
