@@ -18,7 +18,9 @@
 //          stored, as 64 x 128 tiles in the workspace.
 //   dQ:    dQ = scale dS K from the stored tiles: a workgroup owns 256 query rows (32
 //          per wave, one row per lane) and streams the dS tiles and key rows at or
-//          below the diagonal through a three-stage LDS ring, dQ^T += K^T dS^T with
+//          below the diagonal through an LDS ring (32 keys x 2 stages, two
+//          workgroups per CU, on grids of more than two workgroups per CU; else
+//          64 keys x 3 stages), dQ^T += K^T dS^T with
 //          both operands read transposed from LDS.  No S or dP is recomputed, so this
 //          pass is bound by the dS reads from HBM.
 // All tiles move HBM -> LDS through direct-to-LDS buffer loads.
@@ -335,18 +337,23 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     }
 }
 
-template <int D>
+// KK keys per ring step, S ring stages.  <32, 2> takes 48 KB of LDS at D=128, so two
+// workgroups share a CU and each one's loads overlap the other's MFMAs; <64, 3> takes
+// 144 KB, one workgroup per CU, and wins when the whole grid would otherwise be resident
+// at once (the dispatcher then cannot pair long causal row blocks with short ones).
+template <int D, int KK, int S>
 __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const bf16 *__restrict__ k, const bf16 *__restrict__ ds, bf16 *__restrict__ dq, SfaGeom g,
     int64_t ds_tiles)
 {
     constexpr int DB = D / 32;
-    constexpr int kStages = 3;
-    using T = Tile<D>;
-    // a wave's dS slab of one 64-key step: 64 keys x 32 queries, 64 bytes per key
-    constexpr int kSlab = kRows * 64;
+    static_assert(kDsKeys % KK == 0 && KK % 16 == 0 && S >= 2, "ring shape");
+    using T = Tile<D, KK>;
+    // a wave's dS slab of one step: KK keys x 32 queries, 64 bytes per key
+    constexpr int kSlab = KK * 64;
     constexpr int kStage = T::BYTES + kDqWaves * kSlab;  // K rows | dS slabs
-    __shared__ __attribute__((aligned(1024))) char smem[kStages][kStage];
+    static_assert(S * kStage <= 160 * 1024, "the ring must fit in LDS");
+    __shared__ __attribute__((aligned(1024))) char smem[S][kStage];
 
     const int ntiles = (g.qlen + kRowsPerWg - 1) / kRowsPerWg;
     const int nprob = g.B * g.Hq * g.streams;
@@ -379,31 +386,37 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
 
     // keys of the block: up to the key coordinate of its last query row
     const int kend = min(g.len, qpos(g, min(q0 + kRowsPerWg, g.qlen) - 1) + 1);
-    const int nkt = (kend + kRows - 1) / kRows;
-    // first key tile any row of the workgroup sees (0 unless the layer is local)
-    const int jf = max(0, qpos(g, q0) - g.window + 1) / kRows;
-    // wave-uniform: 64-key tile j holds a key that a row of this wave sees (then the dS
+    const int nkt = (kend + KK - 1) / KK;
+    // first key step any row of the workgroup sees (0 unless the layer is local)
+    const int jf = max(0, qpos(g, q0) - g.window + 1) / KK;
+    // wave-uniform: key step j holds a key that a row of this wave sees (then the dS
     // tile that holds it exists)
     auto active = [&](int j) __attribute__((always_inline)) {
-        const int kb0 = j * kRows;
+        const int kb0 = j * KK;
         return wrow_min < g.qlen && kb0 <= qpos(g, wrow_max) &&
-               qpos(g, wrow_min) - (kb0 + kRows - 1) < g.window;
+               qpos(g, wrow_min) - (kb0 + KK - 1) < g.window;
     };
+    constexpr int kSteps = kDsKeys / KK;  // key steps per dS tile
     const int kloads = loads_per_wave(T::INSTR, wave, kDqWaves);
+    // this wave's loads of step j (in-order completion makes counts enough to wait on)
     auto nloads = [&](int j) __attribute__((always_inline)) {
-        return j < nkt ? kloads + (active(j) ? 4 : 0) : 0;
+        return j < nkt ? kloads + (active(j) ? kSlab / 1024 : 0) : 0;
     };
+    static_assert((S - 2) * (T::INSTR / kDqWaves + 1 + kSlab / 1024) <= 15,
+                  "outstanding loads must fit the vmcnt wait");
     auto issue = [&](int j) __attribute__((always_inline)) {
         if (j >= nkt) return;
-        char *st = smem[(j - jf) % kStages];
-        T::load(st, rk, kbase, kstride, j * kRows, g.len, wave, kDqWaves, lane);
+        char *st = smem[(j - jf) % S];
+        T::load(st, rk, kbase, kstride, j * KK, g.len, wave, kDqWaves, lane);
         if (active(j)) {
-            const int64_t t = ds_tile_index(band, kt_lo, qt, j >> 1);
+            const int64_t t = ds_tile_index(band, kt_lo, qt, j / kSteps);
             const rsrc_t rt = make_rsrc(ds_prob + t * (kDsTileBytes / 2), kDsTileBytes);
             char *slab = st + T::BYTES + wave * kSlab;
-            const uint32_t off = (uint32_t)((wave & 1) * kDsKeys + (j & 1) * kRows) * 64 + lane * 16;
+            const uint32_t off =
+                (uint32_t)((wave & 1) * kDsKeys + (j % kSteps) * KK) * 64 + lane * 16;
 #pragma unroll
-            for (int oc = 0; oc < 4; ++oc) dma_lds16_nt(rt, slab + oc * 1024, off + oc * 1024);
+            for (int oc = 0; oc < kSlab / 1024; ++oc)
+                dma_lds16_nt(rt, slab + oc * 1024, off + oc * 1024);
         }
     };
 
@@ -421,17 +434,24 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
 #pragma unroll
     for (int db = 0; db < DB; ++db) adq[db] = f32x16{};
 
-    issue(jf);
-    issue(jf + 1);
-    wait_vmcnt_le(nloads(jf + 1));
+    // steps jf .. jf+S-2 in flight; step j's stage is free again once every wave has
+    // passed the barrier that ends step j - 1
+#pragma unroll
+    for (int i = 0; i < S - 1; ++i) issue(jf + i);
+    {
+        int pend = 0;
+#pragma unroll
+        for (int i = 1; i < S - 1; ++i) pend += nloads(jf + i);
+        wait_vmcnt_le(pend);
+    }
     lds_barrier();
     for (int j = jf; j < nkt; ++j) {
-        issue(j + 2);
+        issue(j + S - 1);
         if (active(j)) {
-            const char *kt = smem[(j - jf) % kStages];
+            const char *kt = smem[(j - jf) % S];
             const char *slab = kt + T::BYTES + wave * kSlab;
 #pragma unroll
-            for (int kk = 0; kk < kRows / 16; ++kk) {
+            for (int kk = 0; kk < KK / 16; ++kk) {
                 const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
                     (lds_v4i16 *)(slab + dso + kk * 1024));
                 const v4i16 hi8 = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
@@ -442,8 +462,14 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
                 for (int db = 0; db < DB; ++db) adq[db] = mfma32(T::tr_at(kt, kto[db], kk), bop, adq[db]);
             }
         }
-        // tile j + 1 has landed once at most the loads of tile j + 2 are outstanding
-        wait_vmcnt_le(nloads(j + 2));
+        // step j + 1 has landed once at most the loads of steps j + 2 .. j + S - 1 are
+        // outstanding
+        {
+            int pend = 0;
+#pragma unroll
+            for (int i = 2; i < S; ++i) pend += nloads(j + i);
+            wait_vmcnt_le(pend);
+        }
         lds_barrier();
     }
 
@@ -483,9 +509,16 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o
     timing_after(s);
     if (e != hipSuccess) return e;
     const int nqt = (g.qlen + kRowsPerWg - 1) / kRowsPerWg;
+    const int wgs = nqt * g.B * g.Hq * g.streams;
+    int dev = 0, cus = 0;
+    if ((e = hipGetDevice(&dev)) != hipSuccess ||
+        (e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
+        return e;
     timing_before(dq_name, s);
-    sfa_dq_bf16_kernel<D><<<nqt * g.B * g.Hq * g.streams, kDqWaves * 64, 0, s>>>(k, ds, dq, g,
-                                                                                 ds_tiles);
+    if (wgs > 2 * cus)
+        sfa_dq_bf16_kernel<D, 32, 2><<<wgs, kDqWaves * 64, 0, s>>>(k, ds, dq, g, ds_tiles);
+    else
+        sfa_dq_bf16_kernel<D, 64, 3><<<wgs, kDqWaves * 64, 0, s>>>(k, ds, dq, g, ds_tiles);
     e = hipGetLastError();
     timing_after(s);
     return e;
