@@ -17,6 +17,9 @@ from tests import gpu_helpers as G
 pytestmark = [pytest.mark.gpu, pytest.mark.slow]
 
 INTRA, MIX, LOCAL = 0, 1, 2
+# The dQ launch picks its LDS ring by grid size: the n=1 sweep shapes (512 workgroups,
+# two per CU on 256 CUs) take the one-workgroup-per-CU ring, the others the ring that
+# puts two workgroups on a CU, so both are checked here at full size.
 CASES = [workloads.QWEN8B, *workloads.SWEEP, workloads.FRONTIER]
 
 
