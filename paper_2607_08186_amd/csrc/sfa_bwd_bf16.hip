@@ -18,12 +18,13 @@
 //          stored, as 64 x 128 tiles in the workspace.
 //   dQ:    dQ = scale dS K from the stored tiles: a workgroup owns 256 query rows (32
 //          per wave, one row per lane) and streams the dS tiles and key rows at or
-//          below the diagonal through an LDS ring (32 keys x 2 stages, two
-//          workgroups per CU, on grids of more than two workgroups per CU; else
-//          64 keys x 3 stages), dQ^T += K^T dS^T with
+//          below the diagonal through an LDS ring (32 keys x 2 stages, several
+//          workgroups per CU, unless that would make the whole grid resident at
+//          once; then 64 keys x 3 stages), dQ^T += K^T dS^T with
 //          both operands read transposed from LDS.  No S or dP is recomputed, so this
 //          pass is bound by the dS reads from HBM.
 // All tiles move HBM -> LDS through direct-to-LDS buffer loads.
+#include <atomic>
 #include <type_traits>
 
 #include "sfa_lds.h"
@@ -510,12 +511,21 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o
     if (e != hipSuccess) return e;
     const int nqt = (g.qlen + kRowsPerWg - 1) / kRowsPerWg;
     const int wgs = nqt * g.B * g.Hq * g.streams;
-    int dev = 0, cus = 0;
+    // the co-resident ring, unless the whole grid would then be resident at once
+    static std::atomic<int> co_resident{0};  // its workgroups per CU (a property of the code)
+    int dev = 0, cus = 0, per_cu = co_resident.load(std::memory_order_relaxed);
+    if (per_cu == 0) {
+        if ((e = hipOccupancyMaxActiveBlocksPerMultiprocessor(
+                 &per_cu, reinterpret_cast<const void *>(&sfa_dq_bf16_kernel<D, 32, 2>),
+                 kDqWaves * 64, 0)) != hipSuccess)
+            return e;
+        co_resident.store(per_cu, std::memory_order_relaxed);
+    }
     if ((e = hipGetDevice(&dev)) != hipSuccess ||
         (e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
         return e;
     timing_before(dq_name, s);
-    if (wgs > 2 * cus)
+    if ((int64_t)wgs > (int64_t)per_cu * cus)
         sfa_dq_bf16_kernel<D, 32, 2><<<wgs, kDqWaves * 64, 0, s>>>(k, ds, dq, g, ds_tiles);
     else
         sfa_dq_bf16_kernel<D, 64, 3><<<wgs, kDqWaves * 64, 0, s>>>(k, ds, dq, g, ds_tiles);
