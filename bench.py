@@ -281,6 +281,11 @@ def main():
     for _ in range(args.warmup):
         step()
     elapsed, ktimes, dom = time_steps(hd, torch, step, args.steps)
+    per_mode = copy_ceiling = None
+    if args.workload == "stack36":
+        per_mode = time_layer_modes(hd, torch, layers, s, scale, dq, dk, dv, ws, ws_bytes,
+                                    stream, W)
+        copy_ceiling = time_copy(torch, emb, stream)
 
     if final:
         flop_step = sum(14 * s.D * W.visible_pairs_final(s, window if m == W.LOCAL else 0)
@@ -328,6 +333,9 @@ def main():
             nbytes = W.embed_bytes(1, s.L, s.n, W.STACK_DMODEL)
             ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
             ent["bytes_per_launch"] = nbytes
+            if copy_ceiling is not None:
+                ent["copy_gbs"] = copy_ceiling["gbs"]
+                ent["of_copy"] = round(ent["gbs"] / copy_ceiling["gbs"], 3)
         if fam in ("final_gather", "final_gather_bwd"):
             nbytes = W.final_gather_bytes(1, s.L, s.n, W.STACK_DMODEL, fam == "final_gather_bwd")
             ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
@@ -351,9 +359,62 @@ def main():
         "roofline": roofline, "breakdown": breakdown, "per_kernel": per_kernel,
         "input_gen_s": round(t_gen, 2),
     }
+    if per_mode is not None:
+        out["per_mode"] = per_mode
+    if copy_ceiling is not None:
+        out["copy_ceiling"] = copy_ceiling
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(args.cpu_sample_tokens)
+        out["cpu_baseline"] = cpu_baseline(args.cpu_sample_tokens, flop_step, ms_per_step)
     print(json.dumps(out), flush=True)
+
+
+def time_layer_modes(hd, torch, layers, s, scale, dq, dk, dv, ws, ws_bytes, stream, W, reps=10):
+    """fwd+bwd of one intra-stream and one mixing layer of the step (its first layer of
+    each kind, same inputs), each alone: `reps` back-to-back passes between two events
+    on the launch stream, after one untimed pass."""
+    res = {}
+    for mode in (W.INTRA, W.MIX):
+        ly = next(x for x in layers if x["mode"] == mode)
+
+        def one():
+            hd.hd_sfa_fwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L, s.n, s.Hq,
+                          s.Hkv, s.D, mode, scale, stream=stream)
+            hd.hd_sfa_bwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq, dk, dv,
+                          s.B, s.L, s.n, s.Hq, s.Hkv, s.D, mode, scale, ws, ws_bytes,
+                          stream=stream)
+
+        one()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(reps):
+            one()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        ms = t0.elapsed_time(t1) / reps
+        tf = W.useful_flop(s, mode) / (ms * 1e-3) / 1e12
+        res[W.MODE_NAMES[mode]] = {"ms": round(ms, 4), "tflops": round(tf, 2),
+                                   "frac_of_peak": round(tf / W.MI355X_BF16_PEAK_TFLOPS, 4),
+                                   "useful_tflop": round(W.useful_flop(s, mode) / 1e12, 4),
+                                   "reps": reps}
+    return res
+
+
+def time_copy(torch, emb, stream, reps=20):
+    """A plain device-to-device copy of as many bytes as the expansion writes (read +
+    write counted), timed like the expansion: the HBM ceiling it is compared with."""
+    src = emb.view(-1)
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for _ in range(reps):
+        dst.copy_(src)
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms = t0.elapsed_time(t1) / reps
+    nbytes = 2 * src.numel() * src.element_size()
+    return {"bytes": nbytes, "ms": round(ms, 5), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
+            "what": "torch copy_ of the expansion's output size (read + write bytes)"}
 
 
 DECODE_BATCH = 16  # sequences decoded together
@@ -487,9 +548,25 @@ def measured_traffic(kernel, workload):
     return int(float(kv["hbm_bytes_per_launch"]))
 
 
-def cpu_baseline(Ls):
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
+def cpu_baseline(Ls, flop_step, ms_step):
     """The fp64 oracle on a bounded sample of the same workload: one intra-stream and
-    one mixing layer of the stack, fwd + bwd, all 32 query heads, first Ls tokens."""
+    one mixing layer of the stack, fwd + bwd, all 32 query heads, first Ls tokens, on
+    every thread this process may use (forward and backward both parallel over the 32
+    query heads).  The oracle's cost is proportional to the useful flop it does (it
+    evaluates visible pairs only), so the whole step's oracle time is extrapolated
+    from the sampled rate and labelled as such."""
     import numpy as np  # noqa: F401
 
     import oracle
@@ -510,11 +587,25 @@ def cpu_baseline(Ls):
         flop += W.useful_flop(sh, mode)
         print(f"[bench] cpu oracle mode {mode} done", file=sys.stderr, flush=True)
     dt = time.perf_counter() - t0
-    return {"value": round(flop / dt / 1e12, 6), "unit": "TFLOP/s", "cores": nthreads,
+    rate = flop / dt
+    try:
+        affinity = len(os.sched_getaffinity(0))
+    except AttributeError:
+        affinity = None
+    step_s = flop_step / rate
+    return {"value": round(rate / 1e12, 6), "unit": "TFLOP/s", "cores": nthreads,
             "kind": "oracle", "seconds": round(dt, 2),
+            "threads": nthreads, "nproc": os.cpu_count(), "affinity_cpus": affinity,
+            "omp_num_threads": os.environ.get("OMP_NUM_THREADS"), "cpu_model": _cpu_model(),
             "sample": (f"one intra + one mix layer, fwd+bwd, B=1 L={Ls} n={sh.n} "
                        f"Hq={sh.Hq} Hkv={sh.Hkv} D={sh.D} (prefix of the step's layer shape), "
-                       f"fp64, {nthreads} threads (bwd parallel over {sh.Hkv} kv-heads)")}
+                       f"fp64, {nthreads} threads, fwd and bwd parallel over the {sh.Hq} "
+                       "query heads"),
+            "extrapolated_step_s": round(step_s, 1),
+            "extrapolated_step_vs_gpu": round(step_s * 1e3 / ms_step, 1),
+            "extrapolation": ("EXTRAPOLATED, not measured: the whole step's useful flop "
+                              "divided by the sampled oracle rate (the oracle's cost is "
+                              "proportional to the visible pairs it evaluates)")}
 
 
 if __name__ == "__main__":

@@ -76,7 +76,15 @@ def _load():
 
 
 def default_threads() -> int:
-    return max(1, min(16, os.cpu_count() or 1))
+    """Every thread this process may use: OMP_NUM_THREADS when set (shared GPU hosts
+    set it to the CPU share of one GPU), else the CPUs of the affinity mask."""
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    if env.isdigit() and int(env) > 0:
+        return int(env)
+    try:
+        return max(1, len(os.sched_getaffinity(0)))
+    except AttributeError:
+        return max(1, os.cpu_count() or 1)
 
 
 def _dtype_code(a: np.ndarray) -> int:

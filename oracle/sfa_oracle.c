@@ -314,50 +314,62 @@ void oracle_sfa_fwd_rows(const void *q, const void *k, const void *v, int dtype,
 
 /* ----------------------------------------------------------- backward */
 
-/* unit = one (b, hk) key/value head: all query heads of its group, all rows */
+/* unit = one (b, hq) query head, all its rows; dq is written in place and the head's
+ * dK/dV contributions go to its own [N][D] buffers (summed per key/value head after
+ * all units have run, in ascending hq order) */
 static void *bwd_job(void *arg)
 {
     job_t *J = arg;
     const problem_t *P = J->P;
-    const int64_t N = P->n * P->L, D = P->D, G = P->Hq / P->Hkv;
-    double *dq = J->out[0], *dk = J->out[1], *dv = J->out[2];
+    const int64_t N = P->n * P->L, D = P->D;
+    double *dq = J->out[0], *dk_part = J->out[3], *dv_part = J->out[4];
     double *x = malloc((size_t)N * sizeof *x);
     double *o = malloc((size_t)D * sizeof *o);
-    double *dk_head = malloc((size_t)(N * D) * sizeof *dk_head);
-    double *dv_head = malloc((size_t)(N * D) * sizeof *dv_head);
     for (int64_t u = J->first; u < J->first + J->count; ++u) {
-        int64_t b = u / P->Hkv, hk = u % P->Hkv;
+        int64_t b = u / P->Hq, hq = u % P->Hq;
+        double *dk_head = dk_part + u * N * D, *dv_head = dv_part + u * N * D;
         memset(dk_head, 0, (size_t)(N * D) * sizeof *dk_head);
         memset(dv_head, 0, (size_t)(N * D) * sizeof *dv_head);
-        for (int64_t hq = hk * G; hq < (hk + 1) * G; ++hq)
-            for (int64_t p = 0; p < N; ++p) {
-                if (!is_query(P, p)) continue;
-                double lse;
-                row_forward(P, b, hq, p, x, o, &lse);
-                row_backward(P, b, hq, p, x, o, &dq[q_index(P, b, p, hq, 0)], dk_head,
-                             dv_head, NULL, 0);
-            }
-        for (int64_t j = 0; j < N; ++j)
-            for (int64_t d = 0; d < D; ++d) {
-                dk[kv_index(P, b, j, hk, d)] = dk_head[j * D + d];
-                dv[kv_index(P, b, j, hk, d)] = dv_head[j * D + d];
-            }
+        for (int64_t p = 0; p < N; ++p) {
+            if (!is_query(P, p)) continue;
+            double lse;
+            row_forward(P, b, hq, p, x, o, &lse);
+            row_backward(P, b, hq, p, x, o, &dq[q_index(P, b, p, hq, 0)], dk_head, dv_head,
+                         NULL, 0);
+        }
     }
     free(x);
     free(o);
-    free(dk_head);
-    free(dv_head);
     return NULL;
 }
 
-/* Full backward from (q, k, v, dO): dq [B][N][Hq][D], dk/dv [B][N][Hkv][D]. */
+/* Full backward from (q, k, v, dO): dq [B][N][Hq][D], dk/dv [B][N][Hkv][D].  Threads
+ * take whole query heads; dk/dv of a key/value head are the sum of its group's query
+ * heads, added in ascending head order. */
 void oracle_sfa_bwd(const void *q, const void *k, const void *v, const void *dout, int dtype,
                     double *dq, double *dk, double *dv, int64_t B, int64_t L, int64_t n,
                     int64_t Hq, int64_t Hkv, int64_t D, int mode, int64_t window, double scale, int nthreads)
 {
     problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, window, scale);
-    job_t J = {&P, 0, 0, {dq, dk, dv}, NULL, 0};
-    run_jobs(bwd_job, &J, B * Hkv, nthreads);
+    const int64_t N = n * L, G = Hq / Hkv;
+    double *dk_part = malloc((size_t)(B * Hq * N * D) * sizeof *dk_part);
+    double *dv_part = malloc((size_t)(B * Hq * N * D) * sizeof *dv_part);
+    job_t J = {&P, 0, 0, {dq, NULL, NULL, dk_part, dv_part}, NULL, 0};
+    run_jobs(bwd_job, &J, B * Hq, nthreads);
+    for (int64_t b = 0; b < B; ++b)
+        for (int64_t hk = 0; hk < Hkv; ++hk)
+            for (int64_t j = 0; j < N; ++j)
+                for (int64_t d = 0; d < D; ++d) {
+                    double sk = 0.0, sv = 0.0;
+                    for (int64_t hq = hk * G; hq < (hk + 1) * G; ++hq) {
+                        sk += dk_part[((b * Hq + hq) * N + j) * D + d];
+                        sv += dv_part[((b * Hq + hq) * N + j) * D + d];
+                    }
+                    dk[kv_index(&P, b, j, hk, d)] = sk;
+                    dv[kv_index(&P, b, j, hk, d)] = sv;
+                }
+    free(dk_part);
+    free(dv_part);
 }
 
 /* unit = one listed query row (b, hq, p) */
@@ -391,25 +403,36 @@ void oracle_sfa_bwd_dq_rows(const void *q, const void *k, const void *v, const v
     run_jobs(dq_rows_job, &J, nrows, nthreads);
 }
 
-/* unit = one listed key row (b, hk, j): sum over the group's query heads and rows */
-static void *dkdv_rows_job(void *arg)
+/* dK/dV of the listed keys of one key/value head (b, hk).  Work units are the query
+ * rows (hq, p) of its group; thread t takes units t, t + nthreads, ... (causal rows
+ * differ in length) and adds each row's contributions to the listed keys into its own
+ * [nkeys][D] buffers; the threads' buffers are summed in thread order afterwards.
+ * Every query row's probabilities are formed once for all listed keys. */
+typedef struct {
+    const problem_t *P;
+    int64_t b, hk, tid, nthreads;
+    const int64_t *keys;
+    int64_t nkeys;
+    double *dk, *dv; /* this thread's [nkeys][D] */
+} keyjob_t;
+
+static void *dkdv_keys_job(void *arg)
 {
-    job_t *J = arg;
+    keyjob_t *J = arg;
     const problem_t *P = J->P;
     const int64_t N = P->n * P->L, D = P->D, G = P->Hq / P->Hkv;
-    double *dk = J->out[0], *dv = J->out[1];
     double *x = malloc((size_t)N * sizeof *x);
     double *o = malloc((size_t)D * sizeof *o);
-    for (int64_t r = J->first; r < J->first + J->count; ++r) {
-        const int64_t b = J->rows[3 * r], hk = J->rows[3 * r + 1], j = J->rows[3 * r + 2];
-        for (int64_t d = 0; d < D; ++d) dk[r * D + d] = dv[r * D + d] = 0.0;
-        for (int64_t hq = hk * G; hq < (hk + 1) * G; ++hq)
-            for (int64_t p = 0; p < N; ++p) {
-                if (!is_query(P, p) || !visible(P->mode, P->n, P->window, p, j)) continue;
-                double lse;
-                row_forward(P, b, hq, p, x, o, &lse);
-                row_backward(P, b, hq, p, x, o, NULL, &dk[r * D], &dv[r * D], &j, 1);
-            }
+    for (int64_t u = J->tid; u < G * N; u += J->nthreads) {
+        const int64_t hq = J->hk * G + u / N, p = u % N;
+        if (!is_query(P, p)) continue;
+        int sees = 0; /* does this row see any listed key? */
+        for (int64_t r = 0; r < J->nkeys && !sees; ++r)
+            sees = visible(P->mode, P->n, P->window, p, J->keys[r]);
+        if (!sees) continue;
+        double lse;
+        row_forward(P, J->b, hq, p, x, o, &lse);
+        row_backward(P, J->b, hq, p, x, o, NULL, J->dk, J->dv, J->keys, J->nkeys);
     }
     free(x);
     free(o);
@@ -423,8 +446,53 @@ void oracle_sfa_bwd_dkdv_rows(const void *q, const void *k, const void *v, const
                               int64_t Hkv, int64_t D, int mode, int64_t window, double scale, int nthreads)
 {
     problem_t P = make_problem(q, k, v, dout, dtype, B, L, n, Hq, Hkv, D, mode, window, scale);
-    job_t J = {&P, 0, 0, {dk_rows, dv_rows}, rows, nrows};
-    run_jobs(dkdv_rows_job, &J, nrows, nthreads);
+    if (nthreads < 1) nthreads = 1;
+    int64_t *keys = malloc((size_t)(nrows > 0 ? nrows : 1) * sizeof *keys);
+    int64_t *slot = malloc((size_t)(nrows > 0 ? nrows : 1) * sizeof *slot);
+    char *done = calloc((size_t)(nrows > 0 ? nrows : 1), 1);
+    pthread_t *th = calloc((size_t)nthreads, sizeof *th);
+    keyjob_t *jobs = calloc((size_t)nthreads, sizeof *jobs);
+    for (int64_t r0 = 0; r0 < nrows; ++r0) {
+        if (done[r0]) continue;
+        const int64_t b = rows[3 * r0], hk = rows[3 * r0 + 1];
+        /* the distinct keys listed for (b, hk); slot[r] = position of row r's key */
+        int64_t nk = 0;
+        for (int64_t r = r0; r < nrows; ++r) {
+            if (rows[3 * r] != b || rows[3 * r + 1] != hk) continue;
+            int64_t s = 0;
+            while (s < nk && keys[s] != rows[3 * r + 2]) ++s;
+            if (s == nk) keys[nk++] = rows[3 * r + 2];
+            slot[r] = s;
+            done[r] = 1;
+        }
+        double *buf = calloc((size_t)(2 * nthreads * nk * D), sizeof *buf);
+        for (int t = 0; t < nthreads; ++t) {
+            keyjob_t j = {&P, b, hk, t, nthreads, keys, nk, buf + (2 * t) * nk * D,
+                          buf + (2 * t + 1) * nk * D};
+            jobs[t] = j;
+        }
+        for (int t = 1; t < nthreads; ++t) pthread_create(&th[t], NULL, dkdv_keys_job, &jobs[t]);
+        dkdv_keys_job(&jobs[0]);
+        for (int t = 1; t < nthreads; ++t) pthread_join(th[t], NULL);
+        for (int64_t r = r0; r < nrows; ++r) {
+            if (rows[3 * r] != b || rows[3 * r + 1] != hk) continue;
+            for (int64_t d = 0; d < D; ++d) {
+                double sk = 0.0, sv = 0.0;
+                for (int t = 0; t < nthreads; ++t) {
+                    sk += jobs[t].dk[slot[r] * D + d];
+                    sv += jobs[t].dv[slot[r] * D + d];
+                }
+                dk_rows[r * D + d] = sk;
+                dv_rows[r * D + d] = sv;
+            }
+        }
+        free(buf);
+    }
+    free(keys);
+    free(slot);
+    free(done);
+    free(th);
+    free(jobs);
 }
 
 /* ---------------------------------------------------- stream expansion */

@@ -265,6 +265,7 @@ def hd_timing_collect(max_entries: int = 64):
 
 # ---------------------------------------------------------------- conveniences
 # Shape inference and output allocation through torch (device memory plumbing only).
+# The softmax scale is a required argument, passed through unchanged.
 
 def _shape(q, k, n):
     B, N, Hq, D = q.shape
@@ -274,13 +275,12 @@ def _shape(q, k, n):
     return B, N // n, Hq, Hkv, D
 
 
-def sfa_forward(q, k, v, *, n, mode, scale=None, window=None, stream=None):
+def sfa_forward(q, k, v, *, n, mode, scale, window=None, stream=None):
     """q [B][n*L][Hq][D], k/v [B][n*L][Hkv][D] -> (o, lse [B][Hq][n*L] fp32).
     ``window`` is required for, and only accepted with, mode HD_SFA_LOCAL."""
     import torch
 
     B, L, Hq, Hkv, D = _shape(q, k, n)
-    scale = scale if scale is not None else D ** -0.5
     o = torch.empty_like(q)
     lse = torch.empty((B, Hq, n * L), dtype=torch.float32, device=q.device)
     if _local(mode, window):
@@ -300,13 +300,12 @@ def _local(mode, window):
     return False
 
 
-def sfa_backward(q, k, v, o, lse, dO, *, n, mode, scale=None, window=None, workspace=None,
+def sfa_backward(q, k, v, o, lse, dO, *, n, mode, scale, window=None, workspace=None,
                  stream=None):
     """-> (dq, dk, dv).  A workspace tensor (uint8, 256-byte aligned) may be passed in."""
     import torch
 
     B, L, Hq, Hkv, D = _shape(q, k, n)
-    scale = scale if scale is not None else D ** -0.5
     dtype = _dtype_code(q, None)
     if _local(mode, window):
         need = hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, window, dtype)
@@ -388,7 +387,7 @@ def final_stream_gather_backward(dout, n, *, stream=None):
     return dh
 
 
-def sfa_final_forward(q, k, v, *, n, window=0, scale=None, stream=None):
+def sfa_final_forward(q, k, v, *, n, scale, window=0, stream=None):
     """Final-stream layer: q [B][L][Hq][D] (final-stream rows), k/v [B][n*L][Hkv][D] ->
     (o [B][L][Hq][D], lse [B][Hq][L] fp32).  window 0: full cross-stream mask."""
     import torch
@@ -397,21 +396,19 @@ def sfa_final_forward(q, k, v, *, n, window=0, scale=None, stream=None):
     Hkv = k.shape[2]
     if k.shape[1] != n * L:
         raise ValueError("k/v must hold n*L expanded rows")
-    scale = scale if scale is not None else D ** -0.5
     o = torch.empty_like(q)
     lse = torch.empty((B, Hq, L), dtype=torch.float32, device=q.device)
     hd_sfa_fwd_final(q, k, v, o, lse, B, L, n, Hq, Hkv, D, window, scale, stream=stream)
     return o, lse
 
 
-def sfa_final_backward(q, k, v, o, lse, dO, *, n, window=0, scale=None, workspace=None,
+def sfa_final_backward(q, k, v, o, lse, dO, *, n, scale, window=0, workspace=None,
                        stream=None):
     """-> (dq [B][L][Hq][D], dk, dv [B][n*L][Hkv][D])."""
     import torch
 
     B, L, Hq, D = q.shape
     Hkv = k.shape[2]
-    scale = scale if scale is not None else D ** -0.5
     need = hd_sfa_bwd_final_workspace_bytes(B, L, n, Hq, Hkv, D, window, _dtype_code(q, None))
     if workspace is None:
         workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
@@ -421,7 +418,7 @@ def sfa_final_backward(q, k, v, o, lse, dO, *, n, window=0, scale=None, workspac
     return dq, dk, dv
 
 
-def sfa_decode(q, k_cache, v_cache, ctx_tokens, *, max_ctx, mode, window=0, scale=None,
+def sfa_decode(q, k_cache, v_cache, ctx_tokens, *, max_ctx, mode, scale, window=0,
                workspace=None, stream=None):
     """Parallel-stream decode: q [B][n][Hq][D] (the new token's n streams), caches
     [B][n*Lcap][Hkv][D], ctx_tokens [B] int32 (device) -> (o [B][n][Hq][D],
@@ -431,7 +428,6 @@ def sfa_decode(q, k_cache, v_cache, ctx_tokens, *, max_ctx, mode, window=0, scal
     B, n, Hq, D = q.shape
     Lcap = k_cache.shape[1] // n
     Hkv = k_cache.shape[2]
-    scale = scale if scale is not None else D ** -0.5
     need = hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, mode, window, max_ctx)
     if workspace is None:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=q.device)

@@ -1,5 +1,6 @@
 // sfa_f32.hip -- fp32 Stream-Factorized Attention forward/backward (with its backward
-// preprocess; the bf16 path forms the same row statistics inside its dQ pass).
+// preprocess, which forms Delta and the base-2 lse of every query row; the bf16 path
+// forms its row statistics in a kernel of its own before the dK/dV pass).
 //
 // The fp32 kernels serve small, accuracy-first workloads: one lane owns one query row
 // (forward, dQ) or one key row (dK/dV), tiles of the other operand are staged in LDS

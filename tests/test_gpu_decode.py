@@ -26,7 +26,8 @@ def _run(ins, ctx, mode, window, max_ctx=None):
     q, k, v = (G.to_dev(ins[x]) for x in ("q", "k", "v"))
     tctx = torch.from_numpy(np.asarray(ctx, dtype=np.int32)).to(G.dev())
     max_ctx = int(np.max(ctx)) if max_ctx is None else max_ctx
-    o, lse = hd.sfa_decode(q, k, v, tctx, max_ctx=max_ctx, mode=mode, window=window)
+    o, lse = hd.sfa_decode(q, k, v, tctx, max_ctx=max_ctx, mode=mode, window=window,
+                           scale=q.shape[-1] ** -0.5)
     torch.cuda.synchronize()
     return G.to_host64(o), G.to_host64(lse)
 
@@ -144,7 +145,7 @@ def test_decode_at_the_cache_slice_limit(mode):
     v = synth.device_normal((B, n * Lcap, Hkv, D), 2 ** -0.5, seed + 2, dev, torch.bfloat16)
     ctx = np.array([Lcap - 1, 100003], dtype=np.int32)
     o, lse = hd.sfa_decode(q, k, v, torch.from_numpy(ctx).to(dev), max_ctx=Lcap - 1, mode=mode,
-                           window=0)
+                           window=0, scale=D ** -0.5)
     torch.cuda.synchronize()
     print("decode slice limit: oracle", flush=True)
     ro, rl = oracle.sfa_decode(G.bits(q), G.bits(k), G.bits(v), ctx, n=n, mode=mode,

@@ -113,7 +113,8 @@ def test_final_stream_deterministic():
 @pytest.mark.parametrize("window", [0, workloads.LOCAL_WINDOW], ids=["full", "local"])
 def test_final_stream_fullsize_sampled(window):
     """Qwen3-8B-like shape (L=4096 final-stream rows over N=16384 keys, Hq=32, Hkv=8,
-    D=128): sampled rows against the oracle, and the softmax gradient sums (the keys'
+    D=128): sampled rows against the oracle (dK/dV of keys across the whole sequence,
+    the first key included, which every final-stream query sees), and the gradient sums (the keys'
     dV add up to the group's summed dO, their dK to zero) over every key."""
     s = workloads.QWEN8B.shape
     seed = synth.seed_for("final_full", window)
@@ -132,12 +133,18 @@ def test_final_stream_fullsize_sampled(window):
     b, h, t = rows.T
     G.assert_close_fwd(got["o"][b, t, h], got["lse"][b, h, t], ro, rl, "bf16", "final")
     G.assert_close_grad(got["dq"][b, t, h], rdq, "bf16", "dq", "final")
-    krows = np.array([(0, int(rng.integers(s.Hkv)), j) for j in
-                      (s.N - 1, s.N - 2, s.N - s.n - 1, s.N - 7)], dtype=np.int64)
-    rdk, rdv = oracle.sfa_bwd_dkdv_rows(ins["q"], ins["k"], ins["v"], ins["dout"], krows, **kw)
-    b, h, j = krows.T
-    G.assert_close_grad(got["dk"][b, j, h], rdk, "bf16", "dk", "final")
-    G.assert_close_grad(got["dv"][b, j, h], rdv, "bf16", "dv", "final")
+    # keys of one key/value head: near the start (seen by every final-stream query, or by
+    # the whole first window), in the first 128-key block, in the middle block, and last
+    hk = int(rng.integers(s.Hkv))
+    heavy = [0, 1, int(rng.integers(2, 128)), s.N // 2 + int(rng.integers(128))]
+    for what, keys in (("heavy keys", heavy), ("last keys", (s.N - 1, s.N - 2, s.N - s.n - 1, s.N - 7))):
+        krows = np.array([(0, hk, j) for j in keys], dtype=np.int64)
+        print(f"  dK/dV of {what}: {krows.tolist()}", flush=True)
+        rdk, rdv = oracle.sfa_bwd_dkdv_rows(ins["q"], ins["k"], ins["v"], ins["dout"], krows,
+                                            **kw)
+        b, h, j = krows.T
+        G.assert_close_grad(got["dk"][b, j, h], rdk, "bf16", "dk", f"final {what}")
+        G.assert_close_grad(got["dv"][b, j, h], rdv, "bf16", "dv", f"final {what}")
     dout = synth.bf16_bits_to_f32(ins["dout"]).astype(np.float64)
     Gq = s.Hq // s.Hkv
     want = dout.reshape(s.B, s.L, s.Hkv, Gq, s.D).sum(axis=(1, 3))

@@ -1,9 +1,14 @@
 """Full-size parity in the launch configuration the benchmark times.
 
-At these sizes the oracle evaluates sampled rows one by one (forward rows, dQ rows,
-and dK/dV rows of keys that only the last tokens see); properties that hold at any
-size check the rest: the gradient sums of softmax attention (sum over keys of dV is the
-group's summed dO; sum over keys of dK is zero), per stream for intra layers.
+At these sizes the oracle evaluates sampled rows one by one: forward rows, dQ rows,
+and dK/dV rows of sampled keys.  The keys come from one key/value head and, where the
+oracle's cost allows it (it forms every query row that sees a listed key, once for all
+of them), span the whole sequence: the first key of a stream, which every query of the
+stream sees, a key of the first 128-key block, one of the middle block, and the last
+keys; elsewhere (the mixing layers at N >= 16384) the keys of the last tokens.
+Properties that hold at any size check the rest: the gradient sums of softmax attention
+(sum over keys of dV is the group's summed dO; sum over keys of dK is zero), per stream
+for intra layers.
 """
 import math
 
@@ -30,12 +35,33 @@ def _sample_rows(rng, B, H, N, count):
     return np.array(sorted(rows), dtype=np.int64)
 
 
-def _tail_key_rows(rng, B, Hkv, N, n, count):
-    rows = set()
-    last = range(max(0, N - 2 * n), N)  # keys of the last two tokens
-    while len(rows) < count:
-        rows.add((int(rng.integers(B)), int(rng.integers(Hkv)), int(rng.choice(list(last)))))
-    return np.array(sorted(rows), dtype=np.int64)
+def _key_rows(rng, s, mode, window):
+    """Sampled key rows (b, hk, j) of one key/value head, split into the keys that many
+    queries see (compared together) and the last keys (compared together)."""
+    b, hk = int(rng.integers(s.B)), int(rng.integers(s.Hkv))
+    G = s.Hq // s.Hkv
+    # oracle cost of a key near the start: every query row that sees it, each formed in
+    # full (about 3D flop per visible pair)
+    if mode == INTRA:
+        heavy_cost = 2 * G * s.L * s.L / 2 * 3 * s.D      # two streams' first keys
+    elif mode == LOCAL:
+        w = min(window, s.N)
+        heavy_cost = G * w * w * 3 * s.D
+    else:
+        heavy_cost = G * s.N * s.N / 2 * 3 * s.D
+    tail = {(b, hk, int(j)) for j in (s.N - 1, s.N - 2, s.N - s.n - 1)}
+    tail.add((b, hk, int(rng.integers(max(0, s.N - 2 * s.n), s.N))))
+    heavy = set()
+    if heavy_cost <= 6e10:
+        if mode == INTRA:  # stream 0 and stream n-1: first key, one of the first 128 tokens,
+            for st in {0, s.n - 1}:  # one of the middle block
+                heavy |= {(b, hk, st), (b, hk, int(rng.integers(1, 128)) * s.n + st),
+                          (b, hk, (s.L // 2 + int(rng.integers(128))) * s.n + st)}
+        else:
+            heavy |= {(b, hk, 0), (b, hk, 1), (b, hk, int(rng.integers(2, 128))),
+                      (b, hk, s.N // 2 + int(rng.integers(128)))}
+    return (np.array(sorted(heavy), dtype=np.int64).reshape(-1, 3),
+            np.array(sorted(tail), dtype=np.int64))
 
 
 @pytest.mark.parametrize("mode", [INTRA, MIX, LOCAL], ids=["intra", "mix", "local"])
@@ -61,13 +87,20 @@ def test_fullsize_sampled(wl, mode):
     G.assert_close_fwd(o[b, p, h], lse[b, h, p], ro, rl, "bf16", wl.name)
     G.assert_close_grad(dq[b, p, h], rdq, "bf16", "dq", wl.name)
 
-    krows = _tail_key_rows(rng, s.B, s.Hkv, s.N, s.n, 8)
-    rdk, rdv = oracle.sfa_bwd_dkdv_rows(ins["q"], ins["k"], ins["v"], ins["dout"], krows, **kw)
+    heavy, tail = _key_rows(rng, s, mode, window or 0)
     dk = G.to_host64(got["dk"])
     dv = G.to_host64(got["dv"])
-    b, h, j = krows.T
-    G.assert_close_grad(dk[b, j, h], rdk, "bf16", "dk", wl.name)
-    G.assert_close_grad(dv[b, j, h], rdv, "bf16", "dv", wl.name)
+    if wl is workloads.QWEN8B and mode != MIX:
+        assert len(heavy), "the Qwen3-8B-like intra and local layers check keys near the start"
+    for what, krows in (("heavy keys", heavy), ("last keys", tail)):
+        if not len(krows):
+            continue
+        print(f"  dK/dV of {what}: {krows.tolist()}", flush=True)
+        rdk, rdv = oracle.sfa_bwd_dkdv_rows(ins["q"], ins["k"], ins["v"], ins["dout"], krows,
+                                            **kw)
+        b, h, j = krows.T
+        G.assert_close_grad(dk[b, j, h], rdk, "bf16", "dk", f"{wl.name} {what}")
+        G.assert_close_grad(dv[b, j, h], rdv, "bf16", "dv", f"{wl.name} {what}")
 
     # gradient sums over all keys, per (b, kv-head) and per stream for intra
     dout = synth.bf16_bits_to_f32(ins["dout"]).astype(np.float64)

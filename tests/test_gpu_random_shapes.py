@@ -106,7 +106,7 @@ def test_random_decode_parity(case):
     v = to(synth.normal(seed + 2, (B, n * Lcap, Hkv, D), 2 ** -0.5))
     tctx = torch.from_numpy(np.asarray(ctx, dtype=np.int32)).to(G.dev())
     o, lse = hd.sfa_decode(G.to_dev(q), G.to_dev(k), G.to_dev(v), tctx, max_ctx=max(ctx),
-                           mode=mode, window=window)
+                           mode=mode, window=window, scale=D ** -0.5)
     torch.cuda.synchronize()
     ro, rl = oracle.sfa_decode(q, k, v, ctx, n=n, mode=mode, scale=D ** -0.5, window=window)
     G.assert_close_fwd(G.to_host64(o), G.to_host64(lse), ro, rl, "bf16", str(case))
