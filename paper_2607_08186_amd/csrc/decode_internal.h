@@ -15,6 +15,7 @@ struct DecGeom {
     int ngc;           // head chunks per key/value head, G / gchunk
     int nchunk;        // 256-row chunks of the cache per problem (for the longest context)
     int problems;      // B * Hkv * ngc (* n for intra-stream layers)
+    int nslot;         // query slots per problem: gchunk (intra-stream) or n * gchunk
 };
 
 DecGeom make_dec_geom(int B, int Lcap, int n, int Hq, int Hkv, int D, int mode, int window,
@@ -22,5 +23,6 @@ DecGeom make_dec_geom(int B, int Lcap, int n, int Hq, int Hkv, int D, int mode, 
 size_t decode_workspace_bytes(const DecGeom &g);
 hipError_t launch_decode_bf16(const void *q, const void *kc, const void *vc, const int32_t *ctx,
                               void *o, float *lse, const DecGeom &g, void *ws, hipStream_t s);
+
 
 }  // namespace hd

@@ -108,7 +108,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 2) void sfa_decode_partial_kernel(
     }
 
     // my query slot (column l32 of the MFMA results): its head and stream
-    const int nslot = g.mode == 0 ? g.gchunk : g.n * g.gchunk;
+    const int nslot = g.nslot;
     const int slot = l32;
     const int sl_s = g.mode == 0 ? pr.s : slot / g.gchunk;
     const int hq = pr.hk * g.G + pr.gc * g.gchunk + (g.mode == 0 ? slot : slot % g.gchunk);
@@ -198,7 +198,9 @@ __global__ __launch_bounds__(kDecWaves * 64, 2) void sfa_decode_partial_kernel(
         sl[wave * kSlots + slot] = lsum;
     }
     __syncthreads();
-    float *dst = part + ((size_t)blockIdx.y * g.nchunk + chunk) * kSlots * (D + 2);
+    // partials [problem][chunk][slot][D + 2]: O, then max and sum, for the problem's
+    // nslot slots only
+    float *dst = part + ((size_t)blockIdx.y * g.nchunk + chunk) * nslot * (D + 2);
     for (int e = tid; e < nslot * D; e += kDecWaves * 64) {  // the problem's slots only
         const int sl_i = e / D, d = e % D;
         float m = -INFINITY;
@@ -246,8 +248,8 @@ __global__ __launch_bounds__(D) void sfa_decode_combine_kernel(const float *__re
     const int klo = g.mode == 2 ? max(0, ctx * g.n - g.window + 1) : 0;
     const int nc = min(g.nchunk, (kvlen + kDecChunk - 1) / kDecChunk);
     const int cl = klo / kDecChunk;
-    const float *src = part + (size_t)prob * g.nchunk * kSlots * (D + 2) + slot * (D + 2);
-    const size_t cstep = (size_t)kSlots * (D + 2);
+    const float *src = part + (size_t)prob * g.nchunk * g.nslot * (D + 2) + slot * (D + 2);
+    const size_t cstep = (size_t)g.nslot * (D + 2);
     // one pass with a running maximum; every chunk in [cl, nc) has a visible row for
     // some query of the problem, but possibly none for this one (max -inf, sum 0)
     float m = -INFINITY, acc = 0.f, l = 0.f;
@@ -289,13 +291,15 @@ DecGeom make_dec_geom(int B, int Lcap, int n, int Hq, int Hkv, int D, int mode, 
     const int64_t rows = mode == 0 ? (int64_t)max_ctx + 1 : ((int64_t)max_ctx + 1) * n;
     g.nchunk = (int)((rows + kDecChunk - 1) / kDecChunk);
     g.problems = B * Hkv * g.ngc * (mode == 0 ? n : 1);
+    g.nslot = g.gchunk * per_head;
     return g;
 }
 
 size_t decode_workspace_bytes(const DecGeom &g)
 {
-    return (size_t)g.problems * g.nchunk * kSlots * (g.D + 2) * sizeof(float);
+    return (size_t)g.problems * g.nchunk * g.nslot * (g.D + 2) * sizeof(float);
 }
+
 
 hipError_t launch_decode_bf16(const void *q, const void *kc, const void *vc, const int32_t *ctx,
                               void *o, float *lse, const DecGeom &g, void *ws, hipStream_t s)

@@ -311,15 +311,16 @@ def test_decode_validation(lib, kw, code):
 
 
 def test_decode_workspace_size(lib):
-    """fp32 partials (max, sum and D sums for 32 query slots) per 256 cached rows of every
-    problem: (b, kv head, head chunk[, stream])."""
+    """fp32 partials (D sums, max and sum per query slot of the problem) per 256 cached
+    rows of every problem: (b, kv head, head chunk[, stream]); a problem's slots are its
+    heads (intra-stream) or its heads times the n streams, at most 32."""
     B, Lcap, n, Hq, Hkv, D = 2, 5000, 4, 32, 8, 128
-    per_chunk = 32 * (D + 2) * 4
     rows = 4096 * n  # max_ctx + 1 = 4096 tokens
     mix = lib.hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, 1, 0, 4095)
-    assert mix == B * Hkv * 1 * (rows // 256) * per_chunk  # G*n = 16 slots: one head chunk
+    # G*n = 16 slots: one head chunk
+    assert mix == B * Hkv * 1 * (rows // 256) * 16 * (D + 2) * 4
     intra = lib.hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, 0, 0, 4095)
-    assert intra == B * Hkv * n * (4096 // 256) * per_chunk
+    assert intra == B * Hkv * n * (4096 // 256) * 4 * (D + 2) * 4  # G = 4 slots per stream
     wide = lib.hd_sfa_decode_workspace_bytes(1, 100, 8, 64, 4, 64, 1, 0, 99)  # G*n = 128 slots
     assert wide == 1 * 4 * 4 * ((100 * 8 + 255) // 256) * 32 * 66 * 4
     assert lib.hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, 1, 0, Lcap) == 0
