@@ -10,8 +10,10 @@
  * Conventions shared by every entry point:
  *   - All tensor pointers are DEVICE pointers owned by the caller, 16-byte aligned,
  *     dense and row-major in the layouts stated per function.
- *   - The library never allocates, frees or synchronises device memory.  Work is
- *     enqueued on `stream` (0 = the null stream) and the call returns after enqueue.
+ *   - The library never allocates, frees or synchronises device memory (the one
+ *     device array it owns, the scratch of hd_sfa_decode_noalloc, is part of its code
+ *     object).  Work is enqueued on `stream` (0 = the null stream) and the call returns
+ *     after enqueue.
  *     Outputs are overwritten, never accumulated into (hd_embed_grad_scatter_add, whose
  *     purpose is to add into a dense gradient, is the one exception).
  *   - Arguments are validated on the host before anything is enqueued.  On a
@@ -314,6 +316,33 @@ hd_status_t hd_sfa_decode(const void *q, const void *k_cache, const void *v_cach
                           int B, int Lcap, int n, int Hq, int Hkv, int D, hd_sfa_mode_t mode,
                           int window, float scale, hd_dtype_t dtype, void *workspace,
                           size_t workspace_bytes, hd_stream_t stream);
+
+/*
+ * hd_sfa_decode_noalloc -- hd_sfa_decode for callers that cannot allocate device memory
+ * (code under HIP graph capture, serving loops that must not call the allocator): the
+ * same computation, arguments and results, with the fp32 partials kept in a scratch
+ * array that the library holds on each GPU it runs on, from the first such call on that
+ * GPU until the process ends.  The call allocates nothing.
+ *
+ * Limit: the partials of one call, hd_sfa_decode_workspace_bytes(...) for the same
+ * arguments, must fit the scratch, hd_sfa_decode_noalloc_max_bytes() = 128 MiB
+ * (for example 16 sequences of 4096 tokens at n=4, 32 query / 8 key-value heads of
+ * width 128, in any mode); larger requests return HD_ERR_INVALID_ARG with nothing
+ * enqueued.
+ * Every call on a GPU uses that GPU's one scratch array: calls that can run at the same
+ * time on one GPU (different streams, or different host threads without ordering)
+ * race and corrupt each other's results; calls on one stream are ordered.  The first
+ * call on a GPU looks the array's address up (hipGetSymbolAddress) and may therefore
+ * return HD_ERR_HIP if the runtime fails.
+ * Errors: as hd_sfa_decode (without the workspace ones), plus INVALID_ARG for sizes
+ * beyond the limit.
+ */
+hd_status_t hd_sfa_decode_noalloc(const void *q, const void *k_cache, const void *v_cache,
+                                  const int32_t *ctx_tokens, int max_ctx_tokens, void *o,
+                                  float *lse, int B, int Lcap, int n, int Hq, int Hkv, int D,
+                                  hd_sfa_mode_t mode, int window, float scale, hd_dtype_t dtype,
+                                  hd_stream_t stream);
+size_t hd_sfa_decode_noalloc_max_bytes(void);
 
 /* Static name of a status code ("HD_OK", ...). */
 const char *hd_status_str(hd_status_t s);

@@ -21,7 +21,8 @@ HD_DTYPE_BF16, HD_DTYPE_F32 = 0, 1
 EXPORTS = ("hd_expand_embed", "hd_expand_embed_bwd_workspace_bytes", "hd_expand_embed_bwd",
            "hd_embed_grad_scatter_add", "hd_cyclic_replicate", "hd_sfa_fwd_final",
            "hd_sfa_bwd_final_workspace_bytes", "hd_sfa_bwd_final", "hd_sfa_decode_workspace_bytes",
-           "hd_sfa_decode", "hd_final_stream_gather", "hd_final_stream_gather_bwd", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
+           "hd_sfa_decode", "hd_sfa_decode_noalloc", "hd_sfa_decode_noalloc_max_bytes",
+           "hd_final_stream_gather", "hd_final_stream_gather_bwd", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
            "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
            "hd_timing_enable", "hd_timing_filter", "hd_timing_collect")
 
@@ -71,6 +72,9 @@ def lib() -> ctypes.CDLL:
     L.hd_sfa_decode_workspace_bytes.argtypes = [i32] * 9
     L.hd_sfa_decode_workspace_bytes.restype = sz
     L.hd_sfa_decode.argtypes = [vp, vp, vp, vp, i32, vp, vp] + [i32] * 8 + [f32, i32, vp, sz, vp]
+    L.hd_sfa_decode_noalloc.argtypes = [vp, vp, vp, vp, i32, vp, vp] + [i32] * 8 + [f32, i32, vp]
+    L.hd_sfa_decode_noalloc_max_bytes.argtypes = []
+    L.hd_sfa_decode_noalloc_max_bytes.restype = sz
     L.hd_expand_embed_bwd_workspace_bytes.argtypes = [i32, i32]
     L.hd_expand_embed_bwd_workspace_bytes.restype = sz
     L.hd_expand_embed_bwd.argtypes = [vp, vp, i32, i32, i32, i64, i32, i32, vp, vp, vp, vp, sz, vp]
@@ -80,7 +84,7 @@ def lib() -> ctypes.CDLL:
     L.hd_final_stream_gather_bwd.argtypes = [vp, vp] + [i32] * 5 + [vp]
     for f in (L.hd_expand_embed, L.hd_expand_embed_bwd, L.hd_embed_grad_scatter_add,
               L.hd_cyclic_replicate, L.hd_final_stream_gather, L.hd_final_stream_gather_bwd,
-              L.hd_sfa_fwd_final, L.hd_sfa_bwd_final, L.hd_sfa_decode,
+              L.hd_sfa_fwd_final, L.hd_sfa_bwd_final, L.hd_sfa_decode, L.hd_sfa_decode_noalloc,
               L.hd_sfa_fwd,
               L.hd_sfa_fwd_local, L.hd_sfa_bwd,
               L.hd_sfa_bwd_local, L.hd_timing_enable, L.hd_timing_filter):
@@ -243,6 +247,18 @@ def hd_sfa_decode(q, k_cache, v_cache, ctx_tokens, max_ctx_tokens, o, lse, B, Lc
                                int(max_ctx_tokens), _ptr(o), _ptr(lse), B, Lcap, n, Hq, Hkv, D,
                                int(mode), int(window), float(scale), _dtype_code(q, dtype),
                                _ptr(workspace), workspace_bytes, _stream(stream)))
+
+
+def hd_sfa_decode_noalloc(q, k_cache, v_cache, ctx_tokens, max_ctx_tokens, o, lse, B, Lcap, n,
+                          Hq, Hkv, D, mode, window, scale, dtype=None, stream=None):
+    _check(lib().hd_sfa_decode_noalloc(_ptr(q), _ptr(k_cache), _ptr(v_cache), _ptr(ctx_tokens),
+                                       int(max_ctx_tokens), _ptr(o), _ptr(lse), B, Lcap, n, Hq,
+                                       Hkv, D, int(mode), int(window), float(scale),
+                                       _dtype_code(q, dtype), _stream(stream)))
+
+
+def hd_sfa_decode_noalloc_max_bytes() -> int:
+    return int(lib().hd_sfa_decode_noalloc_max_bytes())
 
 
 def hd_timing_enable(enable: bool):

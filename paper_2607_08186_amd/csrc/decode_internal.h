@@ -24,5 +24,11 @@ size_t decode_workspace_bytes(const DecGeom &g);
 hipError_t launch_decode_bf16(const void *q, const void *kc, const void *vc, const int32_t *ctx,
                               void *o, float *lse, const DecGeom &g, void *ws, hipStream_t s);
 
+// Library-owned scratch for the decode partials of callers that cannot allocate: a
+// device array of kDecodeScratchBytes per GPU, held until the process ends and shared
+// by every such call on that GPU.  decode_scratch returns its address on the current
+// device (looked up once per device).
+constexpr size_t kDecodeScratchBytes = (size_t)128 << 20;
+hipError_t decode_scratch(void **ptr);
 
 }  // namespace hd

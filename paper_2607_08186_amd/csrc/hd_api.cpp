@@ -548,6 +548,40 @@ hd_status_t hd_sfa_decode(const void *q, const void *k_cache, const void *v_cach
                       "hd_sfa_decode launch");
 }
 
+hd_status_t hd_sfa_decode_noalloc(const void *q, const void *k_cache, const void *v_cache,
+                                  const int32_t *ctx_tokens, int max_ctx_tokens, void *o,
+                                  float *lse, int B, int Lcap, int n, int Hq, int Hkv, int D,
+                                  hd_sfa_mode_t mode, int window, float scale, hd_dtype_t dtype,
+                                  hd_stream_t stream)
+{
+    g_err[0] = 0;
+    if (!q || !k_cache || !v_cache || !ctx_tokens || !o || !lse)
+        return fail(HD_ERR_INVALID_ARG, "null pointer");
+    hd_status_t st = check_decode(B, Lcap, n, Hq, Hkv, D, mode, window, max_ctx_tokens, dtype);
+    if (st != HD_OK) return st;
+    if (!std::isfinite(scale) || !(scale > 0.f))
+        return fail(HD_ERR_INVALID_ARG, "scale must be finite and > 0 (got %g)", (double)scale);
+    if (!aligned16(q) || !aligned16(k_cache) || !aligned16(v_cache) || !aligned16(o) ||
+        !aligned16(lse) || (reinterpret_cast<uintptr_t>(ctx_tokens) & 3))
+        return fail(HD_ERR_INVALID_ARG, "tensors must be 16-byte aligned, ctx_tokens 4-byte aligned");
+    const hd::DecGeom g = hd::make_dec_geom(B, Lcap, n, Hq, Hkv, D, mode, window, scale,
+                                            max_ctx_tokens);
+    const size_t need = hd::decode_workspace_bytes(g);
+    if (need > hd::kDecodeScratchBytes)
+        return fail(HD_ERR_INVALID_ARG,
+                    "these sizes need %zu bytes of decode scratch, more than the %zu bytes the "
+                    "library holds per GPU; call hd_sfa_decode with a workspace instead",
+                    need, hd::kDecodeScratchBytes);
+    void *scratch = nullptr;
+    hd_status_t sst = hip_status(hd::decode_scratch(&scratch), "hd_sfa_decode_noalloc scratch");
+    if (sst != HD_OK) return sst;
+    return hip_status(hd::launch_decode_bf16(q, k_cache, v_cache, ctx_tokens, o, lse, g, scratch,
+                                             (hipStream_t)stream),
+                      "hd_sfa_decode_noalloc launch");
+}
+
+size_t hd_sfa_decode_noalloc_max_bytes(void) { return hd::kDecodeScratchBytes; }
+
 hd_status_t hd_timing_enable(int enable)
 {
     std::lock_guard<std::mutex> lk(g_tmu);

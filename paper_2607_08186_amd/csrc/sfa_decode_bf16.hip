@@ -17,6 +17,8 @@
 //            the four waves merged through LDS into one (max, sum, unnormalised O) per
 //            query slot in the workspace;
 //   combine: per query row, the chunks' partials reduced to o and lse.
+#include <mutex>
+
 #include "decode_internal.h"
 #include "sfa_lds.h"
 
@@ -300,6 +302,31 @@ size_t decode_workspace_bytes(const DecGeom &g)
     return (size_t)g.problems * g.nchunk * g.nslot * (g.D + 2) * sizeof(float);
 }
 
+// The scratch array of the allocation-free decode entry point.  In host code its name
+// stands for a host-side shadow, not for device memory: kernels get the address that
+// hipGetSymbolAddress reports for the current device.
+static __device__ __align__(256) char scratch[kDecodeScratchBytes];
+
+hipError_t decode_scratch(void **ptr)
+{
+    constexpr int kMaxDevices = 64;
+    static std::mutex mu;
+    static void *addr[kMaxDevices] = {};
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(mu);
+    if (addr[dev] == nullptr) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (p == nullptr) return hipErrorInvalidSymbol;
+        addr[dev] = p;
+    }
+    *ptr = addr[dev];
+    return hipSuccess;
+}
 
 hipError_t launch_decode_bf16(const void *q, const void *kc, const void *vc, const int32_t *ctx,
                               void *o, float *lse, const DecGeom &g, void *ws, hipStream_t s)

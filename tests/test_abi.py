@@ -326,6 +326,41 @@ def test_decode_workspace_size(lib):
     assert lib.hd_sfa_decode_workspace_bytes(B, Lcap, n, Hq, Hkv, D, 1, 0, Lcap) == 0
 
 
+def _decode_noalloc(lib, **kw):
+    a = dict(q=FAKE, ctx=FAKE, o=FAKE, B=2, Lcap=16, n=4, Hq=8, Hkv=2, D=64, mode=1, window=0,
+             max_ctx=10, scale=0.125, dtype=0)
+    a.update(kw)
+    return lib.hd_sfa_decode_noalloc(a["q"], FAKE, FAKE, a["ctx"], a["max_ctx"], a["o"], FAKE,
+                                     a["B"], a["Lcap"], a["n"], a["Hq"], a["Hkv"], a["D"],
+                                     a["mode"], a["window"], a["scale"], a["dtype"], None)
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(q=None), INVALID), (dict(ctx=None), INVALID), (dict(B=0), INVALID),
+    (dict(Hkv=3), INVALID), (dict(mode=7), INVALID), (dict(mode=2, window=0), INVALID),
+    (dict(max_ctx=16), INVALID), (dict(scale=0.0), INVALID), (dict(dtype=1), UNSUPPORTED),
+    (dict(D=96), UNSUPPORTED), (dict(o=FAKE + 8), INVALID), (dict(ctx=FAKE + 2), INVALID),
+    # 32 sequences x 4096 tokens, n=4, 32/8 heads of width 128: 136 MB of partials
+    (dict(B=32, Lcap=4096, n=4, Hq=32, Hkv=8, D=128, max_ctx=4095), INVALID),
+])
+def test_decode_noalloc_validation(lib, kw, code):
+    """The allocation-free decode validates like hd_sfa_decode and rejects sizes whose
+    partials exceed its scratch, all before touching the GPU."""
+    assert _decode_noalloc(lib, **kw) == code
+    assert lib.hd_last_error().decode() != ""
+
+
+def test_decode_noalloc_limit(lib):
+    """128 MiB of scratch: the 16-sequence, 4096-token serving shape of every mode fits
+    (65 MiB of partials for a full cross-stream layer), twice that does not."""
+    limit = binding.hd_sfa_decode_noalloc_max_bytes()
+    assert limit == 128 << 20
+    for mode, window in ((0, 0), (1, 0), (2, 4096)):
+        need = lib.hd_sfa_decode_workspace_bytes(16, 4096, 4, 32, 8, 128, mode, window, 4095)
+        assert 0 < need <= limit
+    assert lib.hd_sfa_decode_workspace_bytes(32, 4096, 4, 32, 8, 128, 1, 0, 4095) > limit
+
+
 def test_missing_library_raises(monkeypatch, tmp_path):
     """No silent fallback: a missing libhd.so is an ImportError on first use."""
     monkeypatch.setattr(binding, "_lib", None)
