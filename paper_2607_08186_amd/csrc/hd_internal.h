@@ -109,13 +109,20 @@ hipError_t launch_bwd_preprocess_f32(const float *o, const float *dO, const floa
 // to bf16 (the precision its own dK MFMA uses), and the dQ pass reads it back, so dQ
 // costs one product instead of a recomputation of S and dP.  A tile covers 64 query
 // rows x 128 keys of one causal problem (query tile qt, key tile kt); its 16 KB are
-// laid out [query half (2)][key (128)][query (32)], i.e. for query row r (0..63) and
-// key c (0..127) of the tile the element sits at ((r >> 5) * 128 + c) * 32 + (r & 31).
+// laid out [query half (2)][key (128)][32 queries], i.e. for query row r (0..63) and
+// key c (0..127) of the tile the element sits at ((r >> 5) * 128 + c) * 32 +
+// ds_query_pos(r & 31).  Within a key's 32 queries the order is the one in which an
+// MFMA result holds them (lane half h, register r: query 8 (r / 4) + 4 h + r % 4), so
+// the dK/dV pass stores each lane's 16 values as they are.
 // Only tiles holding a visible pair are stored, per problem in query-tile order:
 //   causal (no window, or window >= len): query tile qt holds key tiles 0 .. qt/2,
 //     so its first tile is m(m+1) (qt = 2m) or (m+1)^2 (qt = 2m+1);
 //   local (window < len): key tiles kt_lo(qt) .. qt/2, at most `band` of them, each
 //     query tile owning `band` slots.
+// position of query q (0..31) inside a key's 32 dS values, and its inverse
+__host__ __device__ inline int ds_query_pos(int q) { return ((q >> 2) & 1) * 16 + (q >> 3) * 4 + (q & 3); }
+__host__ __device__ inline int ds_query_at(int pos) { return ((pos & 15) >> 2) * 8 + (pos >> 4) * 4 + (pos & 3); }
+
 constexpr int kDsRows = 64;                      // query rows per dS tile
 constexpr int kDsKeys = 128;                     // keys per dS tile
 constexpr int kDsTileBytes = kDsRows * kDsKeys * 2;

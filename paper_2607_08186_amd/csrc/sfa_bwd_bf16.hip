@@ -269,17 +269,10 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                 }
             }
             sched_pattern<8, 4 * DB, 1, 2, 0>();
-            // dw[2 rq .. 2 rq + 1]: queries 8 rq + 4 hi .. +3 of my key.  Swap the upper
-            // octets of half 0 with the lower octets of half 1, so that half 0 holds
-            // queries 0..15 and half 1 queries 16..31: 32 contiguous bytes per lane.
+            // dw[0..7] hold queries 8 rq + 4 hi .. +3 of my key (rq = 0..3) in the order of
+            // the tile layout: 32 contiguous bytes per lane
 #pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                const auto sw = __builtin_amdgcn_permlane32_swap(dw[i], dw[4 + i], false, false);
-                dw[i] = sw[0];
-                dw[4 + i] = sw[1];
-            }
-            dsw[0] = dw[0]; dsw[1] = dw[1]; dsw[2] = dw[4]; dsw[3] = dw[5];
-            dsw[4] = dw[2]; dsw[5] = dw[3]; dsw[6] = dw[6]; dsw[7] = dw[7];
+            for (int i = 0; i < 8; ++i) dsw[i] = dw[i];
         } else {
             // no visible pair in this block: its part of the tile is zero
 #pragma unroll
@@ -377,7 +370,8 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches
     const int l32 = lane & 31, hi = lane >> 5;
     const int q0 = tile * kRowsPerWg;
-    const int row = q0 + wave * 32 + l32;
+    // MFMA column l32 holds the query at position l32 of the dS tile layout
+    const int row = q0 + wave * 32 + ds_query_at(l32);
     const int wrow_min = q0 + wave * 32, wrow_max = wrow_min + 31;
     // my rows are half (wave & 1) of dS query tile qt
     const int qt = wrow_min / kDsRows;
