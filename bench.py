@@ -285,7 +285,7 @@ def main():
     if args.workload == "stack36":
         per_mode = time_layer_modes(hd, torch, layers, s, scale, dq, dk, dv, ws, ws_bytes,
                                     stream, W)
-        copy_ceiling = time_copy(torch, emb, stream)
+        copy_ceiling = time_expand_vs_copy(hd, torch, ids, tables, emb, s, W, stream)
 
     if final:
         flop_step = sum(14 * s.D * W.visible_pairs_final(s, window if m == W.LOCAL else 0)
@@ -334,8 +334,10 @@ def main():
             ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
             ent["bytes_per_launch"] = nbytes
             if copy_ceiling is not None:
+                ent["back_to_back_ms"] = copy_ceiling["expand_ms"]
+                ent["back_to_back_gbs"] = copy_ceiling["expand_gbs"]
                 ent["copy_gbs"] = copy_ceiling["gbs"]
-                ent["of_copy"] = round(ent["gbs"] / copy_ceiling["gbs"], 3)
+                ent["of_copy"] = round(copy_ceiling["expand_gbs"] / copy_ceiling["gbs"], 3)
         if fam in ("final_gather", "final_gather_bwd"):
             nbytes = W.final_gather_bytes(1, s.L, s.n, W.STACK_DMODEL, fam == "final_gather_bwd")
             ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
@@ -371,50 +373,76 @@ def main():
 def time_layer_modes(hd, torch, layers, s, scale, dq, dk, dv, ws, ws_bytes, stream, W, reps=10):
     """fwd+bwd of one intra-stream and one mixing layer of the step (its first layer of
     each kind, same inputs), each alone: `reps` back-to-back passes between two events
-    on the launch stream, after one untimed pass."""
+    on the launch stream, after one untimed pass.  Each layer is timed with the one-pass
+    backward (the workspace the step uses) and again with the backward in query bands
+    at the smallest workspace it accepts."""
     res = {}
     for mode in (W.INTRA, W.MIX):
         ly = next(x for x in layers if x["mode"] == mode)
 
-        def one():
+        def one(nbytes):
             hd.hd_sfa_fwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], s.B, s.L, s.n, s.Hq,
                           s.Hkv, s.D, mode, scale, stream=stream)
             hd.hd_sfa_bwd(ly["q"], ly["k"], ly["v"], ly["o"], ly["lse"], ly["do"], dq, dk, dv,
-                          s.B, s.L, s.n, s.Hq, s.Hkv, s.D, mode, scale, ws, ws_bytes,
+                          s.B, s.L, s.n, s.Hq, s.Hkv, s.D, mode, scale, ws, nbytes,
                           stream=stream)
 
-        one()
-        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        t0.record(stream)
-        for _ in range(reps):
-            one()
-        t1.record(stream)
-        torch.cuda.synchronize()
-        ms = t0.elapsed_time(t1) / reps
+        def timed(nbytes):
+            one(nbytes)
+            t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            for _ in range(reps):
+                one(nbytes)
+            t1.record(stream)
+            torch.cuda.synchronize()
+            return t0.elapsed_time(t1) / reps
+
+        ms = timed(ws_bytes)
         tf = W.useful_flop(s, mode) / (ms * 1e-3) / 1e12
-        res[W.MODE_NAMES[mode]] = {"ms": round(ms, 4), "tflops": round(tf, 2),
-                                   "frac_of_peak": round(tf / W.MI355X_BF16_PEAK_TFLOPS, 4),
-                                   "useful_tflop": round(W.useful_flop(s, mode) / 1e12, 4),
-                                   "reps": reps}
+        ent = {"ms": round(ms, 4), "tflops": round(tf, 2),
+               "frac_of_peak": round(tf / W.MI355X_BF16_PEAK_TFLOPS, 4),
+               "useful_tflop": round(W.useful_flop(s, mode) / 1e12, 4), "reps": reps}
+        low = hd.hd_sfa_bwd_min_workspace_bytes(s.B, s.L, s.n, s.Hq, s.Hkv, s.D, mode,
+                                                hd.HD_DTYPE_BF16)
+        ms_b = timed(low)
+        tf_b = W.useful_flop(s, mode) / (ms_b * 1e-3) / 1e12
+        ent["query_bands_min_workspace"] = {
+            "ms": round(ms_b, 4), "tflops": round(tf_b, 2), "workspace_bytes": low,
+            "one_pass_workspace_bytes": hd.hd_sfa_bwd_workspace_bytes(
+                s.B, s.L, s.n, s.Hq, s.Hkv, s.D, mode, hd.HD_DTYPE_BF16)}
+        res[W.MODE_NAMES[mode]] = ent
     return res
 
 
-def time_copy(torch, emb, stream, reps=20):
-    """A plain device-to-device copy of as many bytes as the expansion writes (read +
-    write counted), timed like the expansion: the HBM ceiling it is compared with."""
+def time_expand_vs_copy(hd, torch, ids, tables, emb, s, W, stream, reps=20):
+    """The expansion and a plain device-to-device copy of as many bytes as the expansion
+    moves (read + write counted), each launched `reps` times back to back between two
+    events on the launch stream: the same protocol for both, so that their ratio
+    compares the kernels (a single launch bracketed by events also carries the events'
+    own overhead, a few microseconds, which is large against a 40-microsecond kernel)."""
     src = emb.view(-1)
     dst = torch.empty_like(src)
-    dst.copy_(src)
-    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    t0.record(stream)
-    for _ in range(reps):
-        dst.copy_(src)
-    t1.record(stream)
-    torch.cuda.synchronize()
-    ms = t0.elapsed_time(t1) / reps
     nbytes = 2 * src.numel() * src.element_size()
-    return {"bytes": nbytes, "ms": round(ms, 5), "gbs": round(nbytes / (ms * 1e-3) / 1e9, 1),
-            "what": "torch copy_ of the expansion's output size (read + write bytes)"}
+
+    def b2b(fn):
+        fn()
+        torch.cuda.synchronize()
+        t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        t0.record(stream)
+        for _ in range(reps):
+            fn()
+        t1.record(stream)
+        torch.cuda.synchronize()
+        return t0.elapsed_time(t1) / reps
+
+    ms_copy = b2b(lambda: dst.copy_(src))
+    ms_exp = b2b(lambda: hd.hd_expand_embed(ids, tables, emb, 1, s.L, s.n, W.STACK_VOCAB,
+                                            W.STACK_DMODEL, stream=stream))
+    return {"bytes": nbytes, "ms": round(ms_copy, 5), "gbs": round(nbytes / (ms_copy * 1e-3) / 1e9, 1),
+            "expand_ms": round(ms_exp, 5), "expand_gbs": round(nbytes / (ms_exp * 1e-3) / 1e9, 1),
+            "reps": reps,
+            "what": "torch copy_ of the expansion's output size (read + write bytes) and the "
+                    "expansion itself, each timed back to back over the reps"}
 
 
 DECODE_BATCH = 16  # sequences decoded together

@@ -72,8 +72,9 @@ typedef enum { HD_DTYPE_BF16 = 0, HD_DTYPE_F32 = 1 } hd_dtype_t;
  * bad_id_count device int32 (nullable).  For each id outside [0, V) the n rows of that
  *              token are written as zeros and *bad_id_count is incremented once (so
  *              the caller zeroes it first to obtain a count).
- * Errors: INVALID_ARG for null ids/tables/out, B, L, n, Dm <= 0, V <= 0 or
- *         V > INT32_MAX, or unaligned pointers.
+ * Errors: INVALID_ARG for null ids/tables/out, B, L, n, Dm <= 0, V <= 0,
+ *         V > INT32_MAX, B*L >= 2^31, n*Dm*element size >= 2^31 bytes (one token's
+ *         expanded rows), or unaligned pointers.
  */
 hd_status_t hd_expand_embed(const int32_t *ids, const void *tables, void *out, int B, int L,
                             int n, int64_t V, int Dm, hd_dtype_t dtype,
@@ -211,12 +212,34 @@ size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
                                   hd_sfa_mode_t mode, hd_dtype_t dtype);
 
 /*
+ * hd_sfa_bwd_min_workspace_bytes -- the smallest workspace hd_sfa_bwd accepts for these
+ * sizes.  For bf16 a workspace below hd_sfa_bwd_workspace_bytes(...) runs the backward
+ * in query bands: the query rows are taken in bands of whole 256-row units, and each
+ * band's dK/dV pass stores only that band's dS tiles, which its dQ pass then reads; dK
+ * and dV are carried from band to band as fp32 partials.  The smallest workspace holds
+ * the two row statistics, those partials (2 * B*N*Hkv*D fp32) and the dS tiles of the
+ * largest 256-row unit (about 2*B*Hq*256*N bytes for HD_SFA_MIX), so it grows linearly
+ * in N.  Bands take whatever room the workspace leaves, so more workspace means fewer
+ * and larger bands; results agree with the one-pass run to fp32 summation order (the
+ * band partials are added in a fixed order, so every run is deterministic).  For fp32
+ * (no dS tiles) it equals hd_sfa_bwd_workspace_bytes.  For HD_SFA_LOCAL it returns the
+ * HD_SFA_MIX size.  Returns 0 for arguments hd_sfa_bwd would reject.
+ */
+size_t hd_sfa_bwd_min_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
+                                      hd_sfa_mode_t mode, hd_dtype_t dtype);
+
+/*
  * hd_sfa_bwd_local_workspace_bytes -- workspace hd_sfa_bwd_local needs for a local
  * cross-stream layer of the given window (for bf16 about 2*B*Hq*N*window bytes of dS
  * tiles when the window is well below N).  Returns 0 for arguments hd_sfa_bwd_local would reject.
  */
 size_t hd_sfa_bwd_local_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D, int window,
                                         hd_dtype_t dtype);
+/* hd_sfa_bwd_local_min_workspace_bytes -- the smallest workspace hd_sfa_bwd_local accepts
+ * for this window (query bands as for hd_sfa_bwd_min_workspace_bytes).  Returns 0 for
+ * arguments hd_sfa_bwd_local would reject. */
+size_t hd_sfa_bwd_local_min_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
+                                            int window, hd_dtype_t dtype);
 
 /*
  * hd_sfa_bwd -- gradients of the forward above, recomputing the attention
@@ -227,11 +250,15 @@ size_t hd_sfa_bwd_local_workspace_bytes(int B, int L, int n, int Hq, int Hkv, in
  *
  * q, o, dO, dq  device [B][N][Hq][D] of `dtype`;  k, v, dk, dv  device [B][N][Hkv][D].
  * lse           device float [B][Hq][N] exactly as written by hd_sfa_fwd.
- * workspace     device, 256-byte aligned, at least hd_sfa_bwd_workspace_bytes(...)
- *               bytes; contents on entry are ignored and on exit unspecified.  The
- *               bf16 path stores dS there in its dK/dV pass and its dQ pass reads it
- *               back, so dQ costs one product instead of a recomputation of S and dP.
- * Errors: as hd_sfa_fwd, plus INVALID_ARG for a missing or short workspace.
+ * workspace     device, 256-byte aligned, at least hd_sfa_bwd_min_workspace_bytes(...)
+ *               bytes (workspace_bytes gives its size); contents on entry are ignored
+ *               and on exit unspecified.  The bf16 path stores dS there in its dK/dV
+ *               pass and its dQ pass reads it back, so dQ costs one product instead of
+ *               a recomputation of S and dP.  With hd_sfa_bwd_workspace_bytes(...) or
+ *               more this is one pass over all query rows (the fastest); with less, a
+ *               sequence of query bands (see hd_sfa_bwd_min_workspace_bytes).
+ * Errors: as hd_sfa_fwd, plus INVALID_ARG for a missing workspace or one below
+ *         hd_sfa_bwd_min_workspace_bytes(...).
  */
 hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *o,
                        const float *lse, const void *dO, void *dq, void *dk, void *dv, int B,
@@ -242,7 +269,8 @@ hd_status_t hd_sfa_bwd(const void *q, const void *k, const void *v, const void *
 /*
  * hd_sfa_bwd_local -- hd_sfa_bwd for a local cross-stream layer (Fig. "masks" panel
  * (b)) of the given window; lse as written by hd_sfa_fwd_local with the same window,
- * workspace of at least hd_sfa_bwd_local_workspace_bytes(..., window, dtype) bytes.
+ * workspace of at least hd_sfa_bwd_local_min_workspace_bytes(..., window, dtype) bytes
+ * (one pass from hd_sfa_bwd_local_workspace_bytes(..., window, dtype) bytes up).
  * Arguments, layouts and errors as hd_sfa_bwd, plus INVALID_ARG for window < 1.
  */
 hd_status_t hd_sfa_bwd_local(const void *q, const void *k, const void *v, const void *o,
@@ -268,9 +296,11 @@ hd_status_t hd_sfa_bwd_local(const void *q, const void *k, const void *v, const 
  * hd_sfa_bwd_final
  *   dO, dq device [B][L][Hq][D];  dk, dv  device [B][n*L][Hkv][D] (summed over the query
  *   heads of each group; keys that no final-stream query sees get zero);
- *   workspace of at least hd_sfa_bwd_final_workspace_bytes(...) bytes (the two row
- *   statistics per query row and the bf16 dS tiles: 16 KB per 64 query rows x 128 keys
- *   of a key band, about 2*B*Hq*L*n*L bytes without a window).
+ *   workspace of at least hd_sfa_bwd_final_min_workspace_bytes(...) bytes;
+ *   hd_sfa_bwd_final_workspace_bytes(...) (the two row statistics per query row and the
+ *   bf16 dS tiles: 16 KB per 64 query rows x 128 keys of a key band, about
+ *   2*B*Hq*L*n*L bytes without a window) or more runs it in one pass, less in query
+ *   bands.
  * Other arguments, conventions and errors as hd_sfa_fwd / hd_sfa_bwd, plus INVALID_ARG
  * for window < 0 and UNSUPPORTED for dtype HD_DTYPE_F32 or n > 63.
  */
@@ -279,6 +309,9 @@ hd_status_t hd_sfa_fwd_final(const void *q, const void *k, const void *v, void *
                              float scale, hd_dtype_t dtype, hd_stream_t stream);
 size_t hd_sfa_bwd_final_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D, int window,
                                         hd_dtype_t dtype);
+/* the smallest workspace hd_sfa_bwd_final accepts (query bands as for hd_sfa_bwd) */
+size_t hd_sfa_bwd_final_min_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
+                                            int window, hd_dtype_t dtype);
 hd_status_t hd_sfa_bwd_final(const void *q, const void *k, const void *v, const void *o,
                              const float *lse, const void *dO, void *dq, void *dk, void *dv,
                              int B, int L, int n, int Hq, int Hkv, int D, int window,

@@ -23,7 +23,9 @@ EXPORTS = ("hd_expand_embed", "hd_expand_embed_bwd_workspace_bytes", "hd_expand_
            "hd_sfa_bwd_final_workspace_bytes", "hd_sfa_bwd_final", "hd_sfa_decode_workspace_bytes",
            "hd_sfa_decode", "hd_sfa_decode_noalloc", "hd_sfa_decode_noalloc_max_bytes",
            "hd_final_stream_gather", "hd_final_stream_gather_bwd", "hd_sfa_fwd", "hd_sfa_fwd_local", "hd_sfa_bwd_workspace_bytes",
-           "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
+           "hd_sfa_bwd_local_workspace_bytes", "hd_sfa_bwd_min_workspace_bytes",
+           "hd_sfa_bwd_local_min_workspace_bytes", "hd_sfa_bwd_final_min_workspace_bytes",
+           "hd_sfa_bwd", "hd_sfa_bwd_local", "hd_status_str", "hd_last_error",
            "hd_timing_enable", "hd_timing_filter", "hd_timing_collect")
 
 
@@ -61,6 +63,10 @@ def lib() -> ctypes.CDLL:
     L.hd_sfa_bwd_workspace_bytes.restype = sz
     L.hd_sfa_bwd_local_workspace_bytes.argtypes = [i32] * 8
     L.hd_sfa_bwd_local_workspace_bytes.restype = sz
+    for f in (L.hd_sfa_bwd_min_workspace_bytes, L.hd_sfa_bwd_local_min_workspace_bytes,
+              L.hd_sfa_bwd_final_min_workspace_bytes):
+        f.argtypes = [i32] * 8
+        f.restype = sz
     L.hd_sfa_bwd.argtypes = [vp] * 9 + [i32] * 7 + [f32, i32, vp, sz, vp]
     # the *_local variants take the window where the others take the mode
     L.hd_sfa_fwd_local.argtypes = L.hd_sfa_fwd.argtypes
@@ -196,6 +202,20 @@ def hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, dtype) -> int:
     return int(lib().hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, int(mode), int(dtype)))
 
 
+def hd_sfa_bwd_min_workspace_bytes(B, L, n, Hq, Hkv, D, mode, dtype) -> int:
+    return int(lib().hd_sfa_bwd_min_workspace_bytes(B, L, n, Hq, Hkv, D, int(mode), int(dtype)))
+
+
+def hd_sfa_bwd_local_min_workspace_bytes(B, L, n, Hq, Hkv, D, window, dtype) -> int:
+    return int(lib().hd_sfa_bwd_local_min_workspace_bytes(B, L, n, Hq, Hkv, D, int(window),
+                                                          int(dtype)))
+
+
+def hd_sfa_bwd_final_min_workspace_bytes(B, L, n, Hq, Hkv, D, window, dtype) -> int:
+    return int(lib().hd_sfa_bwd_final_min_workspace_bytes(B, L, n, Hq, Hkv, D, int(window),
+                                                          int(dtype)))
+
+
 def hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, window, dtype) -> int:
     return int(lib().hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, int(window),
                                                       int(dtype)))
@@ -317,8 +337,10 @@ def _local(mode, window):
 
 
 def sfa_backward(q, k, v, o, lse, dO, *, n, mode, scale, window=None, workspace=None,
-                 stream=None):
-    """-> (dq, dk, dv).  A workspace tensor (uint8, 256-byte aligned) may be passed in."""
+                 workspace_bytes=None, stream=None):
+    """-> (dq, dk, dv).  A workspace tensor (uint8, 256-byte aligned) may be passed in;
+    otherwise one of ``workspace_bytes`` bytes is allocated (default: the one-pass
+    size; anything down to the minimum size runs the backward in query bands)."""
     import torch
 
     B, L, Hq, Hkv, D = _shape(q, k, n)
@@ -328,7 +350,8 @@ def sfa_backward(q, k, v, o, lse, dO, *, n, mode, scale, window=None, workspace=
     else:
         need = hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, dtype)
     if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        workspace = torch.empty(need if workspace_bytes is None else int(workspace_bytes),
+                                dtype=torch.uint8, device=q.device)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     if _local(mode, window):
         hd_sfa_bwd_local(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, window, scale,
@@ -419,15 +442,16 @@ def sfa_final_forward(q, k, v, *, n, scale, window=0, stream=None):
 
 
 def sfa_final_backward(q, k, v, o, lse, dO, *, n, scale, window=0, workspace=None,
-                       stream=None):
-    """-> (dq [B][L][Hq][D], dk, dv [B][n*L][Hkv][D])."""
+                       workspace_bytes=None, stream=None):
+    """-> (dq [B][L][Hq][D], dk, dv [B][n*L][Hkv][D]).  Workspace as for sfa_backward."""
     import torch
 
     B, L, Hq, D = q.shape
     Hkv = k.shape[2]
     need = hd_sfa_bwd_final_workspace_bytes(B, L, n, Hq, Hkv, D, window, _dtype_code(q, None))
     if workspace is None:
-        workspace = torch.empty(need, dtype=torch.uint8, device=q.device)
+        workspace = torch.empty(need if workspace_bytes is None else int(workspace_bytes),
+                                dtype=torch.uint8, device=q.device)
     dq, dk, dv = torch.empty_like(q), torch.empty_like(k), torch.empty_like(v)
     hd_sfa_bwd_final(q, k, v, o, lse, dO, dq, dk, dv, B, L, n, Hq, Hkv, D, window, scale,
                      workspace, workspace.numel(), stream=stream)

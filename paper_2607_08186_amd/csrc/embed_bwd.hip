@@ -5,10 +5,13 @@
 // so its gradient is a scatter-add: table s at token id x receives the sum of the
 // upstream rows t*n + s of every token t with id x.  Done deterministically, without
 // atomics on the data:
-//   1. a stable LSD radix sort of the (id, token position) pairs by id, 8-bit digits
-//      (per-block digit histograms, one device-wide exclusive scan, then a scatter in
-//      which every block ranks its chunk stably with eight 1-bit splits in LDS); ids
-//      outside [0, V) get the key V and sort to the end;
+//   1. a stable sort of the (id, token position) pairs by id; ids outside [0, V) get
+//      the key V and sort to the end.  Up to kSmallSortMax tokens the sorted position
+//      of a token is counted directly (the number of tokens whose (key, position) is
+//      smaller, all keys held in LDS; one launch).  Larger batches take an LSD radix
+//      sort with 8-bit digits (per-block digit histograms, one device-wide exclusive
+//      scan, then a scatter in which every block ranks its chunk stably with eight
+//      1-bit splits in LDS);
 //   2. segment heads of the sorted ids give the distinct ids in ascending order and
 //      each id's run of token positions (ascending, as the sort is stable);
 //   3. one gather-reduce per (distinct id, stream): the upstream rows of the run are
@@ -33,10 +36,12 @@ constexpr int kItems = 8;
 constexpr int kChunk = kThreads * kItems;  // keys per block in the scan and sort kernels
 constexpr int kWaves = kThreads / 64;
 
-// Exclusive scan of one int per thread across the workgroup; *total gets the sum.
-// `sh` is LDS scratch of kWaves + 1 ints.
+// Exclusive scan of one int per thread across a workgroup of W waves; *total gets the
+// sum.  `sh` is LDS scratch of W + 1 ints.
+template <int W = kWaves>
 __device__ inline int block_exclusive_scan(int x, int *total, int *sh)
 {
+    constexpr int kWaves = W;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     int v = x;
 #pragma unroll
@@ -237,6 +242,80 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
     }
 }
 
+// ---------------------------------------------------------------- small batches
+
+constexpr int kRankWaves = 16;  // a workgroup ranks 64 tokens, each wave over 1/16 of the keys
+
+// Stable sort by counting: token i goes to position #{j : key_j < key_i, or key_j ==
+// key_i and j < i}, which is the position the stable radix sort gives it.  One lane
+// per token; the 16 waves of a workgroup count over disjoint sixteenths of the keys
+// (read from LDS, where every lane of a wave reads the same word) and add up in LDS.
+__global__ __launch_bounds__(kRankWaves * 64) void rank_sort_kernel(
+    const int32_t *__restrict__ ids, int M, int64_t V, uint32_t *__restrict__ keys_out,
+    int32_t *__restrict__ vals_out)
+{
+    __shared__ __attribute__((aligned(16))) uint32_t sk[kSmallSortMax];
+    __shared__ int cnt[kRankWaves][64];
+    for (int j = threadIdx.x; j < M; j += kRankWaves * 64) sk[j] = id_key(ids, j, V);
+    __syncthreads();
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int i = blockIdx.x * 64 + lane;
+    const uint32_t ki = i < M ? sk[i] : 0xffffffffu;
+    const int per = ((M + kRankWaves - 1) / kRankWaves + 3) & ~3;  // multiple of 4
+    const int j0 = wave * per, j1 = min(M, j0 + per);
+    int c = 0;
+    int j = j0;
+    for (; j + 4 <= j1; j += 4) {
+        const u32x4 kj = *reinterpret_cast<const u32x4 *>(&sk[j]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) c += (kj[e] < ki || (kj[e] == ki && j + e < i)) ? 1 : 0;
+    }
+    for (; j < j1; ++j) c += (sk[j] < ki || (sk[j] == ki && j < i)) ? 1 : 0;
+    cnt[wave][lane] = c;
+    __syncthreads();
+    if (wave == 0 && i < M) {
+        int r = 0;
+#pragma unroll
+        for (int w = 0; w < kRankWaves; ++w) r += cnt[w][lane];
+        keys_out[r] = ki;
+        vals_out[r] = i;
+    }
+}
+
+// Segments of a sorted key array of M <= kSmallSortMax entries in one workgroup: the
+// head of every run of equal keys gets its run's index (a block scan of the head
+// flags), its start and, for in-range keys, its id; the run of key V (if any) is the
+// last one and is not counted as a distinct id.
+__global__ __launch_bounds__(kRankWaves * 64) void small_segments_kernel(
+    const uint32_t *__restrict__ keys, int M, int64_t V, int *__restrict__ seg_start,
+    int32_t *__restrict__ uniq, int32_t *__restrict__ num_uniq)
+{
+    constexpr int kPer = kSmallSortMax / (kRankWaves * 64);
+    __shared__ int sh[kRankWaves + 1];
+    const int i0 = threadIdx.x * kPer;
+    int heads = 0;
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+        const int i = i0 + e;
+        if (i < M && (i == 0 || keys[i] != keys[i - 1])) ++heads;
+    }
+    int S;
+    int u = block_exclusive_scan<kRankWaves>(heads, &S, sh);
+#pragma unroll
+    for (int e = 0; e < kPer; ++e) {
+        const int i = i0 + e;
+        if (i < M && (i == 0 || keys[i] != keys[i - 1])) {
+            seg_start[u] = i;
+            if (keys[i] < (uint64_t)V) uniq[u] = (int32_t)keys[i];
+            ++u;
+        }
+    }
+    if (threadIdx.x == 0) {
+        seg_start[S] = M;
+        *num_uniq = S - (keys[M - 1] == (uint64_t)V ? 1 : 0);
+    }
+}
+
 // ---------------------------------------------------------------- segments
 
 __global__ __launch_bounds__(kThreads) void seg_flags_kernel(const uint32_t *__restrict__ keys,
@@ -288,50 +367,68 @@ __device__ inline float elem<float>(const float *p, int64_t i)
 
 // drows[s][u][:] = sum over the run of distinct id u of dout[pos*n + s][:] (fp32, in
 // ascending token order).  Work items (u, s) are strided over the grid; the item
-// count is read from the device.  VEC consecutive elements per thread.
+// count is read from the device.  VEC consecutive elements per thread and chunk, and
+// kReduceChunks chunks of a row per pass, whose loads are all issued before the adds.
+constexpr int kReduceChunks = 2;
+
+template <typename E, int VEC>
+__device__ inline void load_add(const E *src, float (&acc)[VEC])
+{
+    if constexpr (VEC == 8 && sizeof(E) == 2) {
+        const u32x4 w4 = *reinterpret_cast<const u32x4 *>(src);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            acc[2 * e] += bf16_lo(w4[e]);
+            acc[2 * e + 1] += bf16_hi(w4[e]);
+        }
+    } else if constexpr (VEC == 8) {
+        const f32x4 a = *reinterpret_cast<const f32x4 *>(src);
+        const f32x4 b = *reinterpret_cast<const f32x4 *>(src + 4);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            acc[e] += a[e];
+            acc[4 + e] += b[e];
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] += elem<E>(src, e);
+    }
+}
+
 template <typename E, int VEC>
 __global__ __launch_bounds__(kThreads) void embed_grad_reduce_kernel(
     const E *__restrict__ dout, const int32_t *__restrict__ pos, const int *__restrict__ seg_start,
     const int32_t *__restrict__ num_uniq, int n, int Dm, int rows_cap, float *__restrict__ drows)
 {
+    constexpr int kStride = kThreads * VEC;  // elements between a thread's chunks
     const int64_t items = (int64_t)*num_uniq * n;
     for (int64_t w = blockIdx.x; w < items; w += gridDim.x) {
         const int u = (int)(w / n), s = (int)(w % n);
         const int i0 = seg_start[u], i1 = seg_start[u + 1];
         float *dst = drows + ((int64_t)s * rows_cap + u) * Dm;
-        for (int d0 = threadIdx.x * VEC; d0 < Dm; d0 += kThreads * VEC) {
-            float acc[VEC];
+        for (int d0 = threadIdx.x * VEC; d0 < Dm; d0 += kStride * kReduceChunks) {
+            float acc[kReduceChunks][VEC];
 #pragma unroll
-            for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+            for (int c = 0; c < kReduceChunks; ++c)
+#pragma unroll
+                for (int e = 0; e < VEC; ++e) acc[c][e] = 0.f;
             for (int i = i0; i < i1; ++i) {
-                const int64_t row = (int64_t)pos[i] * n + s;
-                const E *src = dout + row * Dm + d0;
-                if constexpr (VEC == 8 && sizeof(E) == 2) {
-                    const u32x4 w4 = *reinterpret_cast<const u32x4 *>(src);
+                const E *src = dout + ((int64_t)pos[i] * n + s) * Dm + d0;
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        acc[2 * e] += bf16_lo(w4[e]);
-                        acc[2 * e + 1] += bf16_hi(w4[e]);
-                    }
-                } else if constexpr (VEC == 8) {
-                    const f32x4 a = *reinterpret_cast<const f32x4 *>(src);
-                    const f32x4 b = *reinterpret_cast<const f32x4 *>(src + 4);
+                for (int c = 0; c < kReduceChunks; ++c)
+                    if (d0 + c * kStride < Dm) load_add<E, VEC>(src + c * kStride, acc[c]);
+            }
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        acc[e] += a[e];
-                        acc[4 + e] += b[e];
-                    }
+            for (int c = 0; c < kReduceChunks; ++c) {
+                if (d0 + c * kStride >= Dm) continue;
+                float *o = dst + d0 + c * kStride;
+                if constexpr (VEC == 8) {
+                    *reinterpret_cast<f32x4 *>(o) = f32x4{acc[c][0], acc[c][1], acc[c][2], acc[c][3]};
+                    *reinterpret_cast<f32x4 *>(o + 4) = f32x4{acc[c][4], acc[c][5], acc[c][6], acc[c][7]};
                 } else {
 #pragma unroll
-                    for (int e = 0; e < VEC; ++e) acc[e] += elem<E>(src, e);
+                    for (int e = 0; e < VEC; ++e) o[e] = acc[c][e];
                 }
-            }
-            if constexpr (VEC == 8) {
-                *reinterpret_cast<f32x4 *>(dst + d0) = f32x4{acc[0], acc[1], acc[2], acc[3]};
-                *reinterpret_cast<f32x4 *>(dst + d0 + 4) = f32x4{acc[4], acc[5], acc[6], acc[7]};
-            } else {
-#pragma unroll
-                for (int e = 0; e < VEC; ++e) dst[d0 + e] = acc[e];
             }
         }
     }
@@ -417,7 +514,14 @@ hipError_t launch_embed_bwd(const int32_t *ids, const void *dout, int B, int L, 
     hipError_t e = hipSuccess;
     const uint32_t *kin = nullptr;
     const int32_t *vin = nullptr;
-    for (int p = 0; p < passes && e == hipSuccess; ++p) {
+    if (M <= kSmallSortMax) {
+        rank_sort_kernel<<<(M + 63) / 64, kRankWaves * 64, 0, s>>>(ids, M, V, ka, va);
+        small_segments_kernel<<<1, kRankWaves * 64, 0, s>>>(ka, M, V, seg_start, uniq, num_uniq);
+        kin = ka;
+        vin = va;
+        e = hipGetLastError();
+    }
+    for (int p = 0; M > kSmallSortMax && p < passes && e == hipSuccess; ++p) {
         uint32_t *kout = (p & 1) ? kb : ka;
         int32_t *vout = (p & 1) ? vb : va;
         const int32_t *from_ids = p == 0 ? ids : nullptr;
@@ -432,15 +536,17 @@ hipError_t launch_embed_bwd(const int32_t *ids, const void *dout, int B, int L, 
     timing_after(s);
     if (e != hipSuccess) return e;
 
-    timing_before("embed_bwd_segments", s);
-    const int nb1 = (M + kThreads - 1) / kThreads;
-    seg_flags_kernel<<<nb1, kThreads, 0, s>>>(kin, M, segidx);
-    e = scan_exclusive(segidx, M, sums, nseg, s);
-    seg_write_kernel<<<nb1, kThreads, 0, s>>>(kin, segidx, M, V, seg_start, uniq);
-    seg_finish_kernel<<<1, 1, 0, s>>>(kin, M, V, nseg, seg_start, num_uniq);
-    if (e == hipSuccess) e = hipGetLastError();
-    timing_after(s);
-    if (e != hipSuccess) return e;
+    if (M > kSmallSortMax) {
+        timing_before("embed_bwd_segments", s);
+        const int nb1 = (M + kThreads - 1) / kThreads;
+        seg_flags_kernel<<<nb1, kThreads, 0, s>>>(kin, M, segidx);
+        e = scan_exclusive(segidx, M, sums, nseg, s);
+        seg_write_kernel<<<nb1, kThreads, 0, s>>>(kin, segidx, M, V, seg_start, uniq);
+        seg_finish_kernel<<<1, 1, 0, s>>>(kin, M, V, nseg, seg_start, num_uniq);
+        if (e == hipSuccess) e = hipGetLastError();
+        timing_after(s);
+        if (e != hipSuccess) return e;
+    }
 
     // enough workgroups to keep every CU streaming; items beyond *num_uniq * n are
     // strided over them

@@ -14,6 +14,7 @@ struct EmbedBwdWorkspace {
     size_t keys_a, vals_a, keys_b, vals_b, hist, sums, scalars, segidx, seg_start, total;
 };
 constexpr int kEmbedBwdMaxTokens = 2048 * 2048;  // B*L limit of the single-level scans
+constexpr int kSmallSortMax = 16384;              // B*L up to which one counting pass sorts
 EmbedBwdWorkspace embed_bwd_workspace(int M);
 hipError_t launch_embed_bwd(const int32_t *ids, const void *dout, int B, int L, int n, int64_t V,
                             int Dm, int esize, int32_t *uniq, float *drows, int32_t *num_uniq,

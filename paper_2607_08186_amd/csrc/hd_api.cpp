@@ -159,6 +159,8 @@ hd_status_t hd_expand_embed(const int32_t *ids, const void *tables, void *out, i
     if ((int64_t)B * L >= ((int64_t)1 << 31))
         return fail(HD_ERR_INVALID_ARG, "B*L too large");
     const int esize = dtype == HD_DTYPE_BF16 ? 2 : 4;
+    if ((int64_t)n * Dm * esize >= ((int64_t)1 << 31))
+        return fail(HD_ERR_INVALID_ARG, "one token's n rows exceed 2^31-1 bytes (n=%d Dm=%d)", n, Dm);
     return hip_status(hd::launch_expand_embed(ids, tables, out, B, L, n, V, Dm, esize,
                                               bad_id_count, (hipStream_t)stream),
                       "hd_expand_embed launch");
@@ -348,31 +350,56 @@ hd_status_t hd_sfa_fwd_local(const void *q, const void *k, const void *v, void *
                    stream);
 }
 
-size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
-                                  hd_sfa_mode_t mode, hd_dtype_t dtype)
+}  // extern "C"
+
+namespace {
+
+// Workspace of a backward call: the one-pass size, or (smallest) the least it accepts;
+// 0 for arguments the call would reject.  The check leaves hd_last_error untouched.
+size_t bwd_ws_size(int B, int L, int n, int Hq, int Hkv, int D, int mode, int window,
+                   bool final_q, hd_dtype_t dtype, bool smallest)
 {
     char saved[sizeof g_err];
     memcpy(saved, g_err, sizeof g_err);
     hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, 1.0f, dtype);
+    if (st == HD_OK && final_q) st = check_final(n, dtype);
     memcpy(g_err, saved, sizeof g_err);
     if (st != HD_OK) return 0;
-    // without a window a local layer gets the size of the full causal layer, which
-    // bounds that of every window
-    return hd::bwd_workspace_bytes(hd::make_geom(B, L, n, Hq, Hkv, D, mode, 1.0f, hd::kNoWindow),
-                                   dtype == HD_DTYPE_BF16 ? 2 : 4);
+    const hd::SfaGeom g = geom(B, L, n, Hq, Hkv, D, mode, 1.0f, window, final_q);
+    const int esize = dtype == HD_DTYPE_BF16 ? 2 : 4;
+    return smallest ? hd::bwd_workspace_min_bytes(g, esize) : hd::bwd_workspace_bytes(g, esize);
+}
+
+}  // namespace
+
+extern "C" {
+
+// without a window a local layer gets the size of the full causal layer, which bounds
+// that of every window
+size_t hd_sfa_bwd_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
+                                  hd_sfa_mode_t mode, hd_dtype_t dtype)
+{
+    return bwd_ws_size(B, L, n, Hq, Hkv, D, mode, hd::kNoWindow, false, dtype, false);
+}
+
+size_t hd_sfa_bwd_min_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
+                                      hd_sfa_mode_t mode, hd_dtype_t dtype)
+{
+    return bwd_ws_size(B, L, n, Hq, Hkv, D, mode, hd::kNoWindow, false, dtype, true);
 }
 
 size_t hd_sfa_bwd_local_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D, int window,
                                         hd_dtype_t dtype)
 {
-    char saved[sizeof g_err];
-    memcpy(saved, g_err, sizeof g_err);
-    hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, HD_SFA_LOCAL, 1.0f, dtype);
-    memcpy(g_err, saved, sizeof g_err);
-    if (st != HD_OK || window < 1) return 0;
-    return hd::bwd_workspace_bytes(
-        hd::make_geom(B, L, n, Hq, Hkv, D, HD_SFA_LOCAL, 1.0f, window),
-        dtype == HD_DTYPE_BF16 ? 2 : 4);
+    if (window < 1) return 0;
+    return bwd_ws_size(B, L, n, Hq, Hkv, D, HD_SFA_LOCAL, window, false, dtype, false);
+}
+
+size_t hd_sfa_bwd_local_min_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
+                                            int window, hd_dtype_t dtype)
+{
+    if (window < 1) return 0;
+    return bwd_ws_size(B, L, n, Hq, Hkv, D, HD_SFA_LOCAL, window, false, dtype, true);
 }
 
 namespace {
@@ -392,7 +419,8 @@ hd_status_t sfa_bwd(const void *q, const void *k, const void *v, const void *o, 
         !aligned16(dO) || !aligned16(dq) || !aligned16(dk) || !aligned16(dv))
         return fail(HD_ERR_INVALID_ARG, "tensor pointers must be 16-byte aligned");
     const hd::SfaGeom g = geom(B, L, n, Hq, Hkv, D, mode, scale, window, final_q);
-    const size_t need = hd::bwd_workspace_bytes(g, dtype == HD_DTYPE_BF16 ? 2 : 4);
+    // the bf16 path runs in query bands when the workspace is below the one-pass size
+    const size_t need = hd::bwd_workspace_min_bytes(g, dtype == HD_DTYPE_BF16 ? 2 : 4);
     if (!workspace) return fail(HD_ERR_INVALID_ARG, "null workspace (%zu bytes needed)", need);
     if (reinterpret_cast<uintptr_t>(workspace) & 255)
         return fail(HD_ERR_INVALID_ARG, "workspace must be 256-byte aligned");
@@ -401,7 +429,7 @@ hd_status_t sfa_bwd(const void *q, const void *k, const void *v, const void *o, 
                     need);
     hipError_t e;
     if (dtype == HD_DTYPE_BF16)
-        e = hd::launch_bwd_bf16(q, k, v, o, lse, dO, dq, dk, dv, g, workspace,
+        e = hd::launch_bwd_bf16(q, k, v, o, lse, dO, dq, dk, dv, g, workspace, workspace_bytes,
                                 (hipStream_t)stream);
     else
         e = hd::launch_bwd_f32(static_cast<const float *>(q), static_cast<const float *>(k),
@@ -452,14 +480,17 @@ hd_status_t hd_sfa_fwd_final(const void *q, const void *k, const void *v, void *
 size_t hd_sfa_bwd_final_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D, int window,
                                         hd_dtype_t dtype)
 {
-    char saved[sizeof g_err];
-    memcpy(saved, g_err, sizeof g_err);
-    const int mode = window ? HD_SFA_LOCAL : HD_SFA_MIX;
-    hd_status_t st = check_sfa(B, L, n, Hq, Hkv, D, mode, 1.0f, dtype);
-    if (st == HD_OK) st = check_final(n, dtype);
-    memcpy(g_err, saved, sizeof g_err);
-    if (st != HD_OK || window < 0) return 0;
-    return hd::bwd_workspace_bytes(hd::make_geom_final(B, L, n, Hq, Hkv, D, mode, 1.0f, window), 2);
+    if (window < 0) return 0;
+    return bwd_ws_size(B, L, n, Hq, Hkv, D, window ? HD_SFA_LOCAL : HD_SFA_MIX, window, true,
+                       dtype, false);
+}
+
+size_t hd_sfa_bwd_final_min_workspace_bytes(int B, int L, int n, int Hq, int Hkv, int D,
+                                            int window, hd_dtype_t dtype)
+{
+    if (window < 0) return 0;
+    return bwd_ws_size(B, L, n, Hq, Hkv, D, window ? HD_SFA_LOCAL : HD_SFA_MIX, window, true,
+                       dtype, true);
 }
 
 hd_status_t hd_sfa_bwd_final(const void *q, const void *k, const void *v, const void *o,

@@ -90,9 +90,11 @@ hipError_t launch_final_gather(const void *h, void *out, int B, int L, int n, in
 
 hipError_t launch_fwd_bf16(const void *q, const void *k, const void *v, void *o, float *lse,
                            const SfaGeom &g, hipStream_t s);
+// ws_bytes >= bwd_workspace_min_bytes(g, 2); below bwd_workspace_bytes(g, 2) the
+// query rows are processed in bands (see QBand)
 hipError_t launch_bwd_bf16(const void *q, const void *k, const void *v, const void *o,
                            const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                           const SfaGeom &g, void *ws, hipStream_t s);
+                           const SfaGeom &g, void *ws, size_t ws_bytes, hipStream_t s);
 
 hipError_t launch_fwd_f32(const float *q, const float *k, const float *v, float *o, float *lse,
                           const SfaGeom &g, hipStream_t s);
@@ -165,21 +167,47 @@ __host__ __device__ inline int ds_kt_lo(const SfaGeom &g, int qt)
     return first > 0 ? first / kDsKeys : 0;
 }
 
+// index of the first dS tile of query tile qt inside its problem; qt = the query tile
+// count gives the problem's tile count
+__host__ __device__ inline int64_t ds_tile_base(int band, int qt)
+{
+    return band == 0 ? ds_tile_index(0, 0, qt, 0) : (int64_t)qt * band;
+}
+
 // dS tiles per causal problem
 inline int64_t ds_tiles_per_problem(const SfaGeom &g)
 {
-    const int nqt = (g.qlen + kDsRows - 1) / kDsRows;
-    const int band = ds_band(g);
-    return band == 0 ? ds_tile_index(0, 0, nqt, 0) : (int64_t)nqt * band;
+    return ds_tile_base(ds_band(g), (g.qlen + kDsRows - 1) / kDsRows);
 }
+
+// Query bands of the bf16 backward.  With a workspace that holds every dS tile the
+// backward runs in one pass.  With less, the query rows are processed in bands of
+// whole 256-row units (four dS query tiles, one dQ workgroup's rows), in ascending
+// order: the dK/dV pass of a band sweeps only the band's query tiles and stores their
+// dS tiles, the dQ pass of the band reads them back.  dK and dV of a key tile are
+// carried from band to band in fp32: the band holding the first query tile that sees
+// the key tile writes the partials, later ones add to them, and the band holding the
+// last such query tile writes the bf16 result.
+constexpr int kBandUnit = 4;  // 64-row query tiles per band unit
+
+struct QBand {
+    int qt_lo, qt_hi;         // 64-row query tiles [qt_lo, qt_hi) of this band
+    int64_t ds_base;          // index of the band's first dS tile in a problem's full numbering
+    float *part_k, *part_v;   // fp32 dK / dV partials [B][Hkv][streams][len][D]; null: one band
+};
 
 // Backward workspace, each part 256-byte aligned:
 //   per-row statistics, fp32 [B][Hq][qN] each: for fp32 those of
 //   launch_bwd_preprocess_f32, for bf16 -Delta and -lse/scale;
-//   bf16 path only: the dS tiles of every problem (b, hq[, s]), problem-major.
+//   bf16 path only, one pass: the dS tiles of every problem (b, hq[, s]),
+//     problem-major (ds, total);
+//   bf16 path only, in query bands: the fp32 dK and dV partials, then the dS tiles of
+//     one band (part_k, part_v, ds_banded); the smallest workspace holds the dS tiles of
+//     the largest band unit (min_total).
 struct BwdWorkspace {
     size_t delta, lse2, ds, total;
-    int64_t ds_tiles;  // dS tiles per problem
+    int64_t ds_tiles;  // dS tiles per problem (one pass)
+    size_t part_k, part_v, ds_banded, min_total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -193,13 +221,35 @@ inline BwdWorkspace bwd_workspace(const SfaGeom &g, int esize)
     w.ds = w.lse2 + align256(rows * 4);
     w.total = w.ds;
     w.ds_tiles = 0;
-    if (esize == 2) {
-        w.ds_tiles = ds_tiles_per_problem(g);
-        w.total += (size_t)g.B * g.Hq * g.streams * (size_t)w.ds_tiles * kDsTileBytes;
+    w.part_k = w.part_v = w.ds_banded = w.ds;
+    w.min_total = w.total;
+    if (esize != 2) return w;
+    const size_t probs = (size_t)g.B * g.Hq * g.streams;
+    w.ds_tiles = ds_tiles_per_problem(g);
+    w.total += probs * (size_t)w.ds_tiles * kDsTileBytes;
+    w.min_total = w.total;
+    // banded layout; it needs each problem's fp32 partials to stay below 2^31 bytes
+    const size_t part = (size_t)g.B * g.Hkv * g.streams * g.len * g.D * 4;
+    w.part_v = w.part_k + align256(part);
+    w.ds_banded = w.part_v + align256(part);
+    if ((int64_t)g.len * g.D * 4 >= ((int64_t)1 << 31)) return w;
+    const int band = ds_band(g);
+    const int nqt = (g.qlen + kDsRows - 1) / kDsRows;
+    int64_t unit = 0;  // dS tiles per problem of the largest band unit
+    for (int qa = 0; qa < nqt; qa += kBandUnit) {
+        const int qb = qa + kBandUnit < nqt ? qa + kBandUnit : nqt;
+        const int64_t t = ds_tile_base(band, qb) - ds_tile_base(band, qa);
+        unit = t > unit ? t : unit;
     }
+    const size_t banded_min = w.ds_banded + probs * (size_t)unit * kDsTileBytes;
+    if (banded_min < w.total) w.min_total = banded_min;
     return w;
 }
 
 inline size_t bwd_workspace_bytes(const SfaGeom &g, int esize) { return bwd_workspace(g, esize).total; }
+inline size_t bwd_workspace_min_bytes(const SfaGeom &g, int esize)
+{
+    return bwd_workspace(g, esize).min_total;
+}
 
 }  // namespace hd

@@ -37,6 +37,7 @@ constexpr int kKeysPerWg = 128;  // dK/dV: 4 key groups of 32, each shared by 2 
 constexpr int kDkdvWaves = 8;
 constexpr int kDqWaves = 8;
 constexpr int kRowsPerWg = kDqWaves * 32;  // dQ: 8 waves (two per SIMD) x 32 rows
+static_assert(kRowsPerWg == kBandUnit * kDsRows, "a query band unit is one dQ workgroup's rows");
 
 // Row statistics for the dK/dV pass: -Delta = -rowsum(dO * O) (fp32 sum of the bf16
 // products) and -lse/scale, both fp32 [B][Hq][N].  D/8 lanes per query row, 16 bytes
@@ -79,7 +80,8 @@ template <int D>
 __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
     const bf16 *__restrict__ dO, const float *__restrict__ delta, const float *__restrict__ lse2,
-    bf16 *__restrict__ dk, bf16 *__restrict__ dv, bf16 *__restrict__ ds, int64_t ds_tiles, SfaGeom g)
+    bf16 *__restrict__ dk, bf16 *__restrict__ dv, bf16 *__restrict__ ds, int64_t ds_tiles, SfaGeom g,
+    QBand bd)
 {
     constexpr int DB = D / 32, KS = D / 16;
     using T = Tile<D>;
@@ -128,13 +130,22 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     // XCD) then read the same Q/dO tiles at about the same time, and the group's heads
     // follow each other, so most of those reads hit in L2.
     // first query tile with a row that sees the first key (P(i) >= k0)
-    const int qt_first = max(0, (k0 - g.qpoff + g.qpmul - 1) / g.qpmul) / kRows;
+    const int qt_first_all = max(0, (k0 - g.qpoff + g.qpmul - 1) / g.qpmul) / kRows;
     const int band = ds_band(g);
     // last query tile that sees a key of this workgroup: the end of the sequence, or for
     // local layers the window's end past the last key (P(i) <= k0 + 126 + window)
-    const int qt_end = (int)min((int64_t)(g.qlen + kRows - 1) / kRows,
-                                ((int64_t)k0 + kKeysPerWg - 2 + g.window - g.qpoff) / g.qpmul / kRows + 1);
-    const int nqt = qt_end - qt_first;
+    const int qt_end_all = (int)min((int64_t)(g.qlen + kRows - 1) / kRows,
+                                    ((int64_t)k0 + kKeysPerWg - 2 + g.window - g.qpoff) / g.qpmul / kRows + 1);
+    // this query band's part of the sweep; dK/dV go out as bf16 from the band holding
+    // the last query tile of the sweep and as fp32 partials from earlier bands, and a
+    // band after the one holding the first query tile adds to the partials.  Keys that
+    // no query sees are written (as zeros) by the first band.
+    const int qt_first = max(qt_first_all, bd.qt_lo), qt_end = min(qt_end_all, bd.qt_hi);
+    const bool unseen = qt_first_all >= qt_end_all;
+    if (unseen ? bd.qt_lo != 0 : qt_first >= qt_end) return;  // uniform: nothing to do here
+    const bool first_band = unseen || qt_first_all >= bd.qt_lo;
+    const bool last_band = unseen || qt_end_all <= bd.qt_hi;
+    const int nqt = max(0, qt_end - qt_first);
     const int iters = g.G * nqt;
 
     // this workgroup's 128 keys and values, resident in LDS for the whole sweep
@@ -218,7 +229,8 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
         if (it + 1 < iters) issue(nxt_gi, nxt_qt, st ^ 1);
         const int qlo = cur_qt * kRows + qb * 32;
         const rsrc_t rds = make_rsrc(
-            ds_head + ds_tile_index(band, ds_kt_lo(g, cur_qt), cur_qt, ktile) * (kDsTileBytes / 2),
+            ds_head + (ds_tile_index(band, ds_kt_lo(g, cur_qt), cur_qt, ktile) - bd.ds_base) *
+                          (kDsTileBytes / 2),
             kDsTileBytes);
         uint32_t dsw[8];
         // wave-uniform: some of my 32 queries see some of my keys
@@ -313,6 +325,11 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     __syncthreads();
     if (qb == 0 && key < g.len) {
         const uint32_t off = kbase + (uint32_t)key * kstride;
+        // fp32 partials of this problem's keys (query bands only): [key][D]
+        const size_t pslice = (size_t)g.len * D;
+        const rsrc_t rpk = make_rsrc(bd.part_k + prob * pslice, (uint32_t)(pslice * 4));
+        const rsrc_t rpv = make_rsrc(bd.part_v + prob * pslice, (uint32_t)(pslice * 4));
+        const uint32_t poff = (uint32_t)key * D * 4;
 #pragma unroll
         for (int db = 0; db < DB; ++db)
 #pragma unroll
@@ -320,13 +337,22 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                 const f32x4 pk = park[((0 * DB + db) * 4 + rq) * 64 + lane];
                 const f32x4 pv = park[((1 * DB + db) * 4 + rq) * 64 + lane];
                 const int d0 = db * 32 + 8 * rq + 4 * hi;
-                const float sc = g.scale;
-                const u32x2 wk = {pack_bf16((adk[db][4 * rq] + pk[0]) * sc, (adk[db][4 * rq + 1] + pk[1]) * sc),
-                                  pack_bf16((adk[db][4 * rq + 2] + pk[2]) * sc, (adk[db][4 * rq + 3] + pk[3]) * sc)};
-                const u32x2 wv = {pack_bf16(adv[db][4 * rq] + pv[0], adv[db][4 * rq + 1] + pv[1]),
-                                  pack_bf16(adv[db][4 * rq + 2] + pv[2], adv[db][4 * rq + 3] + pv[3])};
-                st8(rdk, off + d0 * 2, wk);
-                st8(rdv, off + d0 * 2, wv);
+                f32x4 sk = {adk[db][4 * rq] + pk[0], adk[db][4 * rq + 1] + pk[1],
+                            adk[db][4 * rq + 2] + pk[2], adk[db][4 * rq + 3] + pk[3]};
+                f32x4 sv = {adv[db][4 * rq] + pv[0], adv[db][4 * rq + 1] + pv[1],
+                            adv[db][4 * rq + 2] + pv[2], adv[db][4 * rq + 3] + pv[3]};
+                if (!first_band) {
+                    sk += __builtin_bit_cast(f32x4, ld16(rpk, poff + d0 * 4));
+                    sv += __builtin_bit_cast(f32x4, ld16(rpv, poff + d0 * 4));
+                }
+                if (last_band) {
+                    const float sc = g.scale;
+                    st8(rdk, off + d0 * 2, u32x2{pack_bf16(sk[0] * sc, sk[1] * sc), pack_bf16(sk[2] * sc, sk[3] * sc)});
+                    st8(rdv, off + d0 * 2, u32x2{pack_bf16(sv[0], sv[1]), pack_bf16(sv[2], sv[3])});
+                } else {
+                    st16(rpk, poff + d0 * 4, __builtin_bit_cast(u32x4, sk));
+                    st16(rpv, poff + d0 * 4, __builtin_bit_cast(u32x4, sv));
+                }
             }
     }
 }
@@ -338,7 +364,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
 template <int D, int KK, int S>
 __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     const bf16 *__restrict__ k, const bf16 *__restrict__ ds, bf16 *__restrict__ dq, SfaGeom g,
-    int64_t ds_tiles)
+    int64_t ds_tiles, QBand bd)
 {
     constexpr int DB = D / 32;
     static_assert(kDsKeys % KK == 0 && KK % 16 == 0 && S >= 2, "ring shape");
@@ -349,10 +375,13 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     static_assert(S * kStage <= 160 * 1024, "the ring must fit in LDS");
     __shared__ __attribute__((aligned(1024))) char smem[S][kStage];
 
-    const int ntiles = (g.qlen + kRowsPerWg - 1) / kRowsPerWg;
+    // the 256-row blocks of this query band (its first tile is a multiple of four)
+    const int rb_lo = bd.qt_lo / kBandUnit;
+    const int ntiles = (min(bd.qt_hi * kDsRows, g.qlen) + kRowsPerWg - 1) / kRowsPerWg - rb_lo;
     const int nprob = g.B * g.Hq * g.streams;
     int prob, tile;
     decode_tile(blockIdx.x, nprob, ntiles, prob, tile);
+    tile += rb_lo;
     const int s = prob % g.streams;
     const int hq = (prob / g.streams) % g.Hq;
     const int b = prob / (g.streams * g.Hq);
@@ -404,7 +433,7 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
         char *st = smem[(j - jf) % S];
         T::load(st, rk, kbase, kstride, j * KK, g.len, wave, kDqWaves, lane);
         if (active(j)) {
-            const int64_t t = ds_tile_index(band, kt_lo, qt, j / kSteps);
+            const int64_t t = ds_tile_index(band, kt_lo, qt, j / kSteps) - bd.ds_base;
             const rsrc_t rt = make_rsrc(ds_prob + t * (kDsTileBytes / 2), kDsTileBytes);
             char *slab = st + T::BYTES + wave * kSlab;
             const uint32_t off =
@@ -484,9 +513,9 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
 
 template <int D>
 hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o,
-                      const float *lse, const bf16 *dO, float *delta, float *lse2, bf16 *ds,
-                      int64_t ds_tiles, bf16 *dq, bf16 *dk, bf16 *dv, const SfaGeom &g,
-                      hipStream_t s, const char *st_name, const char *dq_name,
+                      const float *lse, const bf16 *dO, float *delta, float *lse2, char *wsb,
+                      const BwdWorkspace &w, size_t ws_bytes, bf16 *dq, bf16 *dk, bf16 *dv,
+                      const SfaGeom &g, hipStream_t s, const char *st_name, const char *dq_name,
                       const char *dkdv_name)
 {
     const int64_t rows = (int64_t)g.B * g.qN * g.Hq;
@@ -496,16 +525,8 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o
     hipError_t e = hipGetLastError();
     timing_after(s);
     if (e != hipSuccess) return e;
-    const int nkt = (g.len + kKeysPerWg - 1) / kKeysPerWg;
-    timing_before(dkdv_name, s);
-    sfa_dkdv_bf16_kernel<D><<<nkt * g.B * g.Hkv * g.streams, kDkdvWaves * 64, 0, s>>>(
-        q, k, v, dO, delta, lse2, dk, dv, ds, ds_tiles, g);
-    e = hipGetLastError();
-    timing_after(s);
-    if (e != hipSuccess) return e;
-    const int nqt = (g.qlen + kRowsPerWg - 1) / kRowsPerWg;
-    const int wgs = nqt * g.B * g.Hq * g.streams;
-    // the co-resident ring, unless the whole grid would then be resident at once
+
+    // the co-resident dQ ring, unless the whole grid would then be resident at once
     static std::atomic<int> co_resident{0};  // its workgroups per CU (a property of the code)
     int dev = 0, cus = 0, per_cu = co_resident.load(std::memory_order_relaxed);
     if (per_cu == 0) {
@@ -518,43 +539,74 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o
     if ((e = hipGetDevice(&dev)) != hipSuccess ||
         (e = hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev)) != hipSuccess)
         return e;
-    timing_before(dq_name, s);
-    if ((int64_t)wgs > (int64_t)per_cu * cus)
-        sfa_dq_bf16_kernel<D, 32, 2><<<wgs, kDqWaves * 64, 0, s>>>(k, ds, dq, g, ds_tiles);
-    else
-        sfa_dq_bf16_kernel<D, 64, 3><<<wgs, kDqWaves * 64, 0, s>>>(k, ds, dq, g, ds_tiles);
-    e = hipGetLastError();
-    timing_after(s);
-    return e;
+
+    const int nkt = (g.len + kKeysPerWg - 1) / kKeysPerWg;
+    const int nqt = (g.qlen + kDsRows - 1) / kDsRows;
+    const int band = ds_band(g);
+    const int64_t nprob_q = (int64_t)g.B * g.Hq * g.streams;
+    // one pass when every dS tile fits, else query bands as large as the workspace allows
+    const bool one_pass = ws_bytes >= w.total;
+    if (!one_pass && ws_bytes < w.min_total) return hipErrorInvalidValue;  // checked by the caller
+    bf16 *ds = reinterpret_cast<bf16 *>(wsb + (one_pass ? w.ds : w.ds_banded));
+    const int64_t ds_room = one_pass ? w.ds_tiles : (int64_t)((ws_bytes - w.ds_banded) / kDsTileBytes / nprob_q);
+    auto tiles = [&](int qa, int qb) { return ds_tile_base(band, qb) - ds_tile_base(band, qa); };
+    for (int qa = 0; qa < nqt;) {
+        int qb = one_pass ? nqt : min(nqt, qa + kBandUnit);
+        while (qb < nqt && tiles(qa, min(nqt, qb + kBandUnit)) <= ds_room) qb = min(nqt, qb + kBandUnit);
+        QBand bd;
+        bd.qt_lo = qa;
+        bd.qt_hi = qb;
+        bd.ds_base = ds_tile_base(band, qa);
+        bd.part_k = one_pass ? nullptr : reinterpret_cast<float *>(wsb + w.part_k);
+        bd.part_v = one_pass ? nullptr : reinterpret_cast<float *>(wsb + w.part_v);
+        const int64_t band_tiles = tiles(qa, qb);
+        timing_before(dkdv_name, s);
+        sfa_dkdv_bf16_kernel<D><<<nkt * g.B * g.Hkv * g.streams, kDkdvWaves * 64, 0, s>>>(
+            q, k, v, dO, delta, lse2, dk, dv, ds, band_tiles, g, bd);
+        e = hipGetLastError();
+        timing_after(s);
+        if (e != hipSuccess) return e;
+        const int nrb = (min(qb * kDsRows, g.qlen) + kRowsPerWg - 1) / kRowsPerWg - qa / kBandUnit;
+        const int64_t wgs = nrb * nprob_q;
+        timing_before(dq_name, s);
+        if (wgs > (int64_t)per_cu * cus)
+            sfa_dq_bf16_kernel<D, 32, 2><<<(unsigned)wgs, kDqWaves * 64, 0, s>>>(k, ds, dq, g, band_tiles, bd);
+        else
+            sfa_dq_bf16_kernel<D, 64, 3><<<(unsigned)wgs, kDqWaves * 64, 0, s>>>(k, ds, dq, g, band_tiles, bd);
+        e = hipGetLastError();
+        timing_after(s);
+        if (e != hipSuccess) return e;
+        qa = qb;
+    }
+    return hipSuccess;
 }
 
 }  // namespace
 
 hipError_t launch_bwd_bf16(const void *q, const void *k, const void *v, const void *o,
                            const float *lse, const void *dO, void *dq, void *dk, void *dv,
-                           const SfaGeom &g, void *ws, hipStream_t s)
+                           const SfaGeom &g, void *ws, size_t ws_bytes, hipStream_t s)
 {
     const BwdWorkspace w = bwd_workspace(g, 2);
     char *wsb = static_cast<char *>(ws);
     float *delta = reinterpret_cast<float *>(wsb + w.delta);
     float *lse2 = reinterpret_cast<float *>(wsb + w.lse2);
-    bf16 *ds = reinterpret_cast<bf16 *>(wsb + w.ds);
     const bf16 *qq = static_cast<const bf16 *>(q), *kk = static_cast<const bf16 *>(k),
                *vv = static_cast<const bf16 *>(v), *dd = static_cast<const bf16 *>(dO),
                *oo = static_cast<const bf16 *>(o);
     bf16 *gq = static_cast<bf16 *>(dq), *gk = static_cast<bf16 *>(dk), *gv = static_cast<bf16 *>(dv);
     const bool f = g.qpmul != 1;  // final-stream layer: tagged in the timing names
     if (g.D == 32)
-        return bwd_bf16_d<32>(qq, kk, vv, oo, lse, dd, delta, lse2, ds, w.ds_tiles, gq, gk, gv, g,
+        return bwd_bf16_d<32>(qq, kk, vv, oo, lse, dd, delta, lse2, wsb, w, ws_bytes, gq, gk, gv, g,
                               s, f ? "sfa_bwd_final_stats_d32" : "sfa_bwd_stats_d32",
                               f ? "sfa_dq_final_bf16_d32" : "sfa_dq_bf16_d32",
                               f ? "sfa_dkdv_final_bf16_d32" : "sfa_dkdv_bf16_d32");
     if (g.D == 64)
-        return bwd_bf16_d<64>(qq, kk, vv, oo, lse, dd, delta, lse2, ds, w.ds_tiles, gq, gk, gv, g,
+        return bwd_bf16_d<64>(qq, kk, vv, oo, lse, dd, delta, lse2, wsb, w, ws_bytes, gq, gk, gv, g,
                               s, f ? "sfa_bwd_final_stats_d64" : "sfa_bwd_stats_d64",
                               f ? "sfa_dq_final_bf16_d64" : "sfa_dq_bf16_d64",
                               f ? "sfa_dkdv_final_bf16_d64" : "sfa_dkdv_bf16_d64");
-    return bwd_bf16_d<128>(qq, kk, vv, oo, lse, dd, delta, lse2, ds, w.ds_tiles, gq, gk, gv, g, s,
+    return bwd_bf16_d<128>(qq, kk, vv, oo, lse, dd, delta, lse2, wsb, w, ws_bytes, gq, gk, gv, g, s,
                            f ? "sfa_bwd_final_stats_d128" : "sfa_bwd_stats_d128",
                            f ? "sfa_dq_final_bf16_d128" : "sfa_dq_bf16_d128",
                            f ? "sfa_dkdv_final_bf16_d128" : "sfa_dkdv_bf16_d128");

@@ -141,6 +141,67 @@ def test_workspace_size_formula(lib):
     assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 2, 48, 0, 0) == 0  # D
 
 
+def _ds_tiles_of_query_tiles(len_, qts):
+    """dS tiles holding a visible pair of a causal problem (no window), for the listed
+    64-row query tiles, by brute force over the tiles' pairs."""
+    nkt = -(-len_ // 128)
+    count = 0
+    for qt in qts:
+        rows = range(qt * 64, min(len_, qt * 64 + 64))
+        count += sum(1 for kt in range(nkt) if any(kt * 128 <= r for r in rows))
+    return count
+
+
+@pytest.mark.parametrize("B,L,n,Hq,Hkv,D", [(2, 100, 3, 4, 2, 64), (1, 4096, 4, 32, 8, 128),
+                                            (1, 700, 1, 2, 1, 32)])
+def test_min_workspace_size_formula(lib, B, L, n, Hq, Hkv, D):
+    """The smallest bf16 workspace: the row statistics, fp32 dK/dV partials and the dS
+    tiles of the largest 256-row band unit (four 64-row query tiles)."""
+    a256 = lambda x: math.ceil(x / 256) * 256
+    N = n * L
+    stats = 2 * a256(B * Hq * N * 4)
+    parts = 2 * a256(B * N * Hkv * D * 4)
+    for mode, len_, streams in ((0, L, n), (1, N, 1)):
+        nqt = -(-len_ // 64)
+        unit = max(_ds_tiles_of_query_tiles(len_, range(qa, min(nqt, qa + 4)))
+                   for qa in range(0, nqt, 4))
+        full = lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 0)
+        want = min(full, stats + parts + B * Hq * streams * unit * 16384)
+        assert lib.hd_sfa_bwd_min_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 0) == want
+        # fp32 keeps no dS tiles: one size
+        assert (lib.hd_sfa_bwd_min_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 1)
+                == lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 1))
+    # local layers: never above the one-pass size; at least statistics and partials
+    for w in (1, 300, 10 ** 6):
+        full = lib.hd_sfa_bwd_local_workspace_bytes(B, L, n, Hq, Hkv, D, w, 0)
+        got = lib.hd_sfa_bwd_local_min_workspace_bytes(B, L, n, Hq, Hkv, D, w, 0)
+        assert got <= full and (got == full or got > stats + parts)
+    assert lib.hd_sfa_bwd_min_workspace_bytes(1, 8, 2, 4, 3, 64, 0, 0) == 0  # Hq % Hkv
+    assert lib.hd_sfa_bwd_local_min_workspace_bytes(B, L, n, Hq, Hkv, D, 0, 0) == 0
+    assert lib.hd_sfa_bwd_final_min_workspace_bytes(B, L, n, Hq, Hkv, D, -1, 0) == 0
+
+
+def test_min_workspace_at_the_long_forward_limit(lib):
+    """At B=1, N=131008, Hq=64, Hkv=8, D=128 the one-pass dS tiles take about a
+    terabyte; the banded backward runs from a few gigabytes up."""
+    for mode, (L, n) in ((0, (32752, 4)), (1, (32752, 4))):
+        full = lib.hd_sfa_bwd_workspace_bytes(1, L, n, 64, 8, 128, mode, 0)
+        low = lib.hd_sfa_bwd_min_workspace_bytes(1, L, n, 64, 8, 128, mode, 0)
+        assert full > 2 * 10 ** 11 and 0 < low < 8 * 2 ** 30, (mode, full, low)
+
+
+def test_short_workspace_is_rejected_below_the_minimum(lib):
+    a = dict(B=1, L=300, n=4, Hq=4, Hkv=2, D=64, mode=1, dtype=0)
+    low = lib.hd_sfa_bwd_min_workspace_bytes(a["B"], a["L"], a["n"], a["Hq"], a["Hkv"], a["D"],
+                                             a["mode"], a["dtype"])
+    full = lib.hd_sfa_bwd_workspace_bytes(a["B"], a["L"], a["n"], a["Hq"], a["Hkv"], a["D"],
+                                          a["mode"], a["dtype"])
+    assert 0 < low < full
+    st, _ = bwd(lib, ws_bytes=low - 1, **a)
+    assert st == INVALID
+    assert "short" in lib.hd_last_error().decode()
+
+
 @pytest.mark.parametrize("L,n,window", [(100, 3, 1), (100, 3, 64), (100, 3, 129), (100, 3, 299),
                                         (100, 3, 300), (100, 3, 10 ** 6), (700, 4, 200),
                                         (700, 4, 1000), (2048, 2, 4096)])
@@ -190,6 +251,7 @@ def test_bwd_local_validation(lib, kw, code):
     (dict(ids=None), INVALID), (dict(B=0), INVALID), (dict(V=0), INVALID),
     (dict(V=1 << 40), INVALID), (dict(Dm=0), INVALID), (dict(dtype=5), INVALID),
     (dict(out=FAKE + 8), INVALID), (dict(bad=FAKE + 2), INVALID),
+    (dict(n=1 << 16, Dm=1 << 15), INVALID),  # a token's rows would exceed 2^31 bytes
 ])
 def test_expand_validation(lib, args, code):
     a = dict(ids=FAKE, tables=FAKE, out=FAKE, B=1, L=4, n=2, V=10, Dm=8, dtype=0, bad=None)

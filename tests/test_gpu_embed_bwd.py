@@ -71,6 +71,9 @@ CASES = [
     (1, 5000, 2, 1 << 20, 8, "bf16"),
     (1, 300, 2, 2 ** 31 - 1, 8, "bf16"),  # ids over the whole int32 range: four passes
     (1, 1, 3, 10, 32, "bf16"),           # a single token
+    (1, 16384, 2, 151936, 16, "bf16"),   # the largest batch of the one-pass counting sort
+    (1, 16385, 2, 151936, 16, "bf16"),   # the smallest one of the radix sort
+    (2, 8500, 1, 1000, 2056, "f32"),     # radix sort with heavy repeats; rows of 1+ chunks
 ]
 
 

@@ -121,15 +121,17 @@ _SLICE_LIMIT = {}
 
 
 def _slice_limit_inputs(N, Hq, Hkv, D):
-    """Seeded inputs of the slice-limit shape, drawn once for both modes: N(0, 1/2) from
-    torch's seeded device generator (a host draw of 10^9 normals takes minutes), rounded
-    to bf16; the oracle reads host copies of the same tensors."""
+    """Seeded inputs of the slice-limit shape, drawn once for all tests here: q, k, v
+    ~ N(0, 1/2) and dO ~ N(0, 1) from torch's seeded device generator (a host draw of
+    10^9 normals takes minutes), rounded to bf16; the oracle reads host copies of the
+    same tensors."""
     if not _SLICE_LIMIT:
         import torch
 
         seed = synth.seed_for("slice_limit")
-        t = {name: synth.device_normal((1, N, h, D), 2 ** -0.5, seed + i, G.dev(), torch.bfloat16)
-             for i, (name, h) in enumerate((("q", Hq), ("k", Hkv), ("v", Hkv)))}
+        t = {name: synth.device_normal((1, N, h, D), std, seed + i, G.dev(), torch.bfloat16)
+             for i, (name, h, std) in enumerate((("q", Hq, 2 ** -0.5), ("k", Hkv, 2 ** -0.5),
+                                                 ("v", Hkv, 2 ** -0.5), ("dout", Hq, 1.0)))}
         _SLICE_LIMIT.update(seed=seed, dev=t, **{name: G.bits(x) for name, x in t.items()})
     return _SLICE_LIMIT
 
@@ -139,8 +141,7 @@ def test_forward_at_the_slice_limit(mode):
     """q and o as large as the boundary accepts: B=1, L=32752, n=4 (N=131008), Hq=64,
     Hkv=8, D=128 puts 2146435072 bytes of q in the batch slice, just under the 2^31 bytes
     that the kernels' 32-bit buffer offsets address.  Sampled rows, among them the last
-    rows of the sequence in the last head, against the oracle.  (The backward's dS
-    workspace grows as N^2 and does not fit at this length.)"""
+    rows of the sequence in the last head, against the oracle."""
     B, L, n, Hq, Hkv, D = 1, 32752, 4, 64, 8, 128
     N = n * L
     assert N * Hq * D * 2 < 2 ** 31 <= (N + 64) * Hq * D * 2
@@ -165,3 +166,64 @@ def test_forward_at_the_slice_limit(mode):
     oh = G.to_host64(o[b, p, h])
     lh = G.to_host64(lse[b, h, p])
     G.assert_close_fwd(oh, lh, ro, rl, "bf16", "slice limit")
+
+
+@pytest.mark.parametrize("mode", [INTRA, MIX], ids=["intra", "mix"])
+def test_backward_at_the_slice_limit(mode):
+    """The backward at the same length.  Its one-pass dS workspace would be about 0.27 TB
+    (intra-stream) or 1.1 TB (mixing), so it runs in query bands with a 24 GiB
+    workspace.  Sampled dQ rows and dK/dV of the last keys (which only the last rows
+    see, so the oracle can form them) against the oracle; the gradient sums over all
+    keys (sum of dV = the group's summed dO, sum of dK = 0, per stream for intra)."""
+    import paper_2607_08186_amd as hd
+    import torch
+
+    B, L, n, Hq, Hkv, D = 1, 32752, 4, 64, 8, 128
+    N = n * L
+    scale = D ** -0.5
+    ws_bytes = 24 << 30
+    low = hd.hd_sfa_bwd_min_workspace_bytes(B, L, n, Hq, Hkv, D, mode, hd.HD_DTYPE_BF16)
+    full = hd.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, hd.HD_DTYPE_BF16)
+    assert low <= ws_bytes < full
+    print(f"slice limit backward mode={mode}: drawing inputs", flush=True)
+    ins = _slice_limit_inputs(N, Hq, Hkv, D)
+    seed = ins["seed"]
+    q, k, v, do = (ins["dev"][x] for x in ("q", "k", "v", "dout"))
+    print(f"slice limit backward mode={mode} seed={seed}: forward + backward in bands",
+          flush=True)
+    o, lse = hd.sfa_forward(q, k, v, n=n, mode=mode, scale=scale)
+    dq, dk, dv = hd.sfa_backward(q, k, v, o, lse, do, n=n, mode=mode, scale=scale,
+                                 workspace_bytes=ws_bytes)
+    torch.cuda.synchronize()
+    del o, lse
+    rng = np.random.default_rng((seed + 7 * mode) & 0xFFFFFFFF)
+    rows = {(0, Hq - 1, N - 1), (0, 0, N - 1), (0, 17, N - 3), (0, 0, 0), (0, 40, 1)}
+    while len(rows) < 16:
+        rows.add((0, int(rng.integers(Hq)), int(rng.integers(N - 1024, N))))
+    while len(rows) < 24:
+        rows.add((0, int(rng.integers(Hq)), int(rng.integers(N))))
+    rows = np.array(sorted(rows), dtype=np.int64)
+    kw = dict(L=L, n=n, mode=mode, scale=scale)
+    print(f"  oracle dQ rows: {len(rows)}", flush=True)
+    rdq = oracle.sfa_bwd_dq_rows(ins["q"], ins["k"], ins["v"], ins["dout"], rows, **kw)
+    b, h, p = (torch.as_tensor(x, device=dq.device) for x in rows.T)
+    G.assert_close_grad(G.to_host64(dq[b, p, h]), rdq, "bf16", "dq", "slice limit backward")
+    hk = int(rng.integers(Hkv))
+    keys = np.array(sorted({(0, hk, N - 1), (0, hk, N - 2), (0, hk, N - n - 1),
+                            (0, Hkv - 1 - hk, N - 3)}), dtype=np.int64)
+    print(f"  oracle dK/dV keys: {keys.tolist()}", flush=True)
+    rdk, rdv = oracle.sfa_bwd_dkdv_rows(ins["q"], ins["k"], ins["v"], ins["dout"], keys, **kw)
+    b, h, j = (torch.as_tensor(x, device=dk.device) for x in keys.T)
+    G.assert_close_grad(G.to_host64(dk[b, j, h]), rdk, "bf16", "dk", "slice limit backward")
+    G.assert_close_grad(G.to_host64(dv[b, j, h]), rdv, "bf16", "dv", "slice limit backward")
+    # gradient sums, in fp64 on the device
+    Gq = Hq // Hkv
+    dof = do.double()
+    groups = [slice(None)] if mode != INTRA else [slice(st, None, n) for st in range(n)]
+    for sl in groups:
+        want = dof[:, sl].reshape(B, -1, Hkv, Gq, D).sum(dim=(1, 3))
+        dvs, dks = dv[:, sl].double(), dk[:, sl].double()
+        assert torch.all((dvs.sum(dim=1) - want).abs() <= 1e-2 * dvs.abs().sum(dim=1) + 1e-3), \
+            "sum_j dV_j != sum dO"
+        assert torch.all(dks.sum(dim=1).abs() <= 1e-2 * dks.abs().sum(dim=1) + 1e-3), "sum_j dK_j != 0"
+    assert bool(torch.isfinite(dq).all()) and bool(torch.isfinite(dk).all())
