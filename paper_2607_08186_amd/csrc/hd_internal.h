@@ -174,6 +174,90 @@ __host__ __device__ inline int64_t ds_tile_base(int band, int qt)
     return band == 0 ? ds_tile_index(0, 0, qt, 0) : (int64_t)qt * band;
 }
 
+// Query tiles [first, end) of 64 rows with a row that sees some key of the 128-key
+// tile kt (the sweep of the dK/dV workgroup that owns those keys).
+__host__ __device__ inline void dkdv_sweep(const SfaGeom &g, int kt, int &first, int &end)
+{
+    const int k0 = kt * kDsKeys;
+    const int f = (k0 - g.qpoff + g.qpmul - 1) / g.qpmul;
+    first = (f > 0 ? f : 0) / kDsRows;
+    const int64_t e = ((int64_t)k0 + kDsKeys - 2 + g.window - g.qpoff) / g.qpmul / kDsRows + 1;
+    const int64_t nqt = (g.qlen + kDsRows - 1) / kDsRows;
+    end = (int)(e < nqt ? e : nqt);
+}
+
+// Small dK/dV grids (fewer than kSplitGrid workgroups, i.e. under two per CU on
+// MI355X) split the longest key-tile sweeps over two workgroups each, which run at the
+// same time and leave fp32 partials for a combine pass; without it the step lasts as
+// long as the sweep of the first key tile, which sees every query.  Returns the number
+// of leading key tiles split this way: those whose sweep is longer than half the
+// longest one (0 when the grid is large or has fewer than four key tiles).
+constexpr int kSplitGrid = 512;
+
+// Work items of a dK/dV launch with split sweeps, longest first (a key problem's items
+// are dispatched in this order, so that the workgroups that finish early take the
+// shorter items).  Item i is key tile item[i] >> 2 with code item[i] & 3: 0 the whole
+// sweep, 1 its later half, 2 its earlier half.  A launch has at most kSplitGrid key
+// tiles, so 2 * kSplitGrid items.
+struct SplitOrder {
+    uint16_t item[2 * kSplitGrid];
+};
+
+inline int dkdv_splits(const SfaGeom &g)
+{
+    const int nkt = (g.len + kDsKeys - 1) / kDsKeys;
+    if (nkt < 4 || (int64_t)nkt * g.B * g.Hkv * g.streams >= kSplitGrid) return 0;
+    int maxlen = 0;
+    for (int kt = 0; kt < nkt; ++kt) {
+        int f, e;
+        dkdv_sweep(g, kt, f, e);
+        maxlen = e - f > maxlen ? e - f : maxlen;
+    }
+    int ns = 0;
+    for (; ns < nkt; ++ns) {
+        int f, e;
+        dkdv_sweep(g, ns, f, e);
+        if (2 * (e - f) <= maxlen || e - f < 2) break;
+    }
+    return ns;
+}
+
+// The items of a launch with nsplit split key tiles, longest first (ties: lower key
+// tile, later half first).
+inline SplitOrder dkdv_split_order(const SfaGeom &g, int nsplit)
+{
+    const int nkt = (g.len + kDsKeys - 1) / kDsKeys;
+    struct It {
+        int len, code;
+    };
+    It its[2 * kSplitGrid];
+    int n = 0;
+    for (int kt = 0; kt < nkt; ++kt) {
+        int f, e;
+        dkdv_sweep(g, kt, f, e);
+        const int len = e > f ? e - f : 0;
+        if (kt < nsplit) {
+            its[n++] = {len - len / 2, kt << 2 | 1};  // later half: [f + len/2, e)
+            its[n++] = {len / 2, kt << 2 | 2};        // earlier half
+        } else {
+            its[n++] = {len, kt << 2};
+        }
+    }
+    // insertion sort (at most 2 * kSplitGrid items, once per launch)
+    for (int i = 1; i < n; ++i) {
+        const It x = its[i];
+        int j = i - 1;
+        while (j >= 0 && (its[j].len < x.len || (its[j].len == x.len && its[j].code > x.code))) {
+            its[j + 1] = its[j];
+            --j;
+        }
+        its[j + 1] = x;
+    }
+    SplitOrder o;
+    for (int i = 0; i < n; ++i) o.item[i] = (uint16_t)its[i].code;
+    return o;
+}
+
 // dS tiles per causal problem
 inline int64_t ds_tiles_per_problem(const SfaGeom &g)
 {
@@ -201,13 +285,18 @@ struct QBand {
 //   launch_bwd_preprocess_f32, for bf16 -Delta and -lse/scale;
 //   bf16 path only, one pass: the dS tiles of every problem (b, hq[, s]),
 //     problem-major (ds, total);
+//   bf16 path only, one pass with split sweeps (dkdv_splits > 0): after the dS tiles,
+//     the fp32 partials of the two halves of every split sweep (split), laid out
+//     [half][dK, dV][key problem][split keys][D];
 //   bf16 path only, in query bands: the fp32 dK and dV partials, then the dS tiles of
 //     one band (part_k, part_v, ds_banded); the smallest workspace holds the dS tiles of
-//     the largest band unit (min_total).
+//     the largest band unit (min_total).  Bands do not split sweeps.
 struct BwdWorkspace {
     size_t delta, lse2, ds, total;
     int64_t ds_tiles;  // dS tiles per problem (one pass)
     size_t part_k, part_v, ds_banded, min_total;
+    size_t split;      // offset of the split-sweep partials (one pass)
+    int nsplit;        // key tiles with a split sweep (one pass)
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -223,10 +312,15 @@ inline BwdWorkspace bwd_workspace(const SfaGeom &g, int esize)
     w.ds_tiles = 0;
     w.part_k = w.part_v = w.ds_banded = w.ds;
     w.min_total = w.total;
+    w.split = w.total;
+    w.nsplit = 0;
     if (esize != 2) return w;
     const size_t probs = (size_t)g.B * g.Hq * g.streams;
     w.ds_tiles = ds_tiles_per_problem(g);
     w.total += probs * (size_t)w.ds_tiles * kDsTileBytes;
+    w.split = align256(w.total);
+    w.nsplit = dkdv_splits(g);
+    w.total = w.split + (size_t)4 * g.B * g.Hkv * g.streams * w.nsplit * kDsKeys * g.D * 4;
     w.min_total = w.total;
     // banded layout; it needs each problem's fp32 partials to stay below 2^31 bytes
     const size_t part = (size_t)g.B * g.Hkv * g.streams * g.len * g.D * 4;

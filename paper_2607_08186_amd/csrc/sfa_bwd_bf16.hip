@@ -40,8 +40,12 @@ constexpr int kRowsPerWg = kDqWaves * 32;  // dQ: 8 waves (two per SIMD) x 32 ro
 static_assert(kRowsPerWg == kBandUnit * kDsRows, "a query band unit is one dQ workgroup's rows");
 
 // Row statistics for the dK/dV pass: -Delta = -rowsum(dO * O) (fp32 sum of the bf16
-// products) and -lse/scale, both fp32 [B][Hq][N].  D/8 lanes per query row, 16 bytes
-// each; rows are taken in [b][p][hq] order so the O and dO reads are contiguous.
+// products) and -lse/scale, both fp32 [B][Hq][N].  A workgroup takes 64 consecutive
+// rows p of one (b, hq): D/8 lanes per row read 16 bytes each of O and dO (every
+// thread issues all of its loads first), and the 64 results go out through LDS as
+// two contiguous 256-byte runs.
+constexpr int kStatRows = 64;
+
 template <int D>
 __global__ __launch_bounds__(256) void bwd_stats_bf16_kernel(const bf16 *__restrict__ o,
                                                              const bf16 *__restrict__ dO,
@@ -49,29 +53,43 @@ __global__ __launch_bounds__(256) void bwd_stats_bf16_kernel(const bf16 *__restr
                                                              float *__restrict__ nstat_d,
                                                              float *__restrict__ nstat_l, SfaGeom g)
 {
-    constexpr int LPR = D / 8;
-    const int64_t rows = (int64_t)g.B * g.qN * g.Hq;
-    const int64_t r = ((int64_t)blockIdx.x * 256 + threadIdx.x) / LPR;
-    const int part = threadIdx.x % LPR;
-    float acc = 0.f;
-    if (r < rows) {
-        const u32x4 ow = *reinterpret_cast<const u32x4 *>(o + r * D + part * 8);
-        const u32x4 dw = *reinterpret_cast<const u32x4 *>(dO + r * D + part * 8);
+    constexpr int LPR = D / 8;             // lanes per row
+    constexpr int RPP = 256 / LPR;         // rows per pass
+    constexpr int PASSES = kStatRows / RPP;
+    __shared__ float sh[kStatRows];
+    const int nblk = (g.qN + kStatRows - 1) / kStatRows;
+    const int bh = blockIdx.x / nblk;  // b * Hq + hq
+    const int b = bh / g.Hq, hq = bh % g.Hq;
+    const int p0 = (blockIdx.x % nblk) * kStatRows;
+    const int part = threadIdx.x % LPR, r = threadIdx.x / LPR;
+    u32x4 ow[PASSES], dw[PASSES];
 #pragma unroll
-        for (int w = 0; w < 4; ++w) {
-            acc = __builtin_fmaf(bf16_lo(dw[w]), bf16_lo(ow[w]), acc);
-            acc = __builtin_fmaf(bf16_hi(dw[w]), bf16_hi(ow[w]), acc);
+    for (int i = 0; i < PASSES; ++i) {
+        const int p = p0 + i * RPP + r;
+        ow[i] = dw[i] = u32x4{0u, 0u, 0u, 0u};
+        if (p < g.qN) {
+            const int64_t off = (((int64_t)b * g.qN + p) * g.Hq + hq) * D + part * 8;
+            ow[i] = *reinterpret_cast<const u32x4 *>(o + off);
+            dw[i] = *reinterpret_cast<const u32x4 *>(dO + off);
         }
     }
 #pragma unroll
-    for (int m = LPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
-    if (r < rows && part == 0) {
-        const int hq = (int)(r % g.Hq);
-        const int64_t bp = r / g.Hq;
-        const int p = (int)(bp % g.qN);
-        const int b = (int)(bp / g.qN);
-        const size_t li = ((size_t)b * g.Hq + hq) * g.qN + p;
-        nstat_d[li] = -acc;
+    for (int i = 0; i < PASSES; ++i) {
+        float acc = 0.f;
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            acc = __builtin_fmaf(bf16_lo(dw[i][w]), bf16_lo(ow[i][w]), acc);
+            acc = __builtin_fmaf(bf16_hi(dw[i][w]), bf16_hi(ow[i][w]), acc);
+        }
+#pragma unroll
+        for (int m = LPR / 2; m >= 1; m >>= 1) acc += __shfl_xor(acc, m);
+        if (part == 0) sh[i * RPP + r] = acc;
+    }
+    __syncthreads();
+    const int t = threadIdx.x;
+    if (t < kStatRows && p0 + t < g.qN) {
+        const size_t li = (size_t)bh * g.qN + p0 + t;
+        nstat_d[li] = -sh[t];
         nstat_l[li] = -lse[li] / g.scale;
     }
 }
@@ -81,7 +99,7 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const bf16 *__restrict__ q, const bf16 *__restrict__ k, const bf16 *__restrict__ v,
     const bf16 *__restrict__ dO, const float *__restrict__ delta, const float *__restrict__ lse2,
     bf16 *__restrict__ dk, bf16 *__restrict__ dv, bf16 *__restrict__ ds, int64_t ds_tiles, SfaGeom g,
-    QBand bd)
+    QBand bd, int nsplit, float *__restrict__ split, SplitOrder order)
 {
     constexpr int DB = D / 32, KS = D / 16;
     using T = Tile<D>;
@@ -94,8 +112,19 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
 
     const int nkt = (g.len + kKeysPerWg - 1) / kKeysPerWg;
     const int nprob = g.B * g.Hkv * g.streams;
-    int prob, ktile;
-    decode_key_tile(blockIdx.x, nprob, nkt, prob, ktile);
+    // work item: a key tile's whole sweep, or with split sweeps (nsplit > 0) one half of
+    // the sweep of one of the first nsplit key tiles, the items taken longest first
+    int prob, ktile, half;
+    if (nsplit > 0) {
+        int rank;
+        decode_key_tile(blockIdx.x, nprob, nkt + nsplit, prob, rank);
+        const int code = order.item[rank];
+        ktile = code >> 2;
+        half = (code & 3) - 1;  // -1: the whole sweep, 0: its later half, 1: its earlier half
+    } else {
+        decode_key_tile(blockIdx.x, nprob, nkt, prob, ktile);
+        half = -1;
+    }
     const int s = prob % g.streams;
     const int hk = (prob / g.streams) % g.Hkv;
     const int b = prob / (g.streams * g.Hkv);
@@ -140,11 +169,18 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     // the last query tile of the sweep and as fp32 partials from earlier bands, and a
     // band after the one holding the first query tile adds to the partials.  Keys that
     // no query sees are written (as zeros) by the first band.
-    const int qt_first = max(qt_first_all, bd.qt_lo), qt_end = min(qt_end_all, bd.qt_hi);
+    int qt_first = max(qt_first_all, bd.qt_lo), qt_end = min(qt_end_all, bd.qt_hi);
     const bool unseen = qt_first_all >= qt_end_all;
     if (unseen ? bd.qt_lo != 0 : qt_first >= qt_end) return;  // uniform: nothing to do here
     const bool first_band = unseen || qt_first_all >= bd.qt_lo;
     const bool last_band = unseen || qt_end_all <= bd.qt_hi;
+    if (half >= 0) {  // one half of a split sweep (one pass only): the later tiles, or the earlier
+        const int mid = qt_first + (qt_end - qt_first) / 2;
+        if (half == 0)
+            qt_first = mid;
+        else
+            qt_end = mid;
+    }
     const int nqt = max(0, qt_end - qt_first);
     const int iters = g.G * nqt;
 
@@ -323,6 +359,25 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
             }
     }
     __syncthreads();
+    if (half >= 0 && qb == 0 && key < g.len) {
+        // one half of a split sweep: fp32 sums [half][dK, dV][problem][key][D]
+        const size_t slice = (size_t)nsplit * kKeysPerWg * D;
+        float *pk = split + ((size_t)(half * 2) * nprob + prob) * slice + (size_t)key * D;
+        float *pv = split + ((size_t)(half * 2 + 1) * nprob + prob) * slice + (size_t)key * D;
+#pragma unroll
+        for (int db = 0; db < DB; ++db)
+#pragma unroll
+            for (int rq = 0; rq < 4; ++rq) {
+                const f32x4 a = park[((0 * DB + db) * 4 + rq) * 64 + lane];
+                const f32x4 c = park[((1 * DB + db) * 4 + rq) * 64 + lane];
+                const int d0 = db * 32 + 8 * rq + 4 * hi;
+                *reinterpret_cast<f32x4 *>(pk + d0) = f32x4{adk[db][4 * rq] + a[0], adk[db][4 * rq + 1] + a[1],
+                                                            adk[db][4 * rq + 2] + a[2], adk[db][4 * rq + 3] + a[3]};
+                *reinterpret_cast<f32x4 *>(pv + d0) = f32x4{adv[db][4 * rq] + c[0], adv[db][4 * rq + 1] + c[1],
+                                                            adv[db][4 * rq + 2] + c[2], adv[db][4 * rq + 3] + c[3]};
+            }
+        return;
+    }
     if (qb == 0 && key < g.len) {
         const uint32_t off = kbase + (uint32_t)key * kstride;
         // fp32 partials of this problem's keys (query bands only): [key][D]
@@ -355,6 +410,35 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                 }
             }
     }
+}
+
+// dK, dV of the split key tiles: the two halves' fp32 sums added in a fixed order
+// (half 0, then half 1), scaled (dK) and rounded to bf16; four dims per thread.
+template <int D>
+__global__ __launch_bounds__(256) void dkdv_split_combine_kernel(const float *__restrict__ split,
+                                                                 int nsplit, bf16 *__restrict__ dk,
+                                                                 bf16 *__restrict__ dv, SfaGeom g)
+{
+    const int nprob = g.B * g.Hkv * g.streams;
+    const int keys = nsplit * kKeysPerWg;
+    const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (idx >= (int64_t)nprob * keys * (D / 4)) return;
+    const int d0 = (int)(idx % (D / 4)) * 4;
+    const int key = (int)(idx / (D / 4) % keys);
+    const int prob = (int)(idx / (D / 4) / keys);
+    if (key >= g.len) return;
+    const int s = prob % g.streams;
+    const int hk = (prob / g.streams) % g.Hkv;
+    const int b = prob / (g.streams * g.Hkv);
+    const size_t slice = (size_t)keys * D, at = (size_t)key * D + d0;
+    const f32x4 k0 = *reinterpret_cast<const f32x4 *>(split + (size_t)prob * slice + at);
+    const f32x4 v0 = *reinterpret_cast<const f32x4 *>(split + ((size_t)nprob + prob) * slice + at);
+    const f32x4 k1 = *reinterpret_cast<const f32x4 *>(split + ((size_t)2 * nprob + prob) * slice + at);
+    const f32x4 v1 = *reinterpret_cast<const f32x4 *>(split + ((size_t)3 * nprob + prob) * slice + at);
+    const f32x4 ks = (k0 + k1) * g.scale, vs = v0 + v1;
+    const size_t off = ((size_t)b * g.N + (size_t)key * g.rowmul + s) * g.Hkv * D + (size_t)hk * D + d0;
+    *reinterpret_cast<u32x2 *>(dk + off) = u32x2{pack_bf16(ks[0], ks[1]), pack_bf16(ks[2], ks[3])};
+    *reinterpret_cast<u32x2 *>(dv + off) = u32x2{pack_bf16(vs[0], vs[1]), pack_bf16(vs[2], vs[3])};
 }
 
 // KK keys per ring step, S ring stages.  <32, 2> takes 48 KB of LDS at D=128, so two
@@ -518,9 +602,8 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o
                       const SfaGeom &g, hipStream_t s, const char *st_name, const char *dq_name,
                       const char *dkdv_name)
 {
-    const int64_t rows = (int64_t)g.B * g.qN * g.Hq;
     timing_before(st_name, s);
-    bwd_stats_bf16_kernel<D><<<(unsigned)((rows * (D / 8) + 255) / 256), 256, 0, s>>>(
+    bwd_stats_bf16_kernel<D><<<(unsigned)((g.qN + kStatRows - 1) / kStatRows * g.B * g.Hq), 256, 0, s>>>(
         o, dO, lse, delta, lse2, g);
     hipError_t e = hipGetLastError();
     timing_after(s);
@@ -560,12 +643,27 @@ hipError_t bwd_bf16_d(const bf16 *q, const bf16 *k, const bf16 *v, const bf16 *o
         bd.part_k = one_pass ? nullptr : reinterpret_cast<float *>(wsb + w.part_k);
         bd.part_v = one_pass ? nullptr : reinterpret_cast<float *>(wsb + w.part_v);
         const int64_t band_tiles = tiles(qa, qb);
+        // one pass only: the longest sweeps of a small grid are split in halves
+        const int nsplit = one_pass ? w.nsplit : 0;
+        float *split = reinterpret_cast<float *>(wsb + w.split);
+        SplitOrder order;
+        if (nsplit > 0) order = dkdv_split_order(g, nsplit);
         timing_before(dkdv_name, s);
-        sfa_dkdv_bf16_kernel<D><<<nkt * g.B * g.Hkv * g.streams, kDkdvWaves * 64, 0, s>>>(
-            q, k, v, dO, delta, lse2, dk, dv, ds, band_tiles, g, bd);
+        sfa_dkdv_bf16_kernel<D><<<(nkt + nsplit) * g.B * g.Hkv * g.streams, kDkdvWaves * 64, 0, s>>>(
+            q, k, v, dO, delta, lse2, dk, dv, ds, band_tiles, g, bd, nsplit, split, order);
         e = hipGetLastError();
         timing_after(s);
         if (e != hipSuccess) return e;
+        if (nsplit > 0) {
+            const int64_t n4 = (int64_t)g.B * g.Hkv * g.streams * nsplit * kKeysPerWg * (D / 4);
+            timing_before(D == 32 ? "sfa_dkdv_split_combine_d32"
+                                  : D == 64 ? "sfa_dkdv_split_combine_d64" : "sfa_dkdv_split_combine_d128",
+                          s);
+            dkdv_split_combine_kernel<D><<<(unsigned)((n4 + 255) / 256), 256, 0, s>>>(split, nsplit, dk, dv, g);
+            e = hipGetLastError();
+            timing_after(s);
+            if (e != hipSuccess) return e;
+        }
         const int nrb = (min(qb * kDsRows, g.qlen) + kRowsPerWg - 1) / kRowsPerWg - qa / kBandUnit;
         const int64_t wgs = nrb * nprob_q;
         timing_before(dq_name, s);

@@ -141,6 +141,35 @@ def test_workspace_size_formula(lib):
     assert lib.hd_sfa_bwd_workspace_bytes(1, 8, 2, 4, 2, 48, 0, 0) == 0  # D
 
 
+def _sweep(len_, kt):
+    """64-row query tiles [first, end) of a causal problem (no window) with a row that
+    sees a key of 128-key tile kt."""
+    return kt * 128 // 64, -(-len_ // 64)
+
+
+def test_split_sweep_workspace(lib):
+    """Small dK/dV grids (under 512 workgroups) with at least four key tiles split the
+    sweeps longer than half the longest one; the one-pass workspace then also holds
+    their two halves' fp32 partials: 4 x key problems x split keys x D floats."""
+    a256 = lambda x: math.ceil(x / 256) * 256
+    for B, L, n, Hq, Hkv, D, mode in ((2, 2048, 1, 32, 8, 128, 0), (1, 1000, 1, 2, 2, 64, 1),
+                                      (1, 2000, 2, 8, 1, 64, 0), (1, 4096, 4, 32, 8, 128, 0)):
+        len_, streams = (L, n) if mode == 0 else (n * L, 1)
+        nkt = -(-len_ // 128)
+        kprobs = B * Hkv * streams
+        lens = [e - f for f, e in (_sweep(len_, kt) for kt in range(nkt))]
+        ns = 0
+        if nkt >= 4 and nkt * kprobs < 512:
+            while ns < nkt and 2 * lens[ns] > max(lens) and lens[ns] >= 2:
+                ns += 1
+        stats = 2 * a256(B * Hq * n * L * 4)
+        ds = B * Hq * streams * _ds_tiles(len_) * 16384
+        want = stats + ds + 4 * kprobs * ns * 128 * D * 4
+        assert lib.hd_sfa_bwd_workspace_bytes(B, L, n, Hq, Hkv, D, mode, 0) == want, (B, L, n, mode, ns)
+        if (B, L, n) == (2, 2048, 1):
+            assert ns == 8  # the n=1 sweep shape: key tiles 0..7 of 16
+
+
 def _ds_tiles_of_query_tiles(len_, qts):
     """dS tiles holding a visible pair of a causal problem (no window), for the listed
     64-row query tiles, by brute force over the tiles' pairs."""

@@ -31,7 +31,9 @@ ULP_REL = 2.0 ** -7  # dK/dV of banded and one-pass runs: bf16 roundings of near
 
 
 def _dkdv_launches():
-    return sum(n for name, n, _ in hd.hd_timing_collect() if name.startswith("sfa_dkdv"))
+    """dK/dV sweep launches (one per query band; a split-sweep combine is not one)."""
+    return sum(n for name, n, _ in hd.hd_timing_collect()
+               if name.startswith("sfa_dkdv") and "combine" not in name)
 
 
 def _backward(q, k, v, o, lse, do, *, n, mode, scale, window, final, ws_bytes):
