@@ -8,7 +8,7 @@
 //   1. a stable sort of the (id, token position) pairs by id; ids outside [0, V) get
 //      the key V and sort to the end.  Up to kSmallSortMax tokens the sorted position
 //      of a token is counted directly (the number of tokens whose (key, position) is
-//      smaller, all keys held in LDS; one launch).  Larger batches take an LSD radix
+//      smaller; one launch spread over M / 16 workgroups).  Larger batches take an LSD radix
 //      sort with 8-bit digits (per-block digit histograms, one device-wide exclusive
 //      scan, then a scatter in which every block ranks its chunk stably with eight
 //      1-bit splits in LDS);
@@ -244,39 +244,53 @@ __global__ __launch_bounds__(kThreads) void radix_scatter_kernel(
 
 // ---------------------------------------------------------------- small batches
 
-constexpr int kRankWaves = 16;  // a workgroup ranks 64 tokens, each wave over 1/16 of the keys
+constexpr int kRankWaves = 16;   // the segment pass: one workgroup of 16 waves
+constexpr int kRankTokens = 16;  // tokens a rank workgroup places
+constexpr int kRankChunks = 16;  // key chunks per token, one thread each
 
 // Stable sort by counting: token i goes to position #{j : key_j < key_i, or key_j ==
-// key_i and j < i}, which is the position the stable radix sort gives it.  One lane
-// per token; the 16 waves of a workgroup count over disjoint sixteenths of the keys
-// (read from LDS, where every lane of a wave reads the same word) and add up in LDS.
-__global__ __launch_bounds__(kRankWaves * 64) void rank_sort_kernel(
+// key_i and j < i}, which is the position the stable radix sort gives it.  A
+// workgroup of 256 threads places 16 tokens: thread (c, i) counts over every 16th key
+// from c (all M keys staged in LDS) for token i, and the 16 counts of a token are
+// added in LDS, so the M x M comparisons spread over M / 16 workgroups (every CU at
+// the 36-layer step's 4096 tokens).
+__global__ __launch_bounds__(kRankTokens * kRankChunks) void rank_sort_kernel(
     const int32_t *__restrict__ ids, int M, int64_t V, uint32_t *__restrict__ keys_out,
     int32_t *__restrict__ vals_out)
 {
-    __shared__ __attribute__((aligned(16))) uint32_t sk[kSmallSortMax];
-    __shared__ int cnt[kRankWaves][64];
-    for (int j = threadIdx.x; j < M; j += kRankWaves * 64) sk[j] = id_key(ids, j, V);
-    __syncthreads();
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int i = blockIdx.x * 64 + lane;
-    const uint32_t ki = i < M ? sk[i] : 0xffffffffu;
-    const int per = ((M + kRankWaves - 1) / kRankWaves + 3) & ~3;  // multiple of 4
-    const int j0 = wave * per, j1 = min(M, j0 + per);
-    int c = 0;
-    int j = j0;
-    for (; j + 4 <= j1; j += 4) {
-        const u32x4 kj = *reinterpret_cast<const u32x4 *>(&sk[j]);
+    __shared__ uint32_t sk[kSmallSortMax];
+    __shared__ int cnt[kRankChunks][kRankTokens];
+    // all of a thread's ids in flight at once (up to 64 at kSmallSortMax tokens)
+    constexpr int kFill = kSmallSortMax / (kRankTokens * kRankChunks);
+    uint32_t fk[kFill];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) c += (kj[e] < ki || (kj[e] == ki && j + e < i)) ? 1 : 0;
+    for (int f = 0; f < kFill; ++f) {
+        const int j = f * kRankTokens * kRankChunks + threadIdx.x;
+        fk[f] = j < M ? id_key(ids, j, V) : 0u;
     }
-    for (; j < j1; ++j) c += (sk[j] < ki || (sk[j] == ki && j < i)) ? 1 : 0;
-    cnt[wave][lane] = c;
+#pragma unroll
+    for (int f = 0; f < kFill; ++f) {
+        const int j = f * kRankTokens * kRankChunks + threadIdx.x;
+        if (j < M) sk[j] = fk[f];
+    }
     __syncthreads();
-    if (wave == 0 && i < M) {
+    const int t = threadIdx.x % kRankTokens, c = threadIdx.x / kRankTokens;
+    const int i = blockIdx.x * kRankTokens + t;
+    const uint32_t ki = i < M ? sk[i] : 0xffffffffu;
+    // chunk c: keys c, c + 16, ... (the 16 threads of a chunk read the same word, the
+    // four chunks of a wave four consecutive words)
+    int n = 0;
+#pragma unroll 8
+    for (int j = c; j < M; j += kRankChunks) {
+        const uint32_t kj = sk[j];
+        n += (kj < ki || (kj == ki && j < i)) ? 1 : 0;
+    }
+    cnt[c][t] = n;
+    __syncthreads();
+    if (c == 0 && i < M) {
         int r = 0;
 #pragma unroll
-        for (int w = 0; w < kRankWaves; ++w) r += cnt[w][lane];
+        for (int cc = 0; cc < kRankChunks; ++cc) r += cnt[cc][t];
         keys_out[r] = ki;
         vals_out[r] = i;
     }
@@ -515,7 +529,8 @@ hipError_t launch_embed_bwd(const int32_t *ids, const void *dout, int B, int L, 
     const uint32_t *kin = nullptr;
     const int32_t *vin = nullptr;
     if (M <= kSmallSortMax) {
-        rank_sort_kernel<<<(M + 63) / 64, kRankWaves * 64, 0, s>>>(ids, M, V, ka, va);
+        rank_sort_kernel<<<(M + kRankTokens - 1) / kRankTokens, kRankTokens * kRankChunks, 0, s>>>(
+            ids, M, V, ka, va);
         small_segments_kernel<<<1, kRankWaves * 64, 0, s>>>(ka, M, V, seg_start, uniq, num_uniq);
         kin = ka;
         vin = va;
