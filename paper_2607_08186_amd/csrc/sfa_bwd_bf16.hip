@@ -288,35 +288,61 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
                     pacc[4 * rq + e] = d4[e];
                 }
             }
+            // operands of k-step kk + 2 read while the MFMAs of k-step kk run (two
+            // k-steps in flight); scheduling barriers keep the reads where they are
+            bf16x8 oq[2], ok[2], od[2], ov[2];
+            auto rd = [&](int kk, int sl) __attribute__((always_inline)) {
+                oq[sl] = T::row_operand(qt, qb * 32 + l32, kk, hi);
+                ok[sl] = T::row_operand(ktl, krow, kk, hi);
+                od[sl] = T::row_operand(dot, qb * 32 + l32, kk, hi);
+                ov[sl] = T::row_operand(vtl, krow, kk, hi);
+            };
+            rd(0, 0);
+            rd(1, 1);
+            __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
             for (int kk = 0; kk < KS; ++kk) {
-                sacc = mfma32(T::row_operand(qt, qb * 32 + l32, kk, hi),
-                              T::row_operand(ktl, krow, kk, hi), sacc);
-                pacc = mfma32(T::row_operand(dot, qb * 32 + l32, kk, hi),
-                              T::row_operand(vtl, krow, kk, hi), pacc);
+                sacc = mfma32(oq[kk & 1], ok[kk & 1], sacc);
+                pacc = mfma32(od[kk & 1], ov[kk & 1], pacc);
+                if (kk + 2 < KS) rd(kk + 2, kk & 1);
+                __builtin_amdgcn_sched_barrier(0);
             }
-            // statistics and the first operands up front, then each MFMA's operands
-            // about three MFMAs ahead
-            sched_pattern<12, 2 * KS, 1, 2, 0>();
             uint32_t pw[8], dw[8];
+            // dV += dO^T P and dK += Q^T dS in 4*DB MFMAs; operand i belongs to 16-query
+            // group h, dim block db and dV (i even) or dK (i odd).  Each operand is read
+            // three MFMAs ahead, the first three while the softmax runs.
+            constexpr int NOP = 4 * DB, AHEAD = 3;
+            bf16x8 ot[AHEAD + 1];
+            auto rdt = [&](int i) __attribute__((always_inline)) {
+                ot[i % (AHEAD + 1)] = T::tr_operand((i & 1) ? qt : dot, ((i >> 1) % DB) * 32,
+                                                    qb * 2 + i / (2 * DB), lane);
+            };
+#pragma unroll
+            for (int i = 0; i < AHEAD; ++i) rdt(i);
+            __builtin_amdgcn_sched_barrier(0);
             if (qpos(g, qlo) < kw0 + 31 || qpos(g, qlo + 31) - kw0 >= g.window)  // diagonal or window edge
                 softmax(sacc, pacc, qlo, pw, dw, std::true_type{});
             else
                 softmax(sacc, pacc, qlo, pw, dw, std::false_type{});
+            bf16x8 pb[2], dsb[2];
 #pragma unroll
             for (int h = 0; h < 2; ++h) {
-                const bf16x8 pb = __builtin_bit_cast(
+                pb[h] = __builtin_bit_cast(
                     bf16x8, u32x4{pw[h * 4], pw[h * 4 + 1], pw[h * 4 + 2], pw[h * 4 + 3]});
-                const bf16x8 dsb = __builtin_bit_cast(
+                dsb[h] = __builtin_bit_cast(
                     bf16x8, u32x4{dw[h * 4], dw[h * 4 + 1], dw[h * 4 + 2], dw[h * 4 + 3]});
-                const int kk = qb * 2 + h;  // 16-row group of the 64-row tile
-#pragma unroll
-                for (int db = 0; db < DB; ++db) {
-                    adv[db] = mfma32(T::tr_operand(dot, db * 32, kk, lane), pb, adv[db]);
-                    adk[db] = mfma32(T::tr_operand(qt, db * 32, kk, lane), dsb, adk[db]);
-                }
             }
-            sched_pattern<8, 4 * DB, 1, 2, 0>();
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int i = 0; i < NOP; ++i) {
+                const int h = i / (2 * DB), db = (i >> 1) % DB;
+                if (i & 1)
+                    adk[db] = mfma32(ot[i % (AHEAD + 1)], dsb[h], adk[db]);
+                else
+                    adv[db] = mfma32(ot[i % (AHEAD + 1)], pb[h], adv[db]);
+                if (i + AHEAD < NOP) rdt(i + AHEAD);
+                __builtin_amdgcn_sched_barrier(0);
+            }
             // dw[0..7] hold queries 8 rq + 4 hi .. +3 of my key (rq = 0..3) in the order of
             // the tile layout: 32 contiguous bytes per lane
 #pragma unroll
