@@ -137,8 +137,6 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const rsrc_t rv = make_rsrc(v + b * kslice, (uint32_t)(kslice * 2));
     const rsrc_t rdk = make_rsrc(dk + b * kslice, (uint32_t)(kslice * 2));
     const rsrc_t rdv = make_rsrc(dv + b * kslice, (uint32_t)(kslice * 2));
-    const rsrc_t rl2 = make_rsrc(lse2 + b * lslice, (uint32_t)(lslice * 4));
-    const rsrc_t rdl = make_rsrc(delta + b * lslice, (uint32_t)(lslice * 4));
     const uint32_t qstride = (uint32_t)g.qrowmul * g.Hq * D * 2;
     const uint32_t kstride = (uint32_t)g.rowmul * g.Hkv * D * 2;
     const uint32_t kbase = (uint32_t)(s * g.Hkv + hk) * D * 2;
@@ -203,18 +201,23 @@ __global__ __launch_bounds__(kDkdvWaves * 64, 1) void sfa_dkdv_bf16_kernel(
     const char *vtl = kvt + (kKeysPerWg / kRows + (kw >> 1)) * T::BYTES;
     const int krow = (kw & 1) * 32 + l32;                                      // my key's row there
 
+    // Loads of a query tile: per-lane offsets computed once (rows are relative to the
+    // tile's first row); rows past the end of the problem lie past the end of the
+    // batch's buffer range and load zeros.  The row statistics take a buffer range of
+    // one query head, so their rows past the end load zeros as well.
+    const auto qplan = T::template dma_plan<kDkdvWaves>(0, qstride, wave, lane);
+    const uint32_t stat_lane = (uint32_t)(lane * g.qrowmul + s) * 4;
     auto issue = [&](int gi, int qt, int st) __attribute__((always_inline)) {
         const int hq = hk * g.G + gi;
-        const uint32_t qbase = (uint32_t)(s * g.Hq + hq) * D * 2;
         const int row0 = qt * kRows;
+        const uint32_t row0_off = (uint32_t)(s * g.Hq + hq) * D * 2 + (uint32_t)row0 * qstride;
         char *base = smem + st * STAGE;
-        T::load(base, rq, qbase, qstride, row0, g.qlen, wave, kDkdvWaves, lane);
-        T::load(base + T::BYTES, rdo, qbase, qstride, row0, g.qlen, wave, kDkdvWaves, lane);
+        T::load(base, rq, qplan, row0_off, wave);
+        T::load(base + T::BYTES, rdo, qplan, row0_off, wave);
         if (wave < 2) {  // per-row lse2 (wave 0) and delta (wave 1), 4 bytes per lane
-            const int row = row0 + lane;
-            const uint32_t off =
-                row < g.qlen ? (uint32_t)(((size_t)hq * g.qN + (size_t)row * g.qrowmul + s) * 4) : kOob;
-            dma_lds4(wave == 0 ? rl2 : rdl, base + 2 * T::BYTES + wave * kRows * 4, off);
+            const float *sbase = (wave == 0 ? lse2 : delta) + b * lslice + (size_t)hq * g.qN;
+            dma_lds4(make_rsrc(sbase, (uint32_t)g.qN * 4), base + 2 * T::BYTES + wave * kRows * 4,
+                     stat_lane + (uint32_t)row0 * g.qrowmul * 4);
         }
     };
     if (iters > 0) issue(0, qt_end - 1, 0);
@@ -538,10 +541,13 @@ __global__ __launch_bounds__(kDqWaves * 64, 1) void sfa_dq_bf16_kernel(
     };
     static_assert((S - 2) * (T::INSTR / kDqWaves + 1 + kSlab / 1024) <= 15,
                   "outstanding loads must fit the vmcnt wait");
+    // K rows of a step: per-lane offsets computed once; rows past the end of the
+    // problem lie past the end of the batch's buffer range and load zeros
+    const auto kplan = T::template dma_plan<kDqWaves>(kbase, kstride, wave, lane);
     auto issue = [&](int j) __attribute__((always_inline)) {
         if (j >= nkt) return;
         char *st = smem[(j - jf) % S];
-        T::load(st, rk, kbase, kstride, j * KK, g.len, wave, kDqWaves, lane);
+        T::load(st, rk, kplan, (uint32_t)(j * KK) * kstride, wave);
         if (active(j)) {
             const int64_t t = ds_tile_index(band, kt_lo, qt, j / kSteps) - bd.ds_base;
             const rsrc_t rt = make_rsrc(ds_prob + t * (kDsTileBytes / 2), kDsTileBytes);
