@@ -27,7 +27,7 @@ namespace {
 
 constexpr int kWaves = 8;
 constexpr int kBM = kWaves * 32;           // query rows per workgroup
-constexpr int kLoaders = 2;                // waves 6 and 7 issue the tile loads
+constexpr int kLoaders = 4;                // group B (waves 4-7) issues the tile loads
 constexpr float kRescaleThreshold = 8.0f;  // log2 units
 
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
@@ -100,14 +100,15 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     }
 
     // per-lane address parts (K and V share the row layout)
-    const bool loader = wave >= kWaves - kLoaders;  // waves that see every tile
+    const bool loader = wave >= kWaves - kLoaders;  // the waves of group B
     const int lw = loader ? wave - (kWaves - kLoaders) : 0;
     const auto dma = T::template dma_plan<kLoaders>(kbase0, kstride, lw, lane);
     uint32_t kro[KS], vto[DB][2];
     T::row_offsets(l32, hi, kro);
     T::tr_offsets(lane, vto);
-    // loader waves queue K of tile t+2 and V of tile t+1 in their vector phase of tile
-    // t and wait for them at the end of their next phase
+    // loader waves queue their shares of K of tile t+2 and V of tile t+1 in their
+    // vector phase of tile t (or, once past their last tile, before the barrier that
+    // ends it) and wait for them at the end of their next phase
     auto issue = [&](int t) __attribute__((always_inline)) {
         if (loader) {
             if (t + 2 < ntl)
@@ -239,11 +240,13 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
     // phase per workgroup barrier.  Group B starts one phase after group A, so on every
     // SIMD one wave feeds the matrix unit while the other uses the vector unit.  Waves
     // that finish early pass the remaining barriers idle; every wave passes
-    // 2*ntl + 2 of them.  Loads (loader waves, group B, whose jlast is ntl-1): K of
-    // t+2 goes to the slot of K of t, V of t+1 to the slot of V of t-1, both last read
-    // in the matrix phases of tile t-1 (phases 2t, 2t+1); they are queued in phase
-    // 2t+2 and published by the barrier of phase 2t+3, before group A's matrix phase
-    // of tile t+1 (phase 2t+4).
+    // 2*ntl + 2 of them.  Loads (the four waves of group B, each a quarter of a tile,
+    // also those whose rows end before the block's last key tile): K of t+2 goes to
+    // the slot of K of t, V of t+1 to the slot of V of t-1, both last read in the
+    // matrix phases of tile t-1 (phases 2t, 2t+1); they are queued in phase 2t+2 and
+    // published by the barrier of phase 2t+3, before group A's matrix phase of tile
+    // t+1 (phase 2t+4).  A group B wave passes barrier 2t+2 right after queueing the
+    // loads of tile t and barrier 2t+3 right after waiting for them.
     using F = std::false_type;
     using Tr = std::true_type;
     using Z = std::integral_constant<int, 0>;
@@ -287,7 +290,15 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
         mfma_phase(t, F{}, Tr{}, Z{}, Z{});
     if (loader) wait_vmcnt_le(0);
     bar();
-    while (nb < 2 * ntl + 2) bar();
+    while (nb < 2 * ntl + 2) {  // idle: past this wave's last tile
+        if (loader) {
+            if ((nb & 1) == 0)
+                issue((nb - 2) >> 1);  // barrier 2t+2 ends the vector phase of tile t
+            else
+                wait_vmcnt_le(0);      // barrier 2t+3 ends its matrix phase
+        }
+        bar();
+    }
 
     const float l = lsum0 + lsum1 + __shfl_xor(lsum0 + lsum1, 32);
     if (row < g.qlen) {
