@@ -77,6 +77,21 @@ __device__ inline float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xffff0
 
 __device__ inline float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// Max / sum of v over lanes l and l ^ 32 (the two halves of the wave), in registers:
+// v_permlane32_swap exchanges the upper half of one copy with the lower half of the
+// other, so the two results hold v of both halves for every lane (no LDS round trip,
+// which a cross-half shuffle otherwise takes).
+__device__ inline float max_xor32(float v)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ inline float sum_xor32(float v)
+{
+    const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+    return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // Workgroup id -> (problem, row tile).  Tiles with the longest causal extent go first.
 // Consecutive workgroup ids are spread round-robin over the 8 XCDs, so when the
 // problem count allows it each XCD gets a contiguous band of problems (the query heads

@@ -155,7 +155,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 2) void sfa_decode_partial_kernel(
                 sc[mb][r] = vis ? sc[mb][r] * c2 : -INFINITY;
                 mx = fmaxf(mx, sc[mb][r]);
             }
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        mx = max_xor32(mx);
         const float me = mx == -INFINITY ? 0.f : mx;  // no visible row: weights exp2(-inf) = 0
         bf16x8 pb[4];
         const bf16x2 ones = __builtin_bit_cast(bf16x2, 0x3f803f80u);
@@ -174,7 +174,7 @@ __global__ __launch_bounds__(kDecWaves * 64, 2) void sfa_decode_partial_kernel(
                 }
                 pb[mb * 2 + h] = __builtin_bit_cast(bf16x8, u32x4{w[0], w[1], w[2], w[3]});
             }
-        lsum += __shfl_xor(lsum, 32);
+        lsum = sum_xor32(lsum);
         // O^T (dims x slots) = V^T P^T over my 64 rows
 #pragma unroll
         for (int db = 0; db < DB; ++db)

@@ -192,7 +192,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
             for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[mb][r]);
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        mx = max_xor32(mx);
         const float mcand = fmaxf(m2, mx * c2);
         if (__any(mcand > m2 + kRescaleThreshold)) {
             const float alpha = mcand == -INFINITY ? 1.f : fast_exp2(m2 - mcand);
@@ -300,7 +300,7 @@ __global__ __launch_bounds__(kWaves * 64, 1) void sfa_fwd_bf16_kernel(
         bar();
     }
 
-    const float l = lsum0 + lsum1 + __shfl_xor(lsum0 + lsum1, 32);
+    const float l = sum_xor32(lsum0 + lsum1);
     if (row < g.qlen) {
         const float inv = 1.f / l;
         const uint32_t obase = qbase + (uint32_t)row * qstride;
