@@ -260,18 +260,19 @@ __global__ __launch_bounds__(kRankTokens * kRankChunks) void rank_sort_kernel(
 {
     __shared__ uint32_t sk[kSmallSortMax];
     __shared__ int cnt[kRankChunks][kRankTokens];
-    // all of a thread's ids in flight at once (up to 64 at kSmallSortMax tokens)
+    // all of a thread's ids in flight at once (64 at kSmallSortMax tokens): buffer loads
+    // past the M ids return 0 instead of being branched around, so that no load waits
+    // for the one before it
     constexpr int kFill = kSmallSortMax / (kRankTokens * kRankChunks);
-    uint32_t fk[kFill];
+    const rsrc_t rid = make_rsrc(ids, (uint32_t)M * 4);
+    int32_t fid[kFill];
+#pragma unroll
+    for (int f = 0; f < kFill; ++f)
+        fid[f] = (int32_t)ld4(rid, (uint32_t)(f * kRankTokens * kRankChunks + threadIdx.x) * 4);
 #pragma unroll
     for (int f = 0; f < kFill; ++f) {
         const int j = f * kRankTokens * kRankChunks + threadIdx.x;
-        fk[f] = j < M ? id_key(ids, j, V) : 0u;
-    }
-#pragma unroll
-    for (int f = 0; f < kFill; ++f) {
-        const int j = f * kRankTokens * kRankChunks + threadIdx.x;
-        if (j < M) sk[j] = fk[f];
+        if (j < M) sk[j] = fid[f] >= 0 && (int64_t)fid[f] < V ? (uint32_t)fid[f] : (uint32_t)V;
     }
     __syncthreads();
     const int t = threadIdx.x % kRankTokens, c = threadIdx.x / kRankTokens;
@@ -299,34 +300,48 @@ __global__ __launch_bounds__(kRankTokens * kRankChunks) void rank_sort_kernel(
 // Segments of a sorted key array of M <= kSmallSortMax entries in one workgroup: the
 // head of every run of equal keys gets its run's index (a block scan of the head
 // flags), its start and, for in-range keys, its id; the run of key V (if any) is the
-// last one and is not counted as a distinct id.
+// last one and is not counted as a distinct id.  Each thread takes kPer consecutive
+// keys and the one before them with branch-free buffer loads (zeros past the end).
 __global__ __launch_bounds__(kRankWaves * 64) void small_segments_kernel(
     const uint32_t *__restrict__ keys, int M, int64_t V, int *__restrict__ seg_start,
     int32_t *__restrict__ uniq, int32_t *__restrict__ num_uniq)
 {
     constexpr int kPer = kSmallSortMax / (kRankWaves * 64);
+    static_assert(kPer % 4 == 0, "whole 16-byte loads");
     __shared__ int sh[kRankWaves + 1];
+    const rsrc_t rk = make_rsrc(keys, (uint32_t)M * 4);
     const int i0 = threadIdx.x * kPer;
-    int heads = 0;
+    uint32_t k[kPer];
+#pragma unroll
+    for (int e = 0; e < kPer; e += 4) {
+        const u32x4 w = ld16(rk, (uint32_t)(i0 + e) * 4);
+        k[e] = w[0];
+        k[e + 1] = w[1];
+        k[e + 2] = w[2];
+        k[e + 3] = w[3];
+    }
+    const uint32_t before = i0 > 0 ? ld4(rk, (uint32_t)(i0 - 1) * 4) : 0u;
+    uint32_t head = 0;  // bit e: key i0 + e starts a run
 #pragma unroll
     for (int e = 0; e < kPer; ++e) {
         const int i = i0 + e;
-        if (i < M && (i == 0 || keys[i] != keys[i - 1])) ++heads;
+        const uint32_t prev = e == 0 ? before : k[e - 1];
+        if (i < M && (i == 0 || k[e] != prev)) head |= 1u << e;
     }
     int S;
-    int u = block_exclusive_scan<kRankWaves>(heads, &S, sh);
+    int u = block_exclusive_scan<kRankWaves>(__builtin_popcount(head), &S, sh);
 #pragma unroll
     for (int e = 0; e < kPer; ++e) {
-        const int i = i0 + e;
-        if (i < M && (i == 0 || keys[i] != keys[i - 1])) {
-            seg_start[u] = i;
-            if (keys[i] < (uint64_t)V) uniq[u] = (int32_t)keys[i];
+        if ((head >> e) & 1u) {
+            seg_start[u] = i0 + e;
+            if (k[e] < (uint64_t)V) uniq[u] = (int32_t)k[e];
             ++u;
         }
-    }
-    if (threadIdx.x == 0) {
-        seg_start[S] = M;
-        *num_uniq = S - (keys[M - 1] == (uint64_t)V ? 1 : 0);
+        // the thread holding the last key closes the last run
+        if (i0 + e == M - 1) {
+            seg_start[S] = M;
+            *num_uniq = S - (k[e] == (uint64_t)V ? 1 : 0);
+        }
     }
 }
 
