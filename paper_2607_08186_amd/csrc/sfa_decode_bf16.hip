@@ -252,19 +252,23 @@ __global__ __launch_bounds__(D) void sfa_decode_combine_kernel(const float *__re
     const int cl = klo / kDecChunk;
     const float *src = part + (size_t)prob * g.nchunk * g.nslot * (D + 2) + slot * (D + 2);
     const size_t cstep = (size_t)g.nslot * (D + 2);
-    // one pass with a running maximum; every chunk in [cl, nc) has a visible row for
-    // some query of the problem, but possibly none for this one (max -inf, sum 0)
-    float m = -INFINITY, acc = 0.f, l = 0.f;
-#pragma unroll 4
+    // Every chunk in [cl, nc) has a visible row for some query of the problem, but
+    // possibly none for this one (max -inf, sum 0); the query's own key is in one of
+    // them, so the largest maximum m is finite.  Two passes, m first and then each
+    // chunk's share scaled by exp2(mc - m): no load waits for the previous chunk's
+    // arithmetic, as it would with a running maximum.
+    float m = -INFINITY;
+#pragma unroll 8
+    for (int c = cl; c < nc; ++c) m = fmaxf(m, src[c * cstep + D]);
+    float acc = 0.f, l = 0.f;
+#pragma unroll 8
     for (int c = cl; c < nc; ++c) {
         const float mc = src[c * cstep + D], lc = src[c * cstep + D + 1];
         const float oc = src[c * cstep + threadIdx.x];
-        if (mc == -INFINITY) continue;
-        const float mn = fmaxf(m, mc);
-        const float a = fast_exp2(m - mn), bc = fast_exp2(mc - mn);  // exp2(-inf) = 0
-        acc = acc * a + oc * bc;
-        l = l * a + lc * bc;
-        m = mn;
+        const float w = fast_exp2(mc - m);  // exp2(-inf) = 0
+        // a chunk without a visible row is skipped (select, no branch)
+        acc = mc == -INFINITY ? acc : __builtin_fmaf(oc, w, acc);
+        l = mc == -INFINITY ? l : __builtin_fmaf(lc, w, l);
     }
     const size_t row = ((size_t)b * g.n + s) * g.Hq + hq;
     o[row * D + threadIdx.x] = (bf16)(acc / l);
