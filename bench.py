@@ -338,6 +338,9 @@ def main():
                 ent["back_to_back_gbs"] = copy_ceiling["expand_gbs"]
                 ent["copy_gbs"] = copy_ceiling["gbs"]
                 ent["of_copy"] = round(copy_ceiling["expand_gbs"] / copy_ceiling["gbs"], 3)
+                ent["cold_gbs"] = copy_ceiling["cold_expand_gbs"]
+                ent["cold_copy_gbs"] = copy_ceiling["cold_gbs"]
+                ent["cold_of_copy"] = round(copy_ceiling["cold_expand_gbs"] / copy_ceiling["cold_gbs"], 3)
         if fam in ("final_gather", "final_gather_bwd"):
             nbytes = W.final_gather_bytes(1, s.L, s.n, W.STACK_DMODEL, fam == "final_gather_bwd")
             ent["gbs"] = round(nbytes / (ms * 1e-3) / 1e9, 1)
@@ -435,14 +438,39 @@ def time_expand_vs_copy(hd, torch, ids, tables, emb, s, W, stream, reps=20):
         torch.cuda.synchronize()
         return t0.elapsed_time(t1) / reps
 
-    ms_copy = b2b(lambda: dst.copy_(src))
-    ms_exp = b2b(lambda: hd.hd_expand_embed(ids, tables, emb, 1, s.L, s.n, W.STACK_VOCAB,
-                                            W.STACK_DMODEL, stream=stream))
-    return {"bytes": nbytes, "ms": round(ms_copy, 5), "gbs": round(nbytes / (ms_copy * 1e-3) / 1e9, 1),
-            "expand_ms": round(ms_exp, 5), "expand_gbs": round(nbytes / (ms_exp * 1e-3) / 1e9, 1),
+    flush = torch.empty(1 << 30, dtype=torch.uint8, device=src.device)
+
+    def cold(fn):
+        """Median of single launches, each after writing 1 GiB elsewhere (which evicts
+        the 256 MB Infinity Cache and the L2s), as the step's expansion finds them."""
+        ts = []
+        for i in range(reps // 2):
+            flush.fill_(i & 255)
+            t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            t0.record(stream)
+            fn()
+            t1.record(stream)
+            torch.cuda.synchronize()
+            ts.append(t0.elapsed_time(t1))
+        return sorted(ts)[len(ts) // 2]
+
+    copy = lambda: dst.copy_(src)  # noqa: E731
+    expand = lambda: hd.hd_expand_embed(ids, tables, emb, 1, s.L, s.n, W.STACK_VOCAB,  # noqa: E731
+                                        W.STACK_DMODEL, stream=stream)
+    ms_copy, ms_exp = b2b(copy), b2b(expand)
+    cold_copy, cold_exp = cold(copy), cold(expand)
+    del flush
+    gbs = lambda ms: round(nbytes / (ms * 1e-3) / 1e9, 1)  # noqa: E731
+    return {"bytes": nbytes, "ms": round(ms_copy, 5), "gbs": gbs(ms_copy),
+            "expand_ms": round(ms_exp, 5), "expand_gbs": gbs(ms_exp),
+            "cold_ms": round(cold_copy, 5), "cold_gbs": gbs(cold_copy),
+            "cold_expand_ms": round(cold_exp, 5), "cold_expand_gbs": gbs(cold_exp),
             "reps": reps,
             "what": "torch copy_ of the expansion's output size (read + write bytes) and the "
-                    "expansion itself, each timed back to back over the reps"}
+                    "expansion itself, each timed back to back over the reps (warm: the "
+                    "previous repetition leaves data in the Infinity Cache) and as single "
+                    "launches after a cache flush (cold, medians; these carry the events' "
+                    "own few microseconds)"}
 
 
 DECODE_BATCH = 16  # sequences decoded together
