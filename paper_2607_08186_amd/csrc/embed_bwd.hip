@@ -253,7 +253,13 @@ constexpr int kRankChunks = 16;  // key chunks per token, one thread each
 // workgroup of 256 threads places 16 tokens: thread (c, i) counts over every 16th key
 // from c (all M keys staged in LDS) for token i, and the 16 counts of a token are
 // added in LDS, so the M x M comparisons spread over M / 16 workgroups (every CU at
-// the 36-layer step's 4096 tokens).
+// the 36-layer step's 4096 tokens).  PACKED (V < 2^18, so that every key, V included,
+// fits 18 bits; vocabularies under 262144): LDS holds key << 14 | j, all distinct, and
+// the order above is a single unsigned comparison of those words.
+constexpr int kRankIndexBits = 14;  // token indices below kSmallSortMax = 2^14
+static_assert((1 << kRankIndexBits) == kSmallSortMax, "packed keys carry the token index");
+
+template <bool PACKED>
 __global__ __launch_bounds__(kRankTokens * kRankChunks) void rank_sort_kernel(
     const int32_t *__restrict__ ids, int M, int64_t V, uint32_t *__restrict__ keys_out,
     int32_t *__restrict__ vals_out)
@@ -272,7 +278,10 @@ __global__ __launch_bounds__(kRankTokens * kRankChunks) void rank_sort_kernel(
 #pragma unroll
     for (int f = 0; f < kFill; ++f) {
         const int j = f * kRankTokens * kRankChunks + threadIdx.x;
-        if (j < M) sk[j] = fid[f] >= 0 && (int64_t)fid[f] < V ? (uint32_t)fid[f] : (uint32_t)V;
+        if (j < M) {
+            const uint32_t key = fid[f] >= 0 && (int64_t)fid[f] < V ? (uint32_t)fid[f] : (uint32_t)V;
+            sk[j] = PACKED ? key << kRankIndexBits | (uint32_t)j : key;
+        }
     }
     __syncthreads();
     const int t = threadIdx.x % kRankTokens, c = threadIdx.x / kRankTokens;
@@ -284,7 +293,10 @@ __global__ __launch_bounds__(kRankTokens * kRankChunks) void rank_sort_kernel(
 #pragma unroll 8
     for (int j = c; j < M; j += kRankChunks) {
         const uint32_t kj = sk[j];
-        n += (kj < ki || (kj == ki && j < i)) ? 1 : 0;
+        if constexpr (PACKED)
+            n += kj < ki ? 1 : 0;
+        else
+            n += (kj < ki || (kj == ki && j < i)) ? 1 : 0;
     }
     cnt[c][t] = n;
     __syncthreads();
@@ -292,7 +304,7 @@ __global__ __launch_bounds__(kRankTokens * kRankChunks) void rank_sort_kernel(
         int r = 0;
 #pragma unroll
         for (int cc = 0; cc < kRankChunks; ++cc) r += cnt[cc][t];
-        keys_out[r] = ki;
+        keys_out[r] = PACKED ? ki >> kRankIndexBits : ki;
         vals_out[r] = i;
     }
 }
@@ -546,8 +558,11 @@ hipError_t launch_embed_bwd(const int32_t *ids, const void *dout, int B, int L, 
     const uint32_t *kin = nullptr;
     const int32_t *vin = nullptr;
     if (M <= kSmallSortMax) {
-        rank_sort_kernel<<<(M + kRankTokens - 1) / kRankTokens, kRankTokens * kRankChunks, 0, s>>>(
-            ids, M, V, ka, va);
+        const unsigned nb = (M + kRankTokens - 1) / kRankTokens;
+        if (V < ((int64_t)1 << (32 - kRankIndexBits)))
+            rank_sort_kernel<true><<<nb, kRankTokens * kRankChunks, 0, s>>>(ids, M, V, ka, va);
+        else
+            rank_sort_kernel<false><<<nb, kRankTokens * kRankChunks, 0, s>>>(ids, M, V, ka, va);
         small_segments_kernel<<<1, kRankWaves * 64, 0, s>>>(ka, M, V, seg_start, uniq, num_uniq);
         kin = ka;
         vin = va;
