@@ -92,6 +92,20 @@ def test_expand_bwd_out_of_range_ids_are_dropped():
     _check(ids, _dout(seed + 1, B, n * L, Dm, "bf16"), V)
 
 
+@pytest.mark.parametrize("V", [(1 << 18) - 1, 1 << 18])
+def test_expand_bwd_sort_key_packing_boundary(V):
+    """The counting sort packs (id, token) into one 32-bit word while every key fits 18
+    bits (V < 2^18, the out-of-range marker V included) and compares the two parts
+    otherwise: ids near the top of [0, V), repeats and out-of-range ids on both sides of
+    that boundary."""
+    B, L, n, Dm = 2, 1500, 2, 16
+    seed = synth.seed_for("expand_bwd_pack", V)
+    ids = synth.token_ids(seed, B, L, 64) + (V - 48)  # 48 in range at the top, 16 at or past V
+    ids[0, :7] = -1
+    assert np.any(ids >= V) and np.any(ids == V - 1) and np.any(ids < 0)
+    _check(ids, _dout(seed + 1, B, n * L, Dm, "bf16"), V)
+
+
 def test_expand_bwd_all_ids_equal_and_all_bad():
     B, L, n, Dm = 1, 3000, 2, 32
     seed = synth.seed_for("expand_bwd_same")
